@@ -1,0 +1,339 @@
+"""Oracle: a plain, slow CPU implementation of the DominoTree draft-tree builder.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import or call
+this module; only the tests, the smoke check and the benchmark's CPU-baseline
+leg use it.  It shares no code with the HIP library.
+
+Everything is computed in float64 from the exact stored input values (bf16
+and fp32 widen to float64 exactly).  The code follows the paper's text in its
+own order:
+
+* Domino's causal encoder is a single-layer GRU over the embeddings of the
+  tokens realised along the path (section 2.3); the gate equations are the
+  PyTorch GRUCell ones (gates r, z, n) because the paper does not print them.
+* The correction is the linear head q = W_c S + b_c dotted with the candidate
+  embedding rows, delta(v) = E[v] . q, restricted to the depth's top-M slice
+  (section 3.2, candidate restriction).
+* Children(S, d) scores the slice with the corrected logits, normalises them,
+  keeps the top-k and advances the GRU once per kept child (Alg. 1, step 2).
+* The tree is grown by a max-heap keyed by cumulative log-probability, popped
+  until the budget is spent (Alg. 1, steps 3-4; DDTree heap, section 2.4).
+* Emission orders nodes so parents precede children and builds the
+  ancestor-only verification mask (section 3.5; Appendix B, frontier selection).
+
+Readings of the paper that this file fixes (the paper is silent on them):
+
+* Normalisation (TAIL, default): logZ = LSE(corrected slice logits, R_d) where
+  R_d is the log-sum-exp of the *uncorrected* logits outside the slice, so a
+  zeroed correction gives exactly the full-vocabulary marginal log-probs.
+  SLICE normalises over the slice only.
+* Temperature: tau = T if T > 0 else 1; logits are divided by tau before the
+  log-softmax; the top-M selection uses the raw logits.
+* Ties: top-M by (logit desc, token id asc); children by (log-prob desc,
+  slot asc); heap by (g desc, insertion id asc), children inserted in rank order.
+* k (children per expansion) = min(M, B) unless max_children > 0, then
+  min(max_children, M).
+* Dead slots (logit == -inf) are never returned as children.  A tree whose
+  logits hold NaN or +inf gets status NONFINITE and no nodes.
+* Padding rows: token -1, parent -1, depth 0, position pos_offset,
+  score -inf, all-zero mask row.
+
+Pins: see tests/test_oracle_*.py (library routines, brute force, closed forms,
+the greedy chain, the factorised tree, a frontier builder, a hand-derived
+golden tree).  Absolute score values at the full workload sizes beyond those
+pins are "parity unpinned": the paper prints no worked example.
+"""
+from __future__ import annotations
+
+import heapq
+import math
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+NORM_TAIL = 0
+NORM_SLICE = 1
+TREE_NONFINITE = 0x1
+
+DT_F32 = 0
+DT_BF16 = 1
+
+
+# ---------------------------------------------------------------------------
+# input decoding
+# ---------------------------------------------------------------------------
+
+def widen(a: np.ndarray, dtype: int) -> np.ndarray:
+    """Stored tensor -> float64.  bf16 arrives as uint16 bit patterns."""
+    if a is None:
+        return None
+    if dtype == DT_BF16:
+        u = np.asarray(a, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return u.view(np.float32).astype(np.float64)
+    return np.asarray(a, dtype=np.float32).astype(np.float64)
+
+
+def effective_temperature(T: float) -> float:
+    """tau = T for T > 0; T = 0 (deterministic drafting) scores with tau = 1."""
+    return float(T) if T > 0 else 1.0
+
+
+def logsumexp(a: np.ndarray) -> float:
+    """log sum exp of a 1-D float64 array; -inf for an empty or all -inf array."""
+    if a.size == 0:
+        return -math.inf
+    m = float(np.max(a))
+    if m == -math.inf:
+        return -math.inf
+    return m + math.log(float(np.sum(np.exp(a - m))))
+
+
+# ---------------------------------------------------------------------------
+# Alg. 1 step 1: per-depth marginal top-M (candidate restriction, section 3.2)
+# ---------------------------------------------------------------------------
+
+def scan_row(x: np.ndarray, M: int, tau: float):
+    """Top-M token ids of one depth's marginal logits and the tail log-sum-exp.
+
+    Returns (ids[M] int64 ordered by (logit desc, id asc), logits[M] float64,
+    R) where R = log sum_{v not in ids} exp(x[v] / tau) (-inf if empty).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    order = np.argsort(-x, kind="stable")      # stable: equal logits keep id order
+    ids = order[:M].astype(np.int64)
+    tail = np.ones(x.shape[0], dtype=bool)
+    tail[ids] = False
+    R = logsumexp(x[tail] / tau)
+    return ids, x[ids], R
+
+
+# ---------------------------------------------------------------------------
+# Domino's causal encoder (section 2.3), PyTorch GRUCell convention
+# ---------------------------------------------------------------------------
+
+def sigmoid(a: np.ndarray) -> np.ndarray:
+    return 1.0 / (1.0 + np.exp(-a))
+
+
+def gru_cell(h: np.ndarray, xs: np.ndarray, w_ih, w_hh, b_ih, b_hh) -> np.ndarray:
+    """Advance state h [d_h] by each input row of xs [k, d_in]; returns [k, d_h].
+
+    r = sigmoid(W_ir x + b_ir + W_hr h + b_hr)
+    z = sigmoid(W_iz x + b_iz + W_hz h + b_hz)
+    n = tanh(W_in x + b_in + r * (W_hn h + b_hn))
+    h' = (1 - z) * n + z * h
+    """
+    d_h = h.shape[0]
+    gi = xs @ w_ih.T                      # [k, 3 d_h]
+    if b_ih is not None:
+        gi = gi + b_ih
+    gh = w_hh @ h                         # [3 d_h]
+    if b_hh is not None:
+        gh = gh + b_hh
+    i_r, i_z, i_n = gi[:, :d_h], gi[:, d_h:2 * d_h], gi[:, 2 * d_h:]
+    h_r, h_z, h_n = gh[:d_h], gh[d_h:2 * d_h], gh[2 * d_h:]
+    r = sigmoid(i_r + h_r)
+    z = sigmoid(i_z + h_z)
+    n = np.tanh(i_n + r * h_n)
+    return (1.0 - z) * n + z * h
+
+
+# ---------------------------------------------------------------------------
+# the builder
+# ---------------------------------------------------------------------------
+
+class _Model:
+    """float64 copies of the weights plus the per-depth candidate tables."""
+
+    def __init__(self, X, emb, emb_dtype, w, M, tau, norm_mode):
+        self.L = X.shape[0]
+        self.M = M
+        self.tau = tau
+        self.norm_mode = norm_mode
+        self.w_ih = widen(w["w_ih"], w["dtype"])
+        self.w_hh = widen(w["w_hh"], w["dtype"])
+        self.b_ih = widen(w.get("b_ih"), w["dtype"])
+        self.b_hh = widen(w.get("b_hh"), w["dtype"])
+        self.w_c = widen(w["w_c"], w["dtype"])
+        self.b_c = widen(w.get("b_c"), w["dtype"])
+        # Alg. 1 step 1, once per depth: top-M ids, their logits, their embeddings
+        self.cand, self.xc, self.R, self.Ec = [], [], [], []
+        for d in range(self.L):
+            ids, xs, R = scan_row(X[d], M, tau)
+            self.cand.append(ids)
+            self.xc.append(xs)
+            self.R.append(R)
+            self.Ec.append(widen(np.asarray(emb)[ids], emb_dtype))
+
+    def slot_logprobs(self, S: np.ndarray, d: int):
+        """Corrected, normalised log-probs of depth d's slice given path state S.
+
+        delta_m = E[cand_d[m]] . (W_c S + b_c);  z = (x + delta) / tau;
+        ell = z - logZ.  Returns (ell[M] with -inf for dead slots, live mask).
+        """
+        q = self.w_c @ S
+        if self.b_c is not None:
+            q = q + self.b_c
+        delta = self.Ec[d - 1] @ q
+        x = self.xc[d - 1]
+        live = x > -math.inf
+        z = np.full(self.M, -math.inf)
+        z[live] = (x[live] + delta[live]) / self.tau
+        if self.norm_mode == NORM_SLICE:
+            logZ = logsumexp(z[live])
+        else:
+            logZ = logsumexp(np.append(z[live], self.R[d - 1]))
+        ell = np.full(self.M, -math.inf)
+        ell[live] = z[live] - logZ
+        return ell, live
+
+    def children(self, S: np.ndarray, d: int, k: int, gaps: list):
+        """Children(S_{d-1}, d) of Alg. 1 step 2: top-k (token, ell, slot, child state)."""
+        ell, live = self.slot_logprobs(S, d)
+        slots = [m for m in range(self.M) if live[m]]
+        slots.sort(key=lambda m: (-ell[m], m))
+        if len(slots) > k:
+            gaps.append(ell[slots[k - 1]] - ell[slots[k]])
+        kept = slots[:k]
+        if not kept:
+            return []
+        tokens = [int(self.cand[d - 1][m]) for m in kept]
+        states = gru_cell(S, self.Ec[d - 1][kept], self.w_ih, self.w_hh, self.b_ih, self.b_hh)
+        return [(tokens[i], float(ell[m]), m, states[i]) for i, m in enumerate(kept)]
+
+
+def _empty_tree(B: int, pos_offset: int, status: int):
+    return {
+        "tokens": np.full(B, -1, np.int32),
+        "parents": np.full(B, -1, np.int32),
+        "depth": np.zeros(B, np.int32),
+        "position_ids": np.full(B, pos_offset, np.int32),
+        "mask": np.zeros((B, B), np.uint8),
+        "scores": np.full(B, -np.inf, np.float64),
+        "slots": np.full(B, -1, np.int32),
+        "n_nodes": 0,
+        "status": status,
+        "min_gap": math.inf,
+    }
+
+
+def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
+               h0: Optional[np.ndarray], M: int, B: int, T: float,
+               max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
+               logits_dtype: int = DT_F32):
+    """Build one draft tree (Alg. 1) and emit it in pop order.
+
+    X: [L, V] stored marginal logits of one tree; emb: [V, d_e]; weights: dict
+    with w_ih, w_hh, b_ih, b_hh, w_c, b_c, dtype; h0: [d_h] or None (zeros).
+    Returns a dict of emitted arrays plus the smallest decisive score gap.
+    """
+    Xd = widen(X, logits_dtype)
+    if np.any(np.isnan(Xd)) or np.any(Xd == math.inf):
+        return _empty_tree(B, pos_offset, TREE_NONFINITE)
+    tau = effective_temperature(T)
+    k = min(M, B) if max_children <= 0 else min(max_children, M)
+    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode)
+    L = model.L
+    d_h = model.w_hh.shape[1]
+    S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
+
+    gaps: List[float] = []
+    heap = []          # entries (-g, insertion id, payload)
+    next_id = 0
+    # Alg. 1 step 3: the root's children
+    for tok, ell, m, S in model.children(S0, 1, k, gaps):
+        heapq.heappush(heap, (-ell, next_id, (tok, ell, m, S, 1, -1)))
+        next_id += 1
+    # Alg. 1 step 4: pop the best entry, add it to the tree, push its children
+    tree = []          # (token, g, slot, depth, parent pop index)
+    while len(tree) < B and heap:
+        neg_g, _, (tok, g, m, S, d, parent) = heapq.heappop(heap)
+        i = len(tree)
+        tree.append((tok, g, m, d, parent))
+        if d < L:
+            for ctok, ell, cm, cS in model.children(S, d + 1, k, gaps):
+                heapq.heappush(heap, (-(g + ell), next_id, (ctok, g + ell, cm, cS, d + 1, i)))
+                next_id += 1
+    # decisive gaps: consecutive pops and the last pop vs the best entry left out
+    for i in range(len(tree) - 1):
+        gaps.append(tree[i][1] - tree[i + 1][1])
+    if len(tree) == B and heap:
+        gaps.append(tree[-1][1] - (-heap[0][0]))
+    return _emit(tree, B, pos_offset, min(gaps) if gaps else math.inf)
+
+
+def _emit(tree, B: int, pos_offset: int, min_gap: float):
+    """Pop-order arrays and the ancestor-or-self mask (section 3.5)."""
+    out = _empty_tree(B, pos_offset, 0)
+    n = len(tree)
+    for i, (tok, g, m, d, parent) in enumerate(tree):
+        out["tokens"][i] = tok
+        out["parents"][i] = parent
+        out["depth"][i] = d
+        out["position_ids"][i] = pos_offset + d
+        out["scores"][i] = g
+        out["slots"][i] = m
+        out["mask"][i, i] = 1
+        if parent >= 0:
+            out["mask"][i] |= out["mask"][parent]
+    out["n_nodes"] = n
+    out["min_gap"] = min_gap
+    return out
+
+
+def build_trees(logits: np.ndarray, logits_dtype: int, emb: np.ndarray, emb_dtype: int,
+                weights: dict, h0: Optional[np.ndarray], M: int, B: int, T: float,
+                max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
+                trees: Optional[Sequence[int]] = None):
+    """build_tree over the batch (or the listed tree indices)."""
+    idx = range(logits.shape[0]) if trees is None else trees
+    return [build_tree(logits[t], emb, emb_dtype, weights, None if h0 is None else h0[t],
+                       M, B, T, max_children, norm_mode, pos_offset, logits_dtype) for t in idx]
+
+
+def scan(logits: np.ndarray, logits_dtype: int, M: int, T: float):
+    """Alg. 1 step 1 for every row of a [rows, V] array: (ids, logits, R)."""
+    X = widen(logits, logits_dtype)
+    tau = effective_temperature(T)
+    ids = np.zeros((X.shape[0], M), np.int64)
+    xs = np.zeros((X.shape[0], M))
+    R = np.zeros(X.shape[0])
+    for r in range(X.shape[0]):
+        ids[r], xs[r], R[r] = scan_row(X[r], M, tau)
+    return ids, xs, R
+
+
+def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
+                h0: Optional[np.ndarray], M: int, B: int, T: float, tokens, parents, n_nodes: int,
+                max_children: int = 0, norm_mode: int = NORM_TAIL, logits_dtype: int = DT_F32):
+    """Re-score a given tree with the oracle's Children function.
+
+    Returns (g[n], valid): valid is False when a node's token is not among the
+    top-k children of its parent's path (or a parent index is not earlier).
+    """
+    Xd = widen(X, logits_dtype)
+    tau = effective_temperature(T)
+    k = min(M, B) if max_children <= 0 else min(max_children, M)
+    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode)
+    d_h = model.w_hh.shape[1]
+    S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
+    g = np.zeros(n_nodes)
+    state = [None] * n_nodes
+    depth = [0] * n_nodes
+    valid = True
+    for i in range(n_nodes):
+        p = int(parents[i])
+        if p >= i:
+            return g, False
+        S, gp, d = (S0, 0.0, 1) if p < 0 else (state[p], g[p], depth[p] + 1)
+        if d > model.L:
+            return g, False
+        kids = model.children(S, d, k, [])
+        match = [c for c in kids if c[0] == int(tokens[i])]
+        if not match:
+            return g, False
+        _, ell, _, cS = match[0]
+        g[i] = gp + ell
+        state[i] = cS
+        depth[i] = d
+    return g, valid

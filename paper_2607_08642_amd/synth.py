@@ -1,0 +1,229 @@
+"""Seeded synthetic workloads for the DominoTree draft-tree builder.
+
+This module only draws random inputs.  It holds none of the builder's
+arithmetic, so both the HIP path and the CPU oracle may consume what it
+produces; each side receives identical bytes.
+
+Workloads (names follow the drafter each one is shaped like):
+
+* ``tiny``      -- L=4, V=1024, M=8, B=8, T=0, fp32 everything, GRU d_in=d_h=64
+                   with biases, head d_h->64.
+* ``qwen3_4b``  -- L=16, V=151936, M=64, B=16, T=0, bf16, d_e=2560, d_h=512.
+* ``qwen3_8b``  -- as above with d_e=4096 and T=1.0.
+* ``budget64``  -- Qwen3-8B shapes, B=64, T=0, flattened spikes (wide trees).
+* ``concurrent``-- 32 independent trees of the Qwen3-8B shape, T=0.7, per-tree
+                   h0 ~ N(0, 0.1^2).
+
+The vocabulary (151936) is Qwen3's; the block length 16 matches the b16
+drafters (paper, section 4.1).  Marginal logits are 2*N(0,1) with a few
+planted spikes per position, standing in for a drafter's per-position
+marginals on real prompts (the paper's datasets are not used).
+
+Generation is deterministic: every tensor is drawn from NumPy's PCG64 seeded
+with ``SeedSequence([seed, tag, block])``; large tables are drawn in fixed
+row blocks so a thread pool can fill them without changing the bytes.
+bf16 tensors are produced as ``uint16`` bit patterns, rounded from fp32 to
+nearest-even.
+"""
+from __future__ import annotations
+
+import dataclasses
+from concurrent.futures import ThreadPoolExecutor
+from typing import Optional
+
+import numpy as np
+
+QWEN3_VOCAB = 151936
+
+# tensor tags for SeedSequence
+TAG_LOGITS, TAG_EMB, TAG_WIH, TAG_WHH, TAG_BIH, TAG_BHH, TAG_WC, TAG_BC, TAG_H0, TAG_SPIKE = range(10)
+
+DT_F32 = 0
+DT_BF16 = 1
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round fp32 to bf16 (round-to-nearest-even) and return the uint16 bits."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    out = r.astype(np.uint16)
+    nan = np.isnan(a)
+    if nan.any():
+        out[nan] = np.uint16(0x7FC0)
+    return out
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Widen bf16 bit patterns to fp32 (exact)."""
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _rng(*key: int) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([int(k) for k in key]))
+
+
+def _as_dtype(a32: np.ndarray, dtype: int) -> np.ndarray:
+    return f32_to_bf16_bits(a32) if dtype == DT_BF16 else np.ascontiguousarray(a32, np.float32)
+
+
+def _table(seed: int, tag: int, rows: int, cols: int, kind: str, scale: float, dtype: int,
+           rows_per_block: int = 2048, threads: int = 8) -> np.ndarray:
+    """Draw a [rows, cols] table in fixed row blocks (thread count does not change the bytes)."""
+    out = np.empty((rows, cols), dtype=np.uint16 if dtype == DT_BF16 else np.float32)
+    nblk = (rows + rows_per_block - 1) // rows_per_block
+
+    def fill(i: int) -> None:
+        r0 = i * rows_per_block
+        r1 = min(rows, r0 + rows_per_block)
+        g = _rng(seed, tag, i)
+        n = (r1 - r0) * cols
+        if kind == "normal":
+            a = g.standard_normal(n, dtype=np.float32)
+            a *= np.float32(scale)
+        else:  # symmetric uniform on (-scale, scale)
+            a = g.random(n, dtype=np.float32)
+            a = (a * np.float32(2.0) - np.float32(1.0)) * np.float32(scale)
+        out[r0:r1] = _as_dtype(a, dtype).reshape(r1 - r0, cols)
+
+    if nblk == 1:
+        fill(0)
+    else:
+        with ThreadPoolExecutor(min(threads, nblk)) as ex:
+            list(ex.map(fill, range(nblk)))
+    return out
+
+
+def peaked_logits(seed: int, tree: int, L: int, V: int, dtype: int, n_lo: int, n_hi: int,
+                  spike_lo: float, spike_hi: float, fixed_spike: Optional[float] = None) -> np.ndarray:
+    """[L, V] marginal logits: 2*N(0,1) plus spikes on n ~ U{n_lo..n_hi} distinct tokens per row."""
+    g = _rng(seed, TAG_LOGITS, tree)
+    x = g.standard_normal((L, V), dtype=np.float32) * np.float32(2.0)
+    gs = _rng(seed, TAG_SPIKE, tree)
+    for r in range(L):
+        n = int(gs.integers(n_lo, n_hi + 1))
+        toks = gs.choice(V, size=n, replace=False)
+        if fixed_spike is not None:
+            x[r, toks] += np.float32(fixed_spike)
+        else:
+            x[r, toks] += gs.uniform(spike_lo, spike_hi, size=n).astype(np.float32)
+    return _as_dtype(x, dtype)
+
+
+@dataclasses.dataclass
+class Weights:
+    """Model-side tensors (device-independent host arrays)."""
+    emb: np.ndarray          # [V, d_e]
+    w_ih: np.ndarray         # [3*d_h, d_e]  (PyTorch GRUCell layout, gates r,z,n)
+    w_hh: np.ndarray         # [3*d_h, d_h]
+    b_ih: Optional[np.ndarray]   # [3*d_h] or None
+    b_hh: Optional[np.ndarray]   # [3*d_h] or None
+    w_c: np.ndarray          # [d_e, d_h]    (Linear(d_h -> d_e).weight)
+    b_c: Optional[np.ndarray]    # [d_e] or None
+    dtype: int               # DT_F32 or DT_BF16 for every tensor above
+    V: int
+    d_e: int
+    d_h: int
+
+
+@dataclasses.dataclass
+class Workload:
+    name: str
+    logits: np.ndarray       # [b, L, V]
+    logits_dtype: int
+    h0: Optional[np.ndarray] # [b, d_h] fp32 or None (zeros)
+    weights: Weights
+    L: int
+    M: int
+    B: int
+    T: float
+    batch: int
+
+
+def make_weights(seed: int, V: int, d_e: int, d_h: int, dtype: int, gru_bias: bool,
+                 head_bias: bool, emb_std: float, w_scale: float, threads: int = 8) -> Weights:
+    emb = _table(seed, TAG_EMB, V, d_e, "normal", emb_std, dtype, threads=threads)
+    w_ih = _table(seed, TAG_WIH, 3 * d_h, d_e, "uniform", w_scale, dtype, threads=threads)
+    w_hh = _table(seed, TAG_WHH, 3 * d_h, d_h, "uniform", w_scale, dtype, threads=threads)
+    w_c = _table(seed, TAG_WC, d_e, d_h, "uniform", w_scale, dtype, threads=threads)
+    b_ih = _table(seed, TAG_BIH, 1, 3 * d_h, "uniform", w_scale, dtype)[0] if gru_bias else None
+    b_hh = _table(seed, TAG_BHH, 1, 3 * d_h, "uniform", w_scale, dtype)[0] if gru_bias else None
+    b_c = _table(seed, TAG_BC, 1, d_e, "uniform", w_scale, dtype)[0] if head_bias else None
+    return Weights(emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c, dtype, V, d_e, d_h)
+
+
+_WEIGHT_CACHE: dict = {}
+
+
+def qwen_weights(d_e: int, seed: int, threads: int = 8) -> Weights:
+    key = (d_e, seed)
+    if key not in _WEIGHT_CACHE:
+        _WEIGHT_CACHE[key] = make_weights(seed, QWEN3_VOCAB, d_e, 512, DT_BF16, gru_bias=False,
+                                          head_bias=True, emb_std=0.02,
+                                          w_scale=1.0 / np.sqrt(512.0), threads=threads)
+    return _WEIGHT_CACHE[key]
+
+
+def tiny(seed: int = 0) -> Workload:
+    L, V, M, B = 4, 1024, 8, 8
+    w = make_weights(seed, V, 64, 64, DT_F32, gru_bias=True, head_bias=True, emb_std=0.02,
+                     w_scale=1.0 / 8.0)
+    x = peaked_logits(seed, 0, L, V, DT_F32, 3, 3, 0.0, 0.0, fixed_spike=10.0)[None]
+    return Workload("tiny", x, DT_F32, None, w, L, M, B, 0.0, 1)
+
+
+def qwen3_4b() -> Workload:
+    w = qwen_weights(2560, 1)
+    x = peaked_logits(1, 0, 16, QWEN3_VOCAB, DT_BF16, 1, 4, 6.0, 12.0)[None]
+    return Workload("qwen3_4b", x, DT_BF16, None, w, 16, 64, 16, 0.0, 1)
+
+
+def qwen3_8b() -> Workload:
+    w = qwen_weights(4096, 2)
+    x = peaked_logits(2, 0, 16, QWEN3_VOCAB, DT_BF16, 1, 4, 6.0, 12.0)[None]
+    return Workload("qwen3_8b", x, DT_BF16, None, w, 16, 64, 16, 1.0, 1)
+
+
+def budget64() -> Workload:
+    w = qwen_weights(4096, 2)
+    x = peaked_logits(3, 0, 16, QWEN3_VOCAB, DT_BF16, 4, 16, 3.0, 6.0)[None]
+    return Workload("budget64", x, DT_BF16, None, w, 16, 64, 64, 0.0, 1)
+
+
+def concurrent(batch: int = 32) -> Workload:
+    w = qwen_weights(4096, 2)
+    x = np.stack([peaked_logits(4, t, 16, QWEN3_VOCAB, DT_BF16, 1, 4, 6.0, 12.0)
+                  for t in range(batch)])
+    h0 = np.stack([_rng(4, TAG_H0, 1000 + t).standard_normal(512, dtype=np.float32)
+                   * np.float32(0.1) for t in range(batch)])
+    return Workload("concurrent", x, DT_BF16, h0, w, 16, 64, 16, 0.7, batch)
+
+
+WORKLOADS = {
+    "tiny": tiny,
+    "qwen3_4b": qwen3_4b,
+    "qwen3_8b": qwen3_8b,
+    "budget64": budget64,
+    "concurrent": concurrent,
+}
+
+
+def random_small(seed: int, *, batch: int, L: int, V: int, M: int, B: int, T: float,
+                 d_e: int, d_h: int, dtype: int = DT_F32, logits_dtype: Optional[int] = None,
+                 gru_bias: bool = True, head_bias: bool = True, h0: bool = False,
+                 emb_std: float = 0.5, w_scale: float = 0.5, logit_scale: float = 2.0,
+                 spikes: int = 2, spike: float = 4.0) -> Workload:
+    """Small random workload for parity sweeps (large corrections so paths really differ)."""
+    w = make_weights(seed, V, d_e, d_h, dtype, gru_bias, head_bias, emb_std, w_scale)
+    ldt = dtype if logits_dtype is None else logits_dtype
+    g = _rng(seed, TAG_LOGITS, 99)
+    x = g.standard_normal((batch, L, V), dtype=np.float32) * np.float32(logit_scale)
+    for t in range(batch):
+        for r in range(L):
+            toks = g.choice(V, size=min(spikes, V), replace=False)
+            x[t, r, toks] += np.float32(spike) * g.random(len(toks), dtype=np.float32)
+    hh = None
+    if h0:
+        hh = _rng(seed, TAG_H0, 0).standard_normal((batch, d_h), dtype=np.float32) * np.float32(0.5)
+    return Workload(f"random{seed}", _as_dtype(x, ldt), ldt, hh, w, L, M, B, T, batch)
