@@ -1,0 +1,175 @@
+/*
+ * dominotree.h -- C ABI of the MI355X (gfx950) DominoTree draft-tree builder.
+ *
+ * The library builds the conditional best-first draft tree of DominoTree
+ * (arXiv 2607.08642, section 3, Algorithm 1) on one GPU:
+ *
+ *   S1  per depth, the top-M marginal candidates and the tail log-sum-exp
+ *       (Alg. 1 step 1; section 3.2, candidate restriction);
+ *   S2  the candidate embedding rows folded through the GRU input projection
+ *       and the correction head (section 3.2: gather the M rows once per depth);
+ *   S3  the root's children (Alg. 1 steps 2-3);
+ *   S4  best-first expansion: pop, advance the GRU along the node's own path,
+ *       score the next depth's slice with the path-dependent correction, push
+ *       the top-k children (Alg. 1 step 4; Domino's correction, section 2.3);
+ *   S5  emission of the tree in pop order with parent pointers, depths,
+ *       position ids and the ancestor-only verification mask (section 3.5).
+ *
+ * Scoring of a node at depth d whose parent path has GRU state S (Fact B):
+ *   delta_m = E[cand_d[m]] . (W_c S + b_c)          (correction head)
+ *   z_m     = (x_d[m] + delta_m) / tau,  tau = T if T > 0 else 1
+ *   logZ    = LSE_m(z_m) (SLICE)  or  LSE(LSE_m(z_m), R_d) (TAIL, default)
+ *   ell_m   = z_m - logZ,  R_d = log sum_{v not in slice} exp(x_d[v] / tau)
+ * The GRU follows PyTorch's GRUCell (gates r, z, n; W_ih = [W_ir; W_iz; W_in]).
+ *
+ * Ties: top-M by (logit desc, token id asc); children by (log-prob desc,
+ * slot asc); pops by (score desc, insertion order asc).
+ *
+ * Conventions for every call:
+ *   - all tensor arguments are DEVICE pointers (hipMalloc / torch CUDA tensors),
+ *     row-major and contiguous, owned by the caller; the library never frees
+ *     caller memory;
+ *   - `stream` is a hipStream_t (NULL = the default stream); every call is
+ *     stream-ordered and asynchronous: no host synchronisation happens inside
+ *     dt_build_tree / dt_scan_topm, results are valid once the stream completes;
+ *   - argument errors are detected on the host before any launch: a negative
+ *     dt_status is returned and nothing is written; dt_last_error() gives a
+ *     thread-local message;
+ *   - data errors are per-tree status bits written on the device
+ *     (DT_TREE_NONFINITE: a NaN or +inf logit; that tree gets n_nodes = 0);
+ *   - no C++ exception crosses this interface.
+ *
+ * Envelope: 1 <= M <= min(V, 256); 1 <= B <= 256; 1 <= L <= 64;
+ * 32 <= d_h <= 1024 with d_h % 32 == 0; 1 <= d_e <= 8192; 1 <= V < 2^31.
+ */
+#ifndef DOMINOTREE_H
+#define DOMINOTREE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DT_ABI_VERSION 1
+
+typedef enum { DT_F32 = 0, DT_BF16 = 1 } dt_dtype;
+
+typedef enum {
+  DT_OK = 0,
+  DT_ERR_NULL = -1,        /* a required pointer is NULL */
+  DT_ERR_SHAPE = -2,       /* a size is out of range or inconsistent */
+  DT_ERR_DTYPE = -3,       /* unknown dtype code */
+  DT_ERR_UNSUPPORTED = -4, /* outside the envelope above */
+  DT_ERR_WORKSPACE = -5,   /* workspace missing or smaller than dt_workspace_size */
+  DT_ERR_ALIGN = -6,       /* a pointer is not aligned as required */
+  DT_ERR_HIP = -7          /* a HIP runtime call failed (see dt_last_error) */
+} dt_status;
+
+/* per-tree status bits, written to dt_tree.status[b] */
+#define DT_TREE_NONFINITE 0x1 /* a NaN or +inf logit: the tree has no nodes */
+#define DT_TREE_TRUNCATED 0x2 /* a capacity limit of the expansion was reached; only
+                                 hundreds of exactly tied scores can cause it.  The tree
+                                 is still a valid best-first tree but exact ties may be
+                                 resolved differently from insertion order. */
+
+/* normalisation of the corrected slice (dt_options.norm_mode) */
+#define DT_NORM_TAIL 0  /* logZ includes the uncorrected out-of-slice mass R_d */
+#define DT_NORM_SLICE 1 /* logZ over the top-M slice only */
+
+/* GRU of Domino's causal encoder (section 2.3), PyTorch GRUCell layout.
+ * w_ih: [3*d_h, d_in] with d_in = the embedding width d_e; w_hh: [3*d_h, d_h];
+ * b_ih, b_hh: [3*d_h] or NULL (treated as zeros).  dtype = the plan's
+ * weights dtype. */
+typedef struct {
+  const void *w_ih, *w_hh, *b_ih, *b_hh;
+  int d_in, d_h;
+} dt_gru;
+
+/* Correction head: q = w S + b with w: [d_e, d_h] (a Linear(d_h -> d_e)
+ * weight), b: [d_e] or NULL.  delta(v) = E[v] . q. */
+typedef struct {
+  const void *w, *b;
+} dt_head;
+
+typedef struct {
+  int max_children; /* k, children kept per expansion; 0 -> min(M, B).
+                       The paper's headline setting is 8 (section 4.1). */
+  int norm_mode;    /* DT_NORM_TAIL (default) or DT_NORM_SLICE */
+  int pos_offset;   /* position_ids = pos_offset + depth */
+  int reserved;     /* must be 0 */
+} dt_options;
+
+/* Output tree of every batch entry b (device pointers, caller-owned).
+ * Nodes are in pop order, so a parent always precedes its children. */
+typedef struct {
+  int32_t *tokens;       /* [batch, B] token id; -1 in padding rows */
+  int32_t *parents;      /* [batch, B] pop index of the parent; -1 = child of the root */
+  int32_t *depth;        /* [batch, B] 1..L; 0 in padding rows */
+  int32_t *position_ids; /* [batch, B] pos_offset + depth */
+  uint8_t *mask;         /* [batch, B, B] mask[i][j] = 1 iff j is i or an ancestor of i */
+  float *scores;         /* [batch, B] cumulative log-prob g; -inf in padding rows */
+  int32_t *n_nodes;      /* [batch] nodes emitted (<= B) */
+  int32_t *status;       /* [batch] DT_TREE_* bits */
+} dt_tree;
+
+typedef struct dt_plan dt_plan;
+
+/* ABI version of the loaded library (DT_ABI_VERSION when it matches this header). */
+int dt_abi_version(void);
+
+/* Static text for a dt_status code. */
+const char *dt_status_string(int status);
+
+/* Thread-local detail of the last error returned on this host thread. */
+const char *dt_last_error(void);
+
+/* Create a plan for one model and one (L, M, B) shape.
+ *   emb:  [V, d_e] token-embedding table (caller-owned, must outlive the plan);
+ *   gru, head: the Domino encoder and correction head (copied and repacked
+ *         into plan-owned device memory; the caller may free them afterwards);
+ *   weights_dtype: dtype of emb, GRU and head tensors;
+ *   logits_dtype: dtype of the marginal logits passed to dt_build_tree;
+ *   max_batch: the largest batch dt_build_tree will be called with;
+ *   opts: NULL for defaults.
+ * Runs packing kernels on the default stream and waits for them.  On success
+ * *plan is set; on failure *plan is NULL. */
+dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const dt_gru *gru,
+                         const dt_head *head, int weights_dtype, int L, int M, int B,
+                         int logits_dtype, int max_batch, const dt_options *opts);
+
+/* Device workspace (bytes) dt_build_tree needs for `batch` trees. */
+dt_status dt_workspace_size(const dt_plan *plan, int batch, size_t *bytes);
+
+/* Build `batch` draft trees (Alg. 1) from marginal logits [batch, L, V].
+ *   h0: [batch, d_h] fp32 root GRU states, or NULL for zeros;
+ *   T:  temperature (T <= 0 scores with tau = 1);
+ *   workspace: >= dt_workspace_size bytes, 256-byte aligned, caller-owned;
+ *   out: output arrays as documented in dt_tree.
+ * Launches on `stream` and returns without waiting. */
+dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, const float *h0,
+                        float T, void *workspace, size_t ws_bytes, dt_tree *out, void *stream);
+
+/* Release the plan's device memory (NULL is ignored). */
+void dt_plan_destroy(dt_plan *plan);
+
+/* Workspace (bytes) for dt_scan_topm over `rows` rows. */
+dt_status dt_scan_workspace_size(int rows, int V, int M, size_t *bytes);
+
+/* S1 alone: per row of logits [rows, V], the top-M ids (ordered by logit desc,
+ * id asc), their logits widened to fp32, and the tail log-sum-exp
+ * R = log sum_{v not in top-M} exp(x[v] / tau) (-inf when empty).
+ *   ids: [rows, M] int32; vals: [rows, M] float; tail_lse: [rows] float;
+ *   row_flags: [rows] int32 (DT_TREE_NONFINITE when the row holds NaN / +inf;
+ *   the other outputs of such a row are unspecified).
+ * Alg. 1 step 1; section 3.2. */
+dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, int M, float T,
+                       int32_t *ids, float *vals, float *tail_lse, int32_t *row_flags,
+                       void *workspace, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DOMINOTREE_H */

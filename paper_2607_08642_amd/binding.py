@@ -1,0 +1,250 @@
+"""Thin Python binding of libdominotree (include/dominotree.h).
+
+Argument marshalling only: every step of the tree build runs in the HIP
+kernels behind the C ABI.  torch is used for device memory and streams.  The
+library is loaded from this package directory; if it is missing, every call
+raises (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libdominotree.so")
+
+DT_F32 = 0
+DT_BF16 = 1
+DT_NORM_TAIL = 0
+DT_NORM_SLICE = 1
+DT_TREE_NONFINITE = 0x1
+DT_TREE_TRUNCATED = 0x2
+ABI_VERSION = 1
+
+STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
+          -4: "DT_ERR_UNSUPPORTED", -5: "DT_ERR_WORKSPACE", -6: "DT_ERR_ALIGN", -7: "DT_ERR_HIP"}
+
+# every symbol include/dominotree.h declares
+EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_create",
+           "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_scan_workspace_size",
+           "dt_scan_topm")
+
+
+class DTError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class dt_gru(ctypes.Structure):
+    _fields_ = [("w_ih", ctypes.c_void_p), ("w_hh", ctypes.c_void_p), ("b_ih", ctypes.c_void_p),
+                ("b_hh", ctypes.c_void_p), ("d_in", ctypes.c_int), ("d_h", ctypes.c_int)]
+
+
+class dt_head(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+class dt_options(ctypes.Structure):
+    _fields_ = [("max_children", ctypes.c_int), ("norm_mode", ctypes.c_int),
+                ("pos_offset", ctypes.c_int), ("reserved", ctypes.c_int)]
+
+
+class dt_tree(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p),
+                ("depth", ctypes.c_void_p), ("position_ids", ctypes.c_void_p),
+                ("mask", ctypes.c_void_p), ("scores", ctypes.c_void_p),
+                ("n_nodes", ctypes.c_void_p), ("status", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the shared library (raises if it is missing or its ABI differs)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2607_08642_amd.build.build()")
+    lib = ctypes.CDLL(path)
+    vp, ci, cf, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.dt_abi_version.restype = ci
+    lib.dt_status_string.restype = ctypes.c_char_p
+    lib.dt_status_string.argtypes = [ci]
+    lib.dt_last_error.restype = ctypes.c_char_p
+    lib.dt_plan_create.restype = ci
+    lib.dt_plan_create.argtypes = [ctypes.POINTER(vp), vp, ci, ci, ctypes.POINTER(dt_gru),
+                                   ctypes.POINTER(dt_head), ci, ci, ci, ci, ci, ci,
+                                   ctypes.POINTER(dt_options)]
+    lib.dt_workspace_size.restype = ci
+    lib.dt_workspace_size.argtypes = [vp, ci, ctypes.POINTER(sz)]
+    lib.dt_build_tree.restype = ci
+    lib.dt_build_tree.argtypes = [vp, vp, ci, vp, cf, vp, sz, ctypes.POINTER(dt_tree), vp]
+    lib.dt_plan_destroy.restype = None
+    lib.dt_plan_destroy.argtypes = [vp]
+    lib.dt_scan_workspace_size.restype = ci
+    lib.dt_scan_workspace_size.argtypes = [ci, ci, ci, ctypes.POINTER(sz)]
+    lib.dt_scan_topm.restype = ci
+    lib.dt_scan_topm.argtypes = [vp, ci, ci, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
+    if lib.dt_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"ABI mismatch: library {lib.dt_abi_version()} vs binding {ABI_VERSION}")
+    _lib = lib
+    return lib
+
+
+def _check(st: int) -> None:
+    if st != 0:
+        raise DTError(st, load().dt_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return DT_BF16
+    if t.dtype == torch.float32:
+        return DT_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream or None
+
+
+@dataclasses.dataclass
+class Tree:
+    """Emitted trees (device tensors), nodes in pop order."""
+    tokens: "torch.Tensor"        # [b, B] int32
+    parents: "torch.Tensor"       # [b, B] int32, -1 = child of the root
+    depth: "torch.Tensor"         # [b, B] int32
+    position_ids: "torch.Tensor"  # [b, B] int32
+    mask: "torch.Tensor"          # [b, B, B] uint8 ancestor-or-self
+    scores: "torch.Tensor"        # [b, B] float32
+    n_nodes: "torch.Tensor"       # [b] int32
+    status: "torch.Tensor"        # [b] int32
+
+    @staticmethod
+    def empty(batch: int, B: int, device) -> "Tree":
+        import torch
+        i32 = dict(dtype=torch.int32, device=device)
+        return Tree(torch.empty(batch, B, **i32), torch.empty(batch, B, **i32),
+                    torch.empty(batch, B, **i32), torch.empty(batch, B, **i32),
+                    torch.empty(batch, B, B, dtype=torch.uint8, device=device),
+                    torch.empty(batch, B, dtype=torch.float32, device=device),
+                    torch.empty(batch, **i32), torch.empty(batch, **i32))
+
+    def as_c(self) -> dt_tree:
+        return dt_tree(*(x.data_ptr() for x in (self.tokens, self.parents, self.depth,
+                                                   self.position_ids, self.mask, self.scores,
+                                                   self.n_nodes, self.status)))
+
+
+class Plan:
+    """dt_plan: one model (embedding table, GRU, head) and one (L, M, B) shape.
+
+    The embedding tensor must outlive the plan; the GRU and head weights are
+    packed into plan-owned memory.
+    """
+
+    def __init__(self, emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c, *, L: int, M: int, B: int,
+                 logits_dtype: int, max_batch: int = 1, max_children: int = 0,
+                 norm_mode: int = DT_NORM_TAIL, pos_offset: int = 0):
+        lib = load()
+        self._lib = lib
+        self.emb = emb
+        self.V, self.d_e = emb.shape
+        self.d_h = w_hh.shape[1]
+        self.L, self.M, self.B, self.max_batch = L, M, B, max_batch
+        self.logits_dtype = logits_dtype
+        wdt = _dtype_code(emb)
+        gru = dt_gru(_ptr(w_ih), _ptr(w_hh), _ptr(b_ih), _ptr(b_hh), self.d_e, self.d_h)
+        head = dt_head(_ptr(w_c), _ptr(b_c))
+        opts = dt_options(max_children, norm_mode, pos_offset, 0)
+        h = ctypes.c_void_p()
+        _check(lib.dt_plan_create(ctypes.byref(h), _ptr(emb), self.V, self.d_e, ctypes.byref(gru),
+                                  ctypes.byref(head), wdt, L, M, B, logits_dtype, max_batch,
+                                  ctypes.byref(opts)))
+        self.handle = h
+        self._ws = {}
+
+    def workspace_size(self, batch: int) -> int:
+        n = ctypes.c_size_t()
+        _check(self._lib.dt_workspace_size(self.handle, batch, ctypes.byref(n)))
+        return n.value
+
+    def workspace(self, batch: int):
+        import torch
+        if batch not in self._ws:
+            self._ws[batch] = torch.empty(self.workspace_size(batch), dtype=torch.uint8,
+                                          device=self.emb.device)
+        return self._ws[batch]
+
+    def build_tree(self, logits, T: float, h0=None, out: Optional[Tree] = None,
+                   workspace=None, stream=None) -> Tree:
+        """dt_build_tree on torch's current stream (asynchronous)."""
+        batch = logits.shape[0]
+        if out is None:
+            out = Tree.empty(batch, self.B, logits.device)
+        ws = self.workspace(batch) if workspace is None else workspace
+        c = out.as_c()
+        _check(self._lib.dt_build_tree(self.handle, _ptr(logits), batch, _ptr(h0),
+                                       ctypes.c_float(T), _ptr(ws), ws.numel(), ctypes.byref(c),
+                                       _stream(stream)))
+        return out
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            self._lib.dt_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_tree(marginal_logits, emb, gru_weights, correction_head, L: int, M: int, B: int,
+               T: float, h0=None, max_children: int = 0, norm_mode: int = DT_NORM_TAIL,
+               pos_offset: int = 0) -> Tree:
+    """One-shot form of the paper's build_tree(...) -> tree (creates and drops a plan).
+
+    gru_weights = (w_ih, w_hh, b_ih, b_hh); correction_head = (w_c, b_c).
+    """
+    w_ih, w_hh, b_ih, b_hh = gru_weights
+    w_c, b_c = correction_head
+    plan = Plan(emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c, L=L, M=M, B=B,
+                logits_dtype=_dtype_code(marginal_logits), max_batch=marginal_logits.shape[0],
+                max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset)
+    try:
+        return plan.build_tree(marginal_logits, T, h0)
+    finally:
+        import torch
+        torch.cuda.current_stream().synchronize()
+        plan.close()
+
+
+def scan_topm(logits, M: int, T: float, stream=None):
+    """dt_scan_topm over a [rows, V] tensor: (ids, vals, tail_lse, row_flags)."""
+    import torch
+    lib = load()
+    rows, V = logits.shape
+    n = ctypes.c_size_t()
+    _check(lib.dt_scan_workspace_size(rows, V, M, ctypes.byref(n)))
+    ws = torch.empty(n.value, dtype=torch.uint8, device=logits.device)
+    ids = torch.empty(rows, M, dtype=torch.int32, device=logits.device)
+    vals = torch.empty(rows, M, dtype=torch.float32, device=logits.device)
+    tail = torch.empty(rows, dtype=torch.float32, device=logits.device)
+    flags = torch.empty(rows, dtype=torch.int32, device=logits.device)
+    _check(lib.dt_scan_topm(_ptr(logits), rows, V, _dtype_code(logits), M, ctypes.c_float(T),
+                            _ptr(ids), _ptr(vals), _ptr(tail), _ptr(flags), _ptr(ws), n.value,
+                            _stream(stream)))
+    return ids, vals, tail, flags

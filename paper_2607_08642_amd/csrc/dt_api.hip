@@ -1,0 +1,252 @@
+// Host side of the C ABI declared in include/dominotree.h: argument checks,
+// plan creation (weight packing), workspace layout and launch sequencing.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "dt_internal.h"
+
+namespace dt {
+size_t expand_lds_bytes(int dh, int M);
+}
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dt_status fail(dt_status s, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+dt_status fail(dt_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+dt_status hip_fail(hipError_t e, const char *what) {
+  return fail(DT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool valid_dtype(int d) { return d == DT_F32 || d == DT_BF16; }
+size_t dsize(int d) { return d == DT_BF16 ? 2 : 4; }
+
+int ecap_for(const dt_plan *p) { return p->L * p->B + dt::kChunkNodes; }
+
+}  // namespace
+
+namespace dt {
+
+// Lay out the workspace of one dt_build_tree call; base == nullptr only sizes it.
+Workspace carve(const dt_plan *p, int batch, char *base) {
+  Workspace ws{};
+  const int rows = batch * p->L;
+  const ScanGeom g = scan_geom(rows, p->V, p->M);
+  size_t o = base ? carve_scan(base, g, &ws) : scan_bytes(g);
+  auto at = [&](size_t bytes) {
+    float *ptr = base ? reinterpret_cast<float *>(base + o) : nullptr;
+    o += align_up(bytes, 256);
+    return ptr;
+  };
+  const size_t rm = (size_t)rows * p->M;
+  ws.P = at(rm * 3 * p->d_h * sizeof(float));
+  ws.U = at(rm * p->d_h * sizeof(float));
+  ws.cvec = at(rm * sizeof(float));
+  ws.ecap = ecap_for(p);
+  ws.states = at((size_t)batch * ws.ecap * p->d_h * sizeof(float));
+  ws.bytes = o;
+  return ws;
+}
+
+}  // namespace dt
+
+extern "C" {
+
+int dt_abi_version(void) { return DT_ABI_VERSION; }
+
+const char *dt_status_string(int s) {
+  switch (s) {
+    case DT_OK: return "ok";
+    case DT_ERR_NULL: return "a required pointer is NULL";
+    case DT_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case DT_ERR_DTYPE: return "unknown dtype";
+    case DT_ERR_UNSUPPORTED: return "outside the supported envelope";
+    case DT_ERR_WORKSPACE: return "workspace missing or too small";
+    case DT_ERR_ALIGN: return "misaligned pointer";
+    case DT_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char *dt_last_error(void) { return g_last_error.c_str(); }
+
+dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const dt_gru *gru,
+                         const dt_head *head, int weights_dtype, int L, int M, int B,
+                         int logits_dtype, int max_batch, const dt_options *opts) {
+  if (!plan) return fail(DT_ERR_NULL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  if (!emb || !gru || !head) return fail(DT_ERR_NULL, "emb, gru and head are required");
+  if (!gru->w_ih || !gru->w_hh || !head->w) return fail(DT_ERR_NULL, "w_ih, w_hh and head.w are required");
+  if (!valid_dtype(weights_dtype) || !valid_dtype(logits_dtype))
+    return fail(DT_ERR_DTYPE, "dtype codes must be DT_F32 or DT_BF16");
+  if (V < 1 || d_e < 1 || L < 1 || M < 1 || B < 1 || max_batch < 1)
+    return fail(DT_ERR_SHAPE, "sizes must be positive (V=%d d_e=%d L=%d M=%d B=%d max_batch=%d)", V,
+                d_e, L, M, B, max_batch);
+  if (gru->d_in != d_e) return fail(DT_ERR_SHAPE, "gru.d_in (%d) must equal d_e (%d)", gru->d_in, d_e);
+  const int d_h = gru->d_h;
+  if (M > V) return fail(DT_ERR_SHAPE, "M (%d) exceeds V (%d)", M, V);
+  if (M > dt::kMaxM || B > dt::kMaxB || L > dt::kMaxL || d_e > dt::kMaxDe || d_h < 32 ||
+      d_h > dt::kMaxDh || d_h % 32 != 0)
+    return fail(DT_ERR_UNSUPPORTED,
+                "outside the envelope (M<=256, B<=256, L<=64, d_e<=8192, 32<=d_h<=1024, d_h%%32==0)");
+  dt_options o = {0, DT_NORM_TAIL, 0, 0};
+  if (opts) o = *opts;
+  if (o.max_children < 0) return fail(DT_ERR_SHAPE, "max_children must be >= 0");
+  if (o.norm_mode != DT_NORM_TAIL && o.norm_mode != DT_NORM_SLICE)
+    return fail(DT_ERR_UNSUPPORTED, "norm_mode must be DT_NORM_TAIL or DT_NORM_SLICE");
+  if (o.reserved != 0) return fail(DT_ERR_UNSUPPORTED, "dt_options.reserved must be 0");
+  const size_t ws = dsize(weights_dtype);
+  if (!aligned(emb, 16) || !aligned(gru->w_ih, ws) || !aligned(gru->w_hh, ws) ||
+      !aligned(head->w, ws) || (gru->b_ih && !aligned(gru->b_ih, ws)) ||
+      (gru->b_hh && !aligned(gru->b_hh, ws)) || (head->b && !aligned(head->b, ws)))
+    return fail(DT_ERR_ALIGN, "emb must be 16-byte aligned, weights naturally aligned");
+  int dev = 0, ncu = 0, maxlds = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess)
+    e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  if ((int)dt::expand_lds_bytes(d_h, M) > maxlds)
+    return fail(DT_ERR_UNSUPPORTED, "expansion needs %zu bytes of LDS, device has %d",
+                dt::expand_lds_bytes(d_h, M), maxlds);
+
+  dt_plan *p = new (std::nothrow) dt_plan();
+  if (!p) return fail(DT_ERR_HIP, "host allocation failed");
+  p->V = V;
+  p->d_e = d_e;
+  p->d_h = d_h;
+  p->L = L;
+  p->M = M;
+  p->B = B;
+  int k = o.max_children > 0 ? o.max_children : (M < B ? M : B);
+  if (k > M) k = M;
+  if (k > B) k = B;  // a child ranked B or lower among its siblings can never be popped
+  p->k = k;
+  p->norm_mode = o.norm_mode;
+  p->pos_offset = o.pos_offset;
+  p->wdt = weights_dtype;
+  p->ldt = logits_dtype;
+  p->max_batch = max_batch;
+  p->emb = emb;
+  p->nf = 4 * d_h;
+  p->nf_pad = (p->nf + dt::kFoldBN - 1) / dt::kFoldBN * dt::kFoldBN;
+  p->has_bc = head->b != nullptr;
+  p->num_cus = ncu;
+  e = hipMalloc(&p->wfold, (size_t)p->nf_pad * d_e * ws);
+  if (e == hipSuccess) e = hipMalloc(&p->b_ih, sizeof(float) * 3 * d_h);
+  if (e == hipSuccess) e = hipMalloc(&p->b_hh, sizeof(float) * 3 * d_h);
+  if (e == hipSuccess) e = hipMalloc(&p->b_c, sizeof(float) * d_e);
+  if (e == hipSuccess) e = hipMalloc(&p->whh_t, (size_t)3 * d_h * d_h * ws);
+  if (e == hipSuccess) e = dt::pack_weights(p, gru, head, nullptr);
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  if (e != hipSuccess) {
+    dt_status st = hip_fail(e, "plan creation");
+    dt_plan_destroy(p);
+    return st;
+  }
+  *plan = p;
+  return DT_OK;
+}
+
+void dt_plan_destroy(dt_plan *p) {
+  if (!p) return;
+  if (p->wfold) (void)hipFree(p->wfold);
+  if (p->b_ih) (void)hipFree(p->b_ih);
+  if (p->b_hh) (void)hipFree(p->b_hh);
+  if (p->b_c) (void)hipFree(p->b_c);
+  if (p->whh_t) (void)hipFree(p->whh_t);
+  delete p;
+}
+
+dt_status dt_workspace_size(const dt_plan *plan, int batch, size_t *bytes) {
+  if (!plan || !bytes) return fail(DT_ERR_NULL, "plan and bytes are required");
+  if (batch < 1 || batch > plan->max_batch)
+    return fail(DT_ERR_SHAPE, "batch %d outside [1, max_batch=%d]", batch, plan->max_batch);
+  *bytes = dt::carve(plan, batch, nullptr).bytes;
+  return DT_OK;
+}
+
+dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const float *h0, float T,
+                        void *workspace, size_t ws_bytes, dt_tree *out, void *stream) {
+  if (!plan || !logits || !out) return fail(DT_ERR_NULL, "plan, logits and out are required");
+  if (!out->tokens || !out->parents || !out->depth || !out->position_ids || !out->mask ||
+      !out->scores || !out->n_nodes || !out->status)
+    return fail(DT_ERR_NULL, "every dt_tree output pointer is required");
+  if (batch < 1 || batch > plan->max_batch)
+    return fail(DT_ERR_SHAPE, "batch %d outside [1, max_batch=%d]", batch, plan->max_batch);
+  if (!(T == T)) return fail(DT_ERR_SHAPE, "temperature is NaN");
+  const size_t need = dt::carve(plan, batch, nullptr).bytes;
+  if (!workspace || ws_bytes < need)
+    return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
+  if (!aligned(workspace, 256)) return fail(DT_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (!aligned(logits, dsize(plan->ldt)) || (h0 && !aligned(h0, 4)) || !aligned(out->tokens, 4) ||
+      !aligned(out->parents, 4) || !aligned(out->depth, 4) || !aligned(out->position_ids, 4) ||
+      !aligned(out->scores, 4) || !aligned(out->n_nodes, 4) || !aligned(out->status, 4))
+    return fail(DT_ERR_ALIGN, "logits and outputs must be naturally aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
+  dt::Workspace ws = dt::carve(plan, batch, static_cast<char *>(workspace));
+  const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
+  hipError_t e = dt::launch_scan(logits, plan->ldt, g, inv_tau, ws, s);
+  if (e != hipSuccess) return hip_fail(e, "scan launch");
+  e = dt::launch_fold(plan, batch, ws, s);
+  if (e != hipSuccess) return hip_fail(e, "fold launch");
+  e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);
+  if (e != hipSuccess) return hip_fail(e, "expand launch");
+  return DT_OK;
+}
+
+dt_status dt_scan_workspace_size(int rows, int V, int M, size_t *bytes) {
+  if (!bytes) return fail(DT_ERR_NULL, "bytes is required");
+  if (rows < 1 || V < 1 || M < 1 || M > V) return fail(DT_ERR_SHAPE, "need rows, V >= 1 and 1 <= M <= V");
+  if (M > dt::kMaxM) return fail(DT_ERR_UNSUPPORTED, "M must be <= 256");
+  *bytes = dt::scan_bytes(dt::scan_geom(rows, V, M));
+  return DT_OK;
+}
+
+dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, int M, float T,
+                       int32_t *ids, float *vals, float *tail_lse, int32_t *row_flags,
+                       void *workspace, size_t ws_bytes, void *stream) {
+  if (!logits || !ids || !vals || !tail_lse || !row_flags)
+    return fail(DT_ERR_NULL, "logits and every output are required");
+  if (!valid_dtype(logits_dtype)) return fail(DT_ERR_DTYPE, "dtype must be DT_F32 or DT_BF16");
+  if (rows < 1 || V < 1 || M < 1 || M > V) return fail(DT_ERR_SHAPE, "need rows, V >= 1 and 1 <= M <= V");
+  if (M > dt::kMaxM) return fail(DT_ERR_UNSUPPORTED, "M must be <= 256");
+  if (!(T == T)) return fail(DT_ERR_SHAPE, "temperature is NaN");
+  const dt::ScanGeom g = dt::scan_geom(rows, V, M);
+  const size_t need = dt::scan_bytes(g);
+  if (!workspace || ws_bytes < need)
+    return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
+  if (!aligned(workspace, 256)) return fail(DT_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (!aligned(logits, dsize(logits_dtype)) || !aligned(ids, 4) || !aligned(vals, 4) ||
+      !aligned(tail_lse, 4) || !aligned(row_flags, 4))
+    return fail(DT_ERR_ALIGN, "logits and outputs must be naturally aligned");
+  dt::Workspace ws{};
+  dt::carve_scan(static_cast<char *>(workspace), g, &ws);
+  ws.cand = ids;
+  ws.candv = vals;
+  ws.tail = tail_lse;
+  ws.row_flag = row_flags;
+  const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
+  hipError_t e = dt::launch_scan(logits, logits_dtype, g, inv_tau, ws, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "scan launch");
+  return DT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+// Internal definitions shared by the HIP sources of libdominotree (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "dominotree.h"
+
+namespace dt {
+
+// ---------------------------------------------------------------------------
+// limits (the public envelope is documented in dominotree.h)
+// ---------------------------------------------------------------------------
+constexpr int kMaxM = 256;
+constexpr int kMaxB = 256;
+constexpr int kMaxL = 64;
+constexpr int kMaxDh = 1024;
+constexpr int kMaxDe = 8192;
+
+// scan: one workgroup of 256 threads per (row, chunk)
+constexpr int kScanThreads = 256;
+constexpr int kScanSortCap = 4096;   // bitonic sort buffer (keys) per workgroup
+constexpr int kScanFlushAt = 256;    // flush the candidate buffer beyond this many keys
+
+// fold GEMM tile (bf16 MFMA path)
+constexpr int kFoldBM = 128;
+constexpr int kFoldBN = 128;
+constexpr int kFoldBK = 64;
+
+// expansion kernel
+constexpr int kExpThreads = 1024;
+constexpr int kNodeCap = 1536;       // live nodes per tree kept in LDS
+constexpr int kChunkNodes = 16;      // nodes expanded together (shared weight pass)
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// order-preserving 64-bit keys: (value desc, index asc) <=> key desc.
+// high word: IEEE bits mapped to an unsigned order (-0 folded onto +0);
+// low word: bitwise NOT of the index.  Key 0 is never produced (sentinel).
+// ---------------------------------------------------------------------------
+__host__ __device__ inline uint32_t ordered_bits(float v) {
+  uint32_t u;
+  if (v == 0.0f) v = 0.0f;
+  __builtin_memcpy(&u, &v, 4);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__host__ __device__ inline float ordered_to_float(uint32_t o) {
+  uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+  float v;
+  __builtin_memcpy(&v, &u, 4);
+  return v;
+}
+__host__ __device__ inline uint64_t make_key(float v, uint32_t idx) {
+  return ((uint64_t)ordered_bits(v) << 32) | (uint32_t)(~idx);
+}
+__host__ __device__ inline float key_value(uint64_t k) { return ordered_to_float((uint32_t)(k >> 32)); }
+__host__ __device__ inline uint32_t key_index(uint64_t k) { return ~(uint32_t)k; }
+
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// ---------------------------------------------------------------------------
+// plan
+// ---------------------------------------------------------------------------
+struct ScanGeom {
+  int rows, V, M, chunk, nchunks;
+};
+
+}  // namespace dt
+
+struct dt_plan {
+  int V, d_e, d_h, L, M, B, k, norm_mode, pos_offset;
+  int wdt, ldt, max_batch;
+  const void *emb;
+  void *wfold;      // [nf_pad, d_e] (weights dtype): rows [0,3dh) = W_ih, [3dh,4dh) = W_c^T
+  int nf, nf_pad;   // nf = 4*d_h
+  float *b_ih;      // [3dh] fp32 (zeros when absent)
+  float *b_hh;      // [3dh] fp32
+  float *b_c;       // [d_e] fp32 (zeros when absent)
+  int has_bc;
+  void *whh_t;      // [d_h (k)][3][d_h (unit)] weights dtype: W_hh transposed per gate
+  int num_cus;
+};
+
+namespace dt {
+
+struct Workspace {
+  // scan
+  uint64_t *chunk_keys;   // [rows][nchunks][M]
+  float2 *chunk_tail;     // [rows][nchunks] (max, sum of exp((x-max)/tau))
+  int32_t *chunk_flag;    // [rows][nchunks]
+  int32_t *cand;          // [rows][M]
+  float *candv;           // [rows][M]
+  float *tail;            // [rows]
+  int32_t *row_flag;      // [rows]
+  // fold
+  float *P;               // [rows*M][3dh]
+  float *U;               // [rows*M][dh]
+  float *cvec;            // [rows*M]
+  // expansion
+  float *states;          // [batch][ecap][dh]
+  int ecap;
+  size_t bytes;
+};
+
+ScanGeom scan_geom(int rows, int V, int M);
+size_t scan_bytes(const ScanGeom &g);
+// carve the scan part of a workspace; returns bytes used
+size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws);
+Workspace carve(const dt_plan *p, int batch, char *base);
+
+// kernel launchers (return hipError_t of the launch)
+hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
+                       const Workspace &ws, hipStream_t s);
+hipError_t launch_fold(const dt_plan *p, int batch, const Workspace &ws, hipStream_t s);
+hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
+                         const Workspace &ws, const dt_tree *out, hipStream_t s);
+hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);
+
+}  // namespace dt

@@ -1,0 +1,90 @@
+"""Helpers for GPU tests: upload synthetic workloads, run the library, compare with the oracle."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import oracle
+from helpers import check_tree_valid, rescore, run_oracle
+from paper_2607_08642_amd import binding, synth
+
+GAP_TOL = 1e-4          # decisive score gaps above this must give identical trees
+
+
+def score_tol(wl) -> float:
+    """Score tolerance: 1e-4 when everything is fp32, 2e-2 when bf16 inputs feed the correction."""
+    return 1e-4 if wl.weights.dtype == synth.DT_F32 and wl.logits_dtype == synth.DT_F32 else 2e-2
+
+
+def to_dev(a: np.ndarray, dtype: int, device="cuda"):
+    if a is None:
+        return None
+    if dtype == synth.DT_BF16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+
+class DeviceWorkload:
+    def __init__(self, wl, max_children=0, norm_mode=0, pos_offset=0):
+        w = wl.weights
+        self.wl = wl
+        d = synth.DT_BF16 if w.dtype == synth.DT_BF16 else synth.DT_F32
+        self.emb = to_dev(w.emb, d)
+        self.w_ih = to_dev(w.w_ih, d)
+        self.w_hh = to_dev(w.w_hh, d)
+        self.b_ih = to_dev(w.b_ih, d)
+        self.b_hh = to_dev(w.b_hh, d)
+        self.w_c = to_dev(w.w_c, d)
+        self.b_c = to_dev(w.b_c, d)
+        self.logits = to_dev(wl.logits, wl.logits_dtype)
+        self.h0 = None if wl.h0 is None else torch.from_numpy(wl.h0.astype(np.float32)).cuda()
+        self.plan = binding.Plan(self.emb, self.w_ih, self.w_hh, self.b_ih, self.b_hh, self.w_c,
+                                 self.b_c, L=wl.L, M=wl.M, B=wl.B, logits_dtype=wl.logits_dtype,
+                                 max_batch=wl.batch, max_children=max_children,
+                                 norm_mode=norm_mode, pos_offset=pos_offset)
+        self.kw = dict(max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset)
+
+    def run(self):
+        tree = self.plan.build_tree(self.logits, self.wl.T, self.h0)
+        torch.cuda.synchronize()
+        return {k: getattr(tree, k).cpu().numpy() for k in
+                ("tokens", "parents", "depth", "position_ids", "mask", "scores", "n_nodes",
+                 "status")}
+
+    def close(self):
+        self.plan.close()
+
+
+def compare_tree(wl, t, got, kw, tol=None):
+    """Compare GPU tree t with the oracle.  Returns (kind, max_score_err) where kind
+    is 'exact' or 'ambiguous'; raises AssertionError on a mismatch."""
+    tol = score_tol(wl) if tol is None else tol
+    ref = run_oracle(wl, t, **kw)
+    B = wl.B
+    n = int(got["n_nodes"][t])
+    assert int(got["status"][t]) == ref["status"], (got["status"][t], ref["status"])
+    assert n == ref["n_nodes"], f"tree {t}: n_nodes {n} vs {ref['n_nodes']}"
+    tok, par, dep = got["tokens"][t], got["parents"][t], got["depth"][t]
+    pos, mask, sc = got["position_ids"][t], got["mask"][t], got["scores"][t]
+    errs = check_tree_valid(tok, par, dep, pos, mask, sc, n, B, kw.get("pos_offset", 0))
+    assert not errs, f"tree {t}: {errs[:5]}"
+    if n == 0:
+        return "exact", 0.0
+    if ref["min_gap"] > GAP_TOL:
+        for key in ("tokens", "parents", "depth", "position_ids"):
+            np.testing.assert_array_equal(got[key][t], ref[key], err_msg=f"tree {t} {key}")
+        np.testing.assert_array_equal(mask, ref["mask"], err_msg=f"tree {t} mask")
+        err = float(np.max(np.abs(sc[:n] - ref["scores"][:n])))
+        assert err <= tol, f"tree {t}: score error {err}"
+        return "exact", err
+    # ambiguous seed: the GPU tree must be a valid best-first tree within tolerance
+    g, valid = rescore(wl, t, tok, par, n, max_children=kw.get("max_children", 0),
+                       norm_mode=kw.get("norm_mode", 0))
+    assert valid, f"tree {t}: a GPU node is not a top-k child of its parent"
+    err = float(np.max(np.abs(sc[:n] - g)))
+    assert err <= tol, f"tree {t}: rescored error {err}"
+    ref_min = float(np.min(ref["scores"][:n]))
+    assert float(np.min(g)) >= ref_min - 2 * tol, "GPU tree leaves out a clearly better node"
+    return "ambiguous", err

@@ -1,0 +1,99 @@
+"""S1 parity: the HIP top-M + tail-LSE scan against the oracle (Alg. 1 step 1; section 3.2).
+
+Token ids and their logits must match exactly (pure comparisons of exact
+values, ties by lower id); the tail log-sum-exp within 1e-5 relative.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import to_dev
+from paper_2607_08642_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(x_np, dtype, M, T, rows=None, case=""):
+    print(f"[scan] {case} shape={x_np.shape} dtype={dtype} M={M} T={T}", flush=True)
+    x = to_dev(x_np, dtype)
+    ids, vals, tail, flags = binding.scan_topm(x, M, T)
+    torch.cuda.synchronize()
+    ids, vals, tail, flags = (a.cpu().numpy() for a in (ids, vals, tail, flags))
+    Xw = oracle.widen(x_np, dtype)
+    tau = oracle.effective_temperature(T)
+    for r in (range(x_np.shape[0]) if rows is None else rows):
+        bad = bool(np.any(np.isnan(Xw[r])) or np.any(Xw[r] == np.inf))
+        assert flags[r] == (oracle.TREE_NONFINITE if bad else 0), (case, r)
+        if bad:
+            continue
+        rid, rx, rR = oracle.scan_row(Xw[r], M, tau)
+        np.testing.assert_array_equal(ids[r], rid, err_msg=f"{case} row {r} ids")
+        np.testing.assert_array_equal(vals[r].astype(np.float64), rx, err_msg=f"{case} row {r} vals")
+        if rR == -math.inf:
+            assert tail[r] == -np.inf
+        else:
+            assert abs(tail[r] - rR) <= 1e-5 * max(1.0, abs(rR)), (case, r, tail[r], rR)
+
+
+def test_scan_tiny_fp32():
+    wl = synth.tiny()
+    _check(wl.logits[0], synth.DT_F32, 8, 0.0, case="tiny")
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0, 0.7])
+def test_scan_qwen_rows_bf16(T):
+    x = synth.peaked_logits(2, 0, 16, synth.QWEN3_VOCAB, synth.DT_BF16, 1, 4, 6.0, 12.0)
+    _check(x, synth.DT_BF16, 64, T, case="qwen16")
+
+
+def test_scan_concurrent_rows_sampled():
+    x = np.concatenate([synth.peaked_logits(4, t, 16, synth.QWEN3_VOCAB, synth.DT_BF16, 1, 4,
+                                            6.0, 12.0) for t in range(32)])
+    _check(x, synth.DT_BF16, 64, 0.7, rows=list(range(0, 512, 17)) + [511], case="concurrent")
+
+
+def test_scan_flattened_rows_bf16():
+    x = synth.peaked_logits(3, 0, 16, synth.QWEN3_VOCAB, synth.DT_BF16, 4, 16, 3.0, 6.0)
+    _check(x, synth.DT_BF16, 64, 0.0, case="flattened")
+
+
+def test_scan_heavy_ties():
+    rng = np.random.default_rng(5)
+    x = np.round(rng.standard_normal((6, 20000)) * 3).astype(np.float32)   # integers: huge ties
+    _check(x, synth.DT_F32, 64, 1.0, case="ties-f32")
+    _check(synth.f32_to_bf16_bits(x), synth.DT_BF16, 200, 0.5, case="ties-bf16")
+
+
+def test_scan_all_equal_and_neg_inf():
+    x = np.zeros((3, 5000), np.float32)
+    x[1, ::3] = -np.inf
+    x[2, :] = -np.inf
+    x[2, 4000:4003] = 1.0
+    _check(x, synth.DT_F32, 16, 0.0, case="equal/-inf")
+
+
+@pytest.mark.parametrize("V,M", [(1001, 7), (3, 3), (64, 64), (257, 256), (9000, 1)])
+def test_scan_odd_shapes(V, M):
+    rng = np.random.default_rng(V)
+    x = (rng.standard_normal((5, V)) * 2).astype(np.float32)
+    _check(x, synth.DT_F32, M, 0.0, case=f"f32 V={V}")
+    _check(synth.f32_to_bf16_bits(x), synth.DT_BF16, M, 0.9, case=f"bf16 V={V}")
+
+
+def test_scan_descending_rows_worst_case():
+    # increasing values: every sub-batch beats the running threshold
+    V = 40000
+    x = np.tile(np.arange(V, dtype=np.float32) / 100.0, (2, 1))
+    x[1] = x[1][::-1]
+    _check(x, synth.DT_F32, 256, 1.0, case="monotone")
+
+
+def test_scan_nonfinite_flags():
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((4, 3000)).astype(np.float32)
+    x[1, 17] = np.nan
+    x[2, 2999] = np.inf
+    _check(x, synth.DT_F32, 8, 0.0, case="nonfinite")

@@ -1,0 +1,123 @@
+"""Tree parity: dt_build_tree (all of S1-S5 on the GPU) against the oracle.
+
+Wherever the oracle's decisive score gaps exceed 1e-4 the trees must be
+identical (tokens, parents, depth, position ids, mask, node count) and the
+scores within 1e-4 (fp32 inputs) or 2e-2 (bf16 inputs feeding the
+correction).  Seeds with smaller gaps must still give a valid best-first tree
+within tolerance.  Sizes span several tiles and ragged tails; the full
+Qwen3-shaped workloads are checked on sampled trees.
+"""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import DeviceWorkload, compare_tree
+from paper_2607_08642_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def run_case(wl, trees=None, name="", **kw):
+    print(f"[tree] {name} batch={wl.batch} L={wl.L} M={wl.M} B={wl.B} T={wl.T} kw={kw}", flush=True)
+    dw = DeviceWorkload(wl, **kw)
+    try:
+        got = dw.run()
+    finally:
+        dw.close()
+    kinds = []
+    for t in (range(wl.batch) if trees is None else trees):
+        kinds.append(compare_tree(wl, t, got, dw.kw))
+    print(f"[tree] {name}: {[k for k, _ in kinds]} max score err {max(e for _, e in kinds):.2e}",
+          flush=True)
+    return kinds, got
+
+
+def test_tiny_workload():
+    kinds, _ = run_case(synth.tiny(), name="tiny")
+    assert kinds[0][0] == "exact"
+
+
+SWEEP = [
+    # (seed, batch, L, V, M, B, T, d_e, d_h, dtype, kw, extra)
+    (1, 1, 4, 300, 8, 8, 0.0, 64, 32, synth.DT_F32, {}, {}),
+    (2, 3, 6, 500, 16, 24, 0.7, 64, 64, synth.DT_F32, {}, dict(h0=True)),
+    (3, 2, 5, 1000, 64, 16, 1.0, 128, 64, synth.DT_BF16, {}, {}),
+    (4, 8, 3, 200, 12, 10, 1.5, 40, 32, synth.DT_F32, dict(max_children=3), dict(h0=True)),
+    (5, 4, 8, 700, 32, 16, 0.0, 96, 64, synth.DT_BF16, dict(norm_mode=1), {}),
+    (6, 1, 1, 100, 8, 6, 0.0, 32, 32, synth.DT_F32, {}, {}),
+    (7, 5, 4, 400, 16, 1, 0.9, 32, 32, synth.DT_F32, {}, dict(h0=True)),
+    (8, 2, 6, 300, 8, 6, 0.0, 64, 32, synth.DT_F32, dict(max_children=1), {}),
+    (9, 3, 10, 2000, 64, 48, 0.8, 64, 64, synth.DT_BF16, dict(pos_offset=11), dict(h0=True)),
+    (10, 2, 4, 64, 64, 20, 1.0, 32, 32, synth.DT_F32, {}, {}),
+    (11, 1, 5, 333, 20, 30, 0.6, 36, 32, synth.DT_BF16, dict(max_children=8), {}),
+    (12, 6, 16, 1500, 64, 64, 0.0, 64, 96, synth.DT_BF16, {}, dict(h0=True)),
+]
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=[f"s{c[0]}" for c in SWEEP])
+def test_random_sweep(case):
+    seed, batch, L, V, M, B, T, d_e, d_h, dt, kw, extra = case
+    wl = synth.random_small(seed, batch=batch, L=L, V=V, M=M, B=B, T=T, d_e=d_e, d_h=d_h,
+                            dtype=dt, **extra)
+    kinds, _ = run_case(wl, name=f"sweep{seed}", **kw)
+    assert sum(k == "exact" for k, _ in kinds) >= len(kinds) // 2
+
+
+def test_greedy_chain_on_gpu():
+    wl = synth.random_small(21, batch=2, L=6, V=400, M=16, B=6, T=0.0, d_e=64, d_h=32, h0=True)
+    kinds, got = run_case(wl, name="chain", max_children=1)
+    for t in range(2):
+        np.testing.assert_array_equal(got["parents"][t], np.arange(-1, 5))
+
+
+def test_zeroed_correction_on_gpu():
+    wl = synth.random_small(22, batch=2, L=5, V=800, M=32, B=20, T=0.8, d_e=64, d_h=32)
+    wl.weights.w_c = np.zeros_like(wl.weights.w_c)
+    wl.weights.b_c = np.zeros_like(wl.weights.b_c)
+    run_case(wl, name="zeroed")
+
+
+def test_nonfinite_tree_isolated():
+    wl = synth.random_small(23, batch=3, L=4, V=300, M=8, B=8, T=0.0, d_e=32, d_h=32)
+    x = wl.logits.copy()
+    x[1, 2, 5] = np.nan
+    wl.logits = x
+    kinds, got = run_case(wl, name="nan")
+    assert got["status"][1] == binding.DT_TREE_NONFINITE and got["n_nodes"][1] == 0
+    assert got["status"][0] == 0 and got["status"][2] == 0
+
+
+def test_determinism_and_stream():
+    wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
+                            dtype=synth.DT_BF16, h0=True)
+    dw = DeviceWorkload(wl)
+    try:
+        a = dw.run()
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            b = dw.run()
+    finally:
+        dw.close()
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+@functools.lru_cache(maxsize=None)
+def qwen(name):
+    return synth.WORKLOADS[name]()
+
+
+@pytest.mark.parametrize("name", ["qwen3_4b", "qwen3_8b", "budget64"])
+def test_qwen_workloads(name):
+    run_case(qwen(name), name=name)
+
+
+def test_qwen3_8b_paper_branching():
+    run_case(qwen("qwen3_8b"), name="qwen3_8b-k8", max_children=8)
+
+
+def test_concurrent_workload_sampled():
+    run_case(qwen("concurrent"), trees=[0, 1, 7, 19, 31], name="concurrent")
