@@ -1,0 +1,242 @@
+#!/usr/bin/env python
+"""Benchmark of the DominoTree draft-tree builder on one MI355X.
+
+One step = one dt_build_tree call over one batch of resident synthetic logits:
+top-M scan, fold, expansion and emission (every kernel of the path).  The
+default workload is the Qwen3-8B-shaped single stream (L=16, V=151936, M=64,
+B=16, T=1, d_e=4096, d_h=512).  Logit buffers rotate through >= 512 MB so the
+256 MB Infinity Cache cannot serve the scan.
+
+Prints ONE JSON line: trees/s for the whole job, the per-kernel roofline of the
+dominant kernel (durations from HIP events recorded between the library's
+kernels on the launch stream) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--workload", default="qwen3_8b",
+                    choices=["tiny", "qwen3_4b", "qwen3_8b", "budget64", "concurrent"])
+    ap.add_argument("--rotate-mb", type=float, default=512.0,
+                    help="logit bytes cycled through in the timed loop")
+    ap.add_argument("--profile-steps", type=int, default=50,
+                    help="calls with stage events (per-kernel durations)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 256 MiB device copy (scale for PMC byte counters)")
+    return ap.parse_args()
+
+
+def algorithmic(plan_cfg, stage):
+    """Algorithmic work of one launch of a stage: (bytes or flops, unit, bound)."""
+    c = plan_cfg
+    rows = c["batch"] * c["L"]
+    if stage == "scan_chunks":
+        return rows * c["V"] * c["logit_bytes"], "bytes", "hbm"
+    if stage == "scan_merge":
+        return rows * c["nchunks"] * c["M"] * 8, "bytes", "hbm"
+    # expansion: MFMA work of Alg. 1's expansions (GRU hidden GEMV + slice correction)
+    n = c["expanded_nodes_per_call"]
+    return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["M"] * c["d_h"]), "flops", "mfma"
+
+
+def traffic_from_profiles(workload, stage):
+    """HBM bytes per launch from committed PMC summaries, if they match the current kernel."""
+    path = os.path.join(PROFILES, "pmc_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(workload, {}).get(stage)
+        if not rec:
+            return None
+        import hashlib
+        src = os.path.join(ROOT, "paper_2607_08642_amd", "csrc", rec["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["sha256"]:
+            return None          # the kernel changed since the counters were taken
+        return rec["bytes_per_launch"]
+    except Exception:
+        return None
+
+
+def cpu_baseline(wl_name, wl, bufs_host, seconds):
+    """The oracle as it stands, one BLAS thread, on trees of the same workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    w = wl.weights
+    wd = dict(w_ih=w.w_ih, w_hh=w.w_hh, b_ih=w.b_ih, b_hh=w.b_hh, w_c=w.w_c, b_c=w.b_c,
+              dtype=w.dtype)
+    n = 0
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=1):
+        while True:
+            buf = bufs_host[(n // wl.batch) % len(bufs_host)]
+            t = n % wl.batch
+            oracle.build_tree(buf[t], w.emb, w.dtype, wd, None if wl.h0 is None else wl.h0[t],
+                              wl.M, wl.B, wl.T, logits_dtype=wl.logits_dtype)
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= seconds and n >= 3:
+                break
+    return {"value": n / el, "unit": "trees/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} trees of the {wl_name} workload (first rotation buffers), "
+                      f"float64 numpy oracle, 1 BLAS thread, {el:.1f} s"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(trees shard across GPUs with no exchange; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_08642_amd import binding, synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+
+    wl = synth.WORKLOADS[args.workload]()
+    w = wl.weights
+    d = w.dtype
+
+    def up(a, dt):
+        if a is None:
+            return None
+        if dt == synth.DT_BF16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+    emb = up(w.emb, d)
+    plan = binding.Plan(emb, up(w.w_ih, d), up(w.w_hh, d), up(w.b_ih, d), up(w.b_hh, d),
+                        up(w.w_c, d), up(w.b_c, d), L=wl.L, M=wl.M, B=wl.B,
+                        logits_dtype=wl.logits_dtype, max_batch=wl.batch)
+    per_buf = wl.logits.nbytes
+    nbuf = max(1, math.ceil(args.rotate_mb * 2**20 / per_buf))
+    bufs_host = [wl.logits] + [synth.logits_buffer(wl.name, i, wl.batch) for i in range(1, nbuf)]
+    bufs = [up(b, wl.logits_dtype) for b in bufs_host]
+    h0 = None if wl.h0 is None else torch.from_numpy(wl.h0).to(dev)
+    out = binding.Tree.empty(wl.batch, wl.B, dev)
+    ws = plan.workspace(wl.batch)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        plan.build_tree(bufs[i % nbuf], wl.T, h0, out=out, workspace=ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` calls, synchronised on both sides
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        evs[i].record(stream)
+        step(args.warmup + i)
+    evs[-1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_call = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]) * 1e3  # us
+
+    # per-kernel durations with stage events (same kernels, separate pass)
+    plan.set_profiling(True)
+    stages = {k: [] for k in binding.STAGES}
+    n_exp = []
+    for i in range(args.profile_steps):
+        step(i)
+        for k, v in plan.stage_ms().items():
+            stages[k].append(v * 1e3)
+    plan.set_profiling(False)
+    stage_us = {k: float(np.mean(v)) for k, v in stages.items()}
+
+    # expansions Alg. 1 performs: the root plus every popped node above depth L
+    # (the kernel's extra speculative expansions are not counted as useful work)
+    dep = out.depth.cpu().numpy()
+    nn = out.n_nodes.cpu().numpy()
+    expanded = int(sum(int(np.sum(dep[t, :nn[t]] < wl.L)) + 1 for t in range(wl.batch)))
+    # chunk count of the scan (the library's geometry rule: ~1024 workgroups,
+    # chunks a multiple of 2048 elements)
+    rows = wl.batch * wl.L
+    sub = 256 * 8
+    nch = max(1, min((1024 + rows - 1) // rows, (w.V + sub - 1) // sub))
+    chunk = ((w.V + nch - 1) // nch + sub - 1) // sub * sub
+    g_nchunks = (w.V + chunk - 1) // chunk
+
+    cfg = dict(batch=wl.batch, L=wl.L, V=w.V, M=wl.M, d_e=w.d_e, d_h=w.d_h,
+               logit_bytes=2 if wl.logits_dtype == synth.DT_BF16 else 4, nchunks=g_nchunks,
+               expanded_nodes_per_call=expanded)
+    dom = max(stage_us, key=stage_us.get)
+    work, unit, bound = algorithmic(cfg, dom)
+    dur_s = stage_us[dom] * 1e-6
+    if unit == "bytes":
+        achieved, peak, runit = work / dur_s / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = work / dur_s / 1e12
+        peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
+        runit = "TFLOP/s"
+    scan_bytes = rows * w.V * cfg["logit_bytes"]
+    scan_us = stage_us["scan_chunks"] + stage_us["scan_merge"]
+    trees = wl.batch * args.steps
+    res = {
+        "metric": "draft trees built/sec",
+        "value": trees / wall,
+        "unit": "trees/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if d == synth.DT_BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "L": wl.L, "V": w.V, "M": wl.M,
+                   "B": wl.B, "T": wl.T, "d_e": w.d_e, "d_h": w.d_h, "logit_buffers": nbuf},
+        "us_per_tree": wall / trees * 1e6,
+        "gpu_us_per_call_p50": float(np.percentile(per_call, 50)),
+        "gpu_us_per_call_p99": float(np.percentile(per_call, 99)),
+        "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
+        "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "stages_us": stage_us,
+        "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
+                     "unit": runit, "frac": achieved / peak,
+                     "traffic": traffic_from_profiles(wl.name, dom)},
+    }
+
+    if args.copy_calibration:
+        x = torch.empty(256 * 2**20 // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        y = torch.empty_like(x)
+        y.copy_(x)
+        torch.cuda.synchronize()
+
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds)
+    plan.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -6,8 +6,10 @@
  *
  *   S1  per depth, the top-M marginal candidates and the tail log-sum-exp
  *       (Alg. 1 step 1; section 3.2, candidate restriction);
- *   S2  the candidate embedding rows folded through the GRU input projection
- *       and the correction head (section 3.2: gather the M rows once per depth);
+ *   S2  the rows of the GRU input projection and of the correction head that
+ *       the candidates need (section 3.2: gather the M rows once per depth);
+ *       they depend on the model only, so the plan folds them for the whole
+ *       vocabulary once and each call gathers them;
  *   S3  the root's children (Alg. 1 steps 2-3);
  *   S4  best-first expansion: pop, advance the GRU along the node's own path,
  *       score the next depth's slice with the path-dependent correction, push
@@ -126,7 +128,12 @@ const char *dt_status_string(int status);
 const char *dt_last_error(void);
 
 /* Create a plan for one model and one (L, M, B) shape.
- *   emb:  [V, d_e] token-embedding table (caller-owned, must outlive the plan);
+ * The plan folds the embedding table through the GRU input projection and the
+ * correction head for every token (W_ih E[v] + b_ih, W_c^T E[v], E[v] . b_c),
+ * held in fp32: V * (4 d_h + 1) * 4 bytes of plan-owned device memory
+ * (1.24 GB for Qwen3's vocabulary at d_h = 512).
+ *   emb:  [V, d_e] token-embedding table (caller-owned; only read while the
+ *         plan is created);
  *   gru, head: the Domino encoder and correction head (copied and repacked
  *         into plan-owned device memory; the caller may free them afterwards);
  *   weights_dtype: dtype of emb, GRU and head tensors;
@@ -153,6 +160,15 @@ dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, c
 
 /* Release the plan's device memory (NULL is ignored). */
 void dt_plan_destroy(dt_plan *plan);
+
+/* Stage timing (measurement aid).  When enabled, dt_build_tree records a HIP
+ * event on its stream before its first kernel and after each kernel:
+ * stage 0 = scan of the logit chunks, 1 = per-row merge, 2 = expansion and
+ * emission.  dt_plan_stage_ms waits for the last call's final event and writes
+ * the 3 stage durations in milliseconds to ms[0..2].
+ * Returns DT_ERR_SHAPE if no profiled call has been made yet. */
+dt_status dt_plan_set_profiling(dt_plan *plan, int enable);
+dt_status dt_plan_stage_ms(dt_plan *plan, float *ms);
 
 /* Workspace (bytes) for dt_scan_topm over `rows` rows. */
 dt_status dt_scan_workspace_size(int rows, int V, int M, size_t *bytes);

@@ -28,8 +28,9 @@ STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
 
 # every symbol include/dominotree.h declares
 EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_create",
-           "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_scan_workspace_size",
-           "dt_scan_topm")
+           "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
+           "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm")
+STAGES = ("scan_chunks", "scan_merge", "expand")
 
 
 class DTError(RuntimeError):
@@ -85,6 +86,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dt_build_tree.argtypes = [vp, vp, ci, vp, cf, vp, sz, ctypes.POINTER(dt_tree), vp]
     lib.dt_plan_destroy.restype = None
     lib.dt_plan_destroy.argtypes = [vp]
+    lib.dt_plan_set_profiling.restype = ci
+    lib.dt_plan_set_profiling.argtypes = [vp, ci]
+    lib.dt_plan_stage_ms.restype = ci
+    lib.dt_plan_stage_ms.argtypes = [vp, ctypes.POINTER(ctypes.c_float)]
     lib.dt_scan_workspace_size.restype = ci
     lib.dt_scan_workspace_size.argtypes = [ci, ci, ci, ctypes.POINTER(sz)]
     lib.dt_scan_topm.restype = ci
@@ -199,6 +204,15 @@ class Plan:
                                        ctypes.c_float(T), _ptr(ws), ws.numel(), ctypes.byref(c),
                                        _stream(stream)))
         return out
+
+    def set_profiling(self, enable: bool) -> None:
+        _check(self._lib.dt_plan_set_profiling(self.handle, int(enable)))
+
+    def stage_ms(self) -> dict:
+        """Durations (ms) of the last profiled call's kernels (waits for it)."""
+        ms = (ctypes.c_float * 3)()
+        _check(self._lib.dt_plan_stage_ms(self.handle, ms))
+        return dict(zip(STAGES, list(ms)))
 
     def close(self) -> None:
         if getattr(self, "handle", None):

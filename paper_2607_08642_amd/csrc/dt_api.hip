@@ -54,10 +54,6 @@ Workspace carve(const dt_plan *p, int batch, char *base) {
     o += align_up(bytes, 256);
     return ptr;
   };
-  const size_t rm = (size_t)rows * p->M;
-  ws.P = at(rm * 3 * p->d_h * sizeof(float));
-  ws.U = at(rm * p->d_h * sizeof(float));
-  ws.cvec = at(rm * sizeof(float));
   ws.ecap = ecap_for(p);
   ws.states = at((size_t)batch * ws.ecap * p->d_h * sizeof(float));
   ws.bytes = o;
@@ -153,8 +149,16 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (e == hipSuccess) e = hipMalloc(&p->b_hh, sizeof(float) * 3 * d_h);
   if (e == hipSuccess) e = hipMalloc(&p->b_c, sizeof(float) * d_e);
   if (e == hipSuccess) e = hipMalloc(&p->whh_t, (size_t)3 * d_h * d_h * ws);
+  if (e == hipSuccess) e = hipMalloc(&p->P_all, (size_t)V * 3 * d_h * sizeof(float));
+  if (e == hipSuccess) e = hipMalloc(&p->U_all, (size_t)V * d_h * sizeof(float));
+  if (e == hipSuccess) e = hipMalloc(&p->c_all, (size_t)V * sizeof(float));
   if (e == hipSuccess) e = dt::pack_weights(p, gru, head, nullptr);
+  if (e == hipSuccess) e = dt::fold_vocab(p, nullptr);
   if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  if (e == hipSuccess) {
+    e = hipFree(p->wfold);
+    p->wfold = nullptr;
+  }
   if (e != hipSuccess) {
     dt_status st = hip_fail(e, "plan creation");
     dt_plan_destroy(p);
@@ -164,13 +168,41 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   return DT_OK;
 }
 
+dt_status dt_plan_set_profiling(dt_plan *p, int enable) {
+  if (!p) return fail(DT_ERR_NULL, "plan is required");
+  if (enable && !p->ev[0]) {
+    for (int i = 0; i < 4; ++i) {
+      hipError_t e = hipEventCreate(&p->ev[i]);
+      if (e != hipSuccess) return hip_fail(e, "event create");
+    }
+  }
+  p->profiling = enable ? 1 : 0;
+  p->profiled_calls = 0;
+  return DT_OK;
+}
+
+dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
+  if (!p || !ms) return fail(DT_ERR_NULL, "plan and ms are required");
+  if (!p->ev[0] || p->profiled_calls == 0)
+    return fail(DT_ERR_SHAPE, "no profiled dt_build_tree call yet");
+  hipError_t e = hipEventSynchronize(p->ev[3]);
+  for (int i = 0; i < 3 && e == hipSuccess; ++i) e = hipEventElapsedTime(&ms[i], p->ev[i], p->ev[i + 1]);
+  if (e != hipSuccess) return hip_fail(e, "event timing");
+  return DT_OK;
+}
+
 void dt_plan_destroy(dt_plan *p) {
   if (!p) return;
+  for (int i = 0; i < 4; ++i)
+    if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
   if (p->wfold) (void)hipFree(p->wfold);
   if (p->b_ih) (void)hipFree(p->b_ih);
   if (p->b_hh) (void)hipFree(p->b_hh);
   if (p->b_c) (void)hipFree(p->b_c);
   if (p->whh_t) (void)hipFree(p->whh_t);
+  if (p->P_all) (void)hipFree(p->P_all);
+  if (p->U_all) (void)hipFree(p->U_all);
+  if (p->c_all) (void)hipFree(p->c_all);
   delete p;
 }
 
@@ -203,12 +235,18 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
   dt::Workspace ws = dt::carve(plan, batch, static_cast<char *>(workspace));
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
-  hipError_t e = dt::launch_scan(logits, plan->ldt, g, inv_tau, ws, s);
+  const bool prof = plan->profiling != 0;
+  hipError_t e = prof ? hipEventRecord(plan->ev[0], s) : hipSuccess;
+  if (e == hipSuccess) e = dt::launch_scan(logits, plan->ldt, g, inv_tau, ws, s, prof ? plan->ev[1] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
-  e = dt::launch_fold(plan, batch, ws, s);
-  if (e != hipSuccess) return hip_fail(e, "fold launch");
-  e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);
+  if (prof) e = hipEventRecord(plan->ev[2], s);
+  if (e == hipSuccess) e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
+  if (prof) {
+    e = hipEventRecord(plan->ev[3], s);
+    if (e != hipSuccess) return hip_fail(e, "event record");
+    plan->profiled_calls++;
+  }
   return DT_OK;
 }
 

@@ -44,9 +44,9 @@ struct ExpArgs {
   const float *candv;
   const float *tail;
   const int32_t *rflag;
-  const float *P;
-  const float *U;
-  const float *cvec;
+  const float *P_all;  // [V][3dh] W_ih E[v] + b_ih
+  const float *U_all;  // [V][dh]  W_c^T E[v]
+  const float *c_all;  // [V]      E[v] . b_c
   const void *whh;
   const float *b_hh;
   const float *h0;
@@ -326,8 +326,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       const int ngr = dh / 16;
       const int c = lane & 15;
       const int node = c < nc ? cn[c] : 0;
-      const float *prow =
-          a.P + ((size_t)(t * L + d - 1) * M + (c < nc ? nslot[node] : 0)) * (3 * dh);
+      const float *prow = a.P_all + (size_t)(c < nc ? ntok[node] : 0) * (3 * dh);
       float *srow = a.states + ((size_t)t * a.ecap + (c < nc ? nstate[node] : 0)) * dh;
       for (int u = wave; u < ngr; u += NW) {
         f32x4 gh[3];
@@ -362,10 +361,11 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       const int q0 = (nq * f) / F, q1 = (nq * (f + 1)) / F;
       const int m = rt * 16 + (lane & 15);
       const int c = lane & 15, kq = (lane >> 4) * 4;
+      const float *urow = a.U_all + (size_t)(m < M ? a.cand[rbase + m] : 0) * dh;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
       for (int q = q0; q < q1; ++q) {
         float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (m < M) av = *reinterpret_cast<const float4 *>(a.U + (rbase + m) * dh + q * 16 + kq);
+        if (m < M) av = *reinterpret_cast<const float4 *>(urow + q * 16 + kq);
         const float4 bv = *reinterpret_cast<const float4 *>(Scur + c * dh + q * 16 + kq);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
@@ -395,7 +395,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         if (m < M) {
           const float x = a.candv[rbase + m];
           if (x > NEG_INF) {
-            float dl = a.cvec[rbase + m];
+            float dl = a.c_all[a.cand[rbase + m]];
             for (int f = 0; f < F; ++f) dl += part[(f * RT * 16 + m) * CH + c];
             z = (x + dl) * a.inv_tau;
           }
@@ -717,9 +717,9 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.candv = ws.candv;
   a.tail = ws.tail;
   a.rflag = ws.row_flag;
-  a.P = ws.P;
-  a.U = ws.U;
-  a.cvec = ws.cvec;
+  a.P_all = p->P_all;
+  a.U_all = p->U_all;
+  a.c_all = p->c_all;
   a.whh = p->whh_t;
   a.b_hh = p->b_hh;
   a.h0 = h0;

@@ -1,14 +1,16 @@
-// S2: candidate gather and per-depth fold (section 3.2: the M candidate rows are
-// gathered once per depth and shared by every node at that depth).
+// Plan-time work: the vocabulary fold and weight packing.
 //
-// For every candidate row r = (tree, depth, slot) with embedding e = E[cand[r]]:
-//   P[r] = W_ih e + b_ih     (GRU input projection, 3*d_h)
-//   U[r] = W_c^T e           (so that delta = U[r] . S + c[r] = e . (W_c S + b_c))
-//   c[r] = e . b_c
-// This is one GEMM of the gathered rows against the packed matrix
+// Candidate restriction (section 3.2) gathers, once per depth, the rows of the
+// correction that the top-M candidates need.  Here the rows are model-only
+// quantities, so they are computed once per plan for the whole vocabulary and
+// every call just gathers them:
+//   P[v] = W_ih E[v] + b_ih   (GRU input projection of token v, 3*d_h)
+//   U[v] = W_c^T E[v]         (so delta(v) = U[v] . S + c[v] = E[v] . (W_c S + b_c))
+//   c[v] = E[v] . b_c
+// This is one GEMM of the embedding table against the packed matrix
 // [W_ih ; W_c^T] ([4 d_h, d_e], K = d_e contiguous).  bf16 weights run on the
 // gfx950 bf16 MFMA (exact products, fp32 accumulation); fp32 weights use a plain
-// FMA kernel.  Plan-time packing kernels also live here.
+// FMA kernel.
 #include "dt_internal.h"
 
 namespace dt {
@@ -45,7 +47,7 @@ __global__ __launch_bounds__(kFoldThreads) void fold_mfma_kernel(
 
   for (int i = tid; i < BM; i += kFoldThreads) {
     const int r = r0 + i;
-    rowtok[i] = (r < rows_total) ? cand[r] : -1;
+    rowtok[i] = (r < rows_total) ? (cand ? cand[r] : r) : -1;
   }
   __syncthreads();
 
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(256) void fold_simple_kernel(
   // one block per candidate row; threads over the nf+1 outputs
   const int r = blockIdx.x;
   if (r >= rows_total) return;
-  const int tok = cand[r];
+  const int tok = cand ? cand[r] : r;
   for (int n = threadIdx.x; n <= nf; n += blockDim.x) {
     float s = 0.0f;
     if (tok >= 0) {
@@ -289,37 +291,26 @@ hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipS
   return hipGetLastError();
 }
 
-hipError_t launch_fold(const dt_plan *p, int batch, const Workspace &ws, hipStream_t s) {
-  const int rows_total = batch * p->L * p->M;
+hipError_t fold_vocab(const dt_plan *p, hipStream_t s) {
+  const int rows_total = p->V;
   const float *bc = p->b_c;  // zeros when the head has no bias
   if (p->wdt == DT_BF16 && p->d_e % 8 == 0) {
     const int ntile_n = (p->nf + 127) / 128;
-    // 128x128 tiles when there are enough of them to fill the chip, else 64x128
-    const int t128 = ntile_n * ((rows_total + 127) / 128);
-    if (t128 >= 2 * p->num_cus) {
-      dim3 grid(ntile_n, (rows_total + 127) / 128);
-      hipLaunchKernelGGL((fold_mfma_kernel<2, 2, 2, 2>), grid, dim3(kFoldThreads), 0, s,
-                         (const uint16_t *)p->emb, ws.cand, rows_total, p->d_e,
-                         (const uint16_t *)p->wfold, p->nf, p->d_h, p->b_ih, bc, ws.P, ws.U,
-                         ws.cvec);
-    } else {
-      dim3 grid(ntile_n, (rows_total + 63) / 64);
-      hipLaunchKernelGGL((fold_mfma_kernel<1, 4, 2, 1>), grid, dim3(kFoldThreads), 0, s,
-                         (const uint16_t *)p->emb, ws.cand, rows_total, p->d_e,
-                         (const uint16_t *)p->wfold, p->nf, p->d_h, p->b_ih, bc, ws.P, ws.U,
-                         ws.cvec);
-    }
-    return hipGetLastError();
-  }
-  if (p->wdt == DT_BF16)
+    dim3 grid(ntile_n, (rows_total + 127) / 128);
+    hipLaunchKernelGGL((fold_mfma_kernel<2, 2, 2, 2>), grid, dim3(kFoldThreads), 0, s,
+                       (const uint16_t *)p->emb, nullptr, rows_total, p->d_e,
+                       (const uint16_t *)p->wfold, p->nf, p->d_h, p->b_ih, bc, p->P_all, p->U_all,
+                       p->c_all);
+  } else if (p->wdt == DT_BF16) {
     hipLaunchKernelGGL(fold_simple_kernel<uint16_t>, dim3(rows_total), dim3(256), 0, s,
-                       (const uint16_t *)p->emb, ws.cand, rows_total, p->d_e,
-                       (const uint16_t *)p->wfold, p->nf, p->d_h, p->b_ih, bc, ws.P, ws.U,
-                       ws.cvec);
-  else
+                       (const uint16_t *)p->emb, nullptr, rows_total, p->d_e,
+                       (const uint16_t *)p->wfold, p->nf, p->d_h, p->b_ih, bc, p->P_all, p->U_all,
+                       p->c_all);
+  } else {
     hipLaunchKernelGGL(fold_simple_kernel<float>, dim3(rows_total), dim3(256), 0, s,
-                       (const float *)p->emb, ws.cand, rows_total, p->d_e, (const float *)p->wfold,
-                       p->nf, p->d_h, p->b_ih, bc, ws.P, ws.U, ws.cvec);
+                       (const float *)p->emb, nullptr, rows_total, p->d_e, (const float *)p->wfold,
+                       p->nf, p->d_h, p->b_ih, bc, p->P_all, p->U_all, p->c_all);
+  }
   return hipGetLastError();
 }
 

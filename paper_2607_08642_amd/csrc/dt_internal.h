@@ -73,14 +73,21 @@ struct dt_plan {
   int V, d_e, d_h, L, M, B, k, norm_mode, pos_offset;
   int wdt, ldt, max_batch;
   const void *emb;
-  void *wfold;      // [nf_pad, d_e] (weights dtype): rows [0,3dh) = W_ih, [3dh,4dh) = W_c^T
+  void *wfold;      // [nf_pad, d_e] (weights dtype): rows [0,3dh) = W_ih, [3dh,4dh) = W_c^T;
+                    // only alive while the plan is created
+  float *P_all;     // [V][3dh]  W_ih E[v] + b_ih
+  float *U_all;     // [V][dh]   W_c^T E[v]
+  float *c_all;     // [V]       E[v] . b_c
   int nf, nf_pad;   // nf = 4*d_h
   float *b_ih;      // [3dh] fp32 (zeros when absent)
   float *b_hh;      // [3dh] fp32
   float *b_c;       // [d_e] fp32 (zeros when absent)
   int has_bc;
-  void *whh_t;      // [d_h (k)][3][d_h (unit)] weights dtype: W_hh transposed per gate
+  void *whh_t;      // W_hh in MFMA A-fragment order (see pack_whh_*_kernel)
   int num_cus;
+  int profiling;            // record stage events in dt_build_tree
+  int profiled_calls;       // calls recorded since profiling was enabled
+  hipEvent_t ev[4];         // stage boundaries of the last profiled call
 };
 
 namespace dt {
@@ -94,10 +101,6 @@ struct Workspace {
   float *candv;           // [rows][M]
   float *tail;            // [rows]
   int32_t *row_flag;      // [rows]
-  // fold
-  float *P;               // [rows*M][3dh]
-  float *U;               // [rows*M][dh]
-  float *cvec;            // [rows*M]
   // expansion
   float *states;          // [batch][ecap][dh]
   int ecap;
@@ -112,8 +115,8 @@ Workspace carve(const dt_plan *p, int batch, char *base);
 
 // kernel launchers (return hipError_t of the launch)
 hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
-                       const Workspace &ws, hipStream_t s);
-hipError_t launch_fold(const dt_plan *p, int batch, const Workspace &ws, hipStream_t s);
+                       const Workspace &ws, hipStream_t s, hipEvent_t between = nullptr);
+hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s);
 hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);

@@ -423,7 +423,7 @@ size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws) {
 }
 
 hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
-                       const Workspace &ws, hipStream_t s) {
+                       const Workspace &ws, hipStream_t s, hipEvent_t between) {
   const float c = 1.4426950408889634f * inv_tau;  // exp(x / tau) = exp2(x * c)
   dim3 grid(g.nchunks, g.rows);
   const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16) == 0;
@@ -446,6 +446,10 @@ hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (between) {
+    e = hipEventRecord(between, s);
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(scan_merge_kernel, dim3(g.rows), dim3(kScanThreads), 0, s, g, c, inv_tau,
                      ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, ws.cand, ws.candv, ws.tail,
                      ws.row_flag);

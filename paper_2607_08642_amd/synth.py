@@ -227,3 +227,32 @@ def random_small(seed: int, *, batch: int, L: int, V: int, M: int, B: int, T: fl
     if h0:
         hh = _rng(seed, TAG_H0, 0).standard_normal((batch, d_h), dtype=np.float32) * np.float32(0.5)
     return Workload(f"random{seed}", _as_dtype(x, ldt), ldt, hh, w, L, M, B, T, batch)
+
+
+# generator settings of each workload's logits, for drawing more buffers of the same kind
+LOGIT_RECIPES = {
+    "tiny": dict(seed=0, dtype=DT_F32, L=4, V=1024, n_lo=3, n_hi=3, lo=0.0, hi=0.0, fixed=10.0),
+    "qwen3_4b": dict(seed=1, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=1, n_hi=4, lo=6.0, hi=12.0,
+                     fixed=None),
+    "qwen3_8b": dict(seed=2, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=1, n_hi=4, lo=6.0, hi=12.0,
+                     fixed=None),
+    "budget64": dict(seed=3, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=4, n_hi=16, lo=3.0, hi=6.0,
+                     fixed=None),
+    "concurrent": dict(seed=4, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=1, n_hi=4, lo=6.0,
+                       hi=12.0, fixed=None),
+}
+
+
+def logits_buffer(name: str, index: int, batch: int, threads: int = 8) -> np.ndarray:
+    """[batch, L, V] logits for buffer `index` of a workload (buffer 0 = the workload's own).
+
+    Tree t of buffer i is drawn with tree index i*batch + t, so buffers never repeat.
+    """
+    r = LOGIT_RECIPES[name]
+
+    def one(t: int) -> np.ndarray:
+        return peaked_logits(r["seed"], index * batch + t, r["L"], r["V"], r["dtype"], r["n_lo"],
+                             r["n_hi"], r["lo"], r["hi"], fixed_spike=r["fixed"])
+
+    with ThreadPoolExecutor(min(threads, batch)) as ex:
+        return np.stack(list(ex.map(one, range(batch))))
