@@ -2,7 +2,7 @@
 """Benchmark of the DominoTree draft-tree builder on one MI355X.
 
 One step = one dt_build_tree call over one batch of resident synthetic logits:
-top-M scan, fold, expansion and emission (every kernel of the path).  The
+top-M scan, row merge, expansion and emission (every kernel of the path).  The
 default workload is the Qwen3-8B-shaped single stream (L=16, V=151936, M=64,
 B=16, T=1, d_e=4096, d_h=512).  Logit buffers rotate through >= 512 MB so the
 256 MB Infinity Cache cannot serve the scan.
@@ -50,10 +50,8 @@ def algorithmic(plan_cfg, stage):
     """Algorithmic work of one launch of a stage: (bytes or flops, unit, bound)."""
     c = plan_cfg
     rows = c["batch"] * c["L"]
-    if stage == "scan_chunks":
+    if stage == "scan":
         return rows * c["V"] * c["logit_bytes"], "bytes", "hbm"
-    if stage == "scan_merge":
-        return rows * c["nchunks"] * c["M"] * 8, "bytes", "hbm"
     # expansion: MFMA work of Alg. 1's expansions (GRU hidden GEMV + slice correction)
     n = c["expanded_nodes_per_call"]
     return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["M"] * c["d_h"]), "flops", "mfma"
@@ -177,16 +175,9 @@ def main():
     dep = out.depth.cpu().numpy()
     nn = out.n_nodes.cpu().numpy()
     expanded = int(sum(int(np.sum(dep[t, :nn[t]] < wl.L)) + 1 for t in range(wl.batch)))
-    # chunk count of the scan (the library's geometry rule: ~1024 workgroups,
-    # chunks a multiple of 2048 elements)
     rows = wl.batch * wl.L
-    sub = 256 * 8
-    nch = max(1, min((1024 + rows - 1) // rows, (w.V + sub - 1) // sub))
-    chunk = ((w.V + nch - 1) // nch + sub - 1) // sub * sub
-    g_nchunks = (w.V + chunk - 1) // chunk
-
     cfg = dict(batch=wl.batch, L=wl.L, V=w.V, M=wl.M, d_e=w.d_e, d_h=w.d_h,
-               logit_bytes=2 if wl.logits_dtype == synth.DT_BF16 else 4, nchunks=g_nchunks,
+               logit_bytes=2 if wl.logits_dtype == synth.DT_BF16 else 4,
                expanded_nodes_per_call=expanded)
     dom = max(stage_us, key=stage_us.get)
     work, unit, bound = algorithmic(cfg, dom)
@@ -198,7 +189,7 @@ def main():
         peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
         runit = "TFLOP/s"
     scan_bytes = rows * w.V * cfg["logit_bytes"]
-    scan_us = stage_us["scan_chunks"] + stage_us["scan_merge"]
+    scan_us = stage_us["scan"]
     trees = wl.batch * args.steps
     res = {
         "metric": "draft trees built/sec",

@@ -42,7 +42,10 @@
  *   - no C++ exception crosses this interface.
  *
  * Envelope: 1 <= M <= min(V, 256); 1 <= B <= 256; 1 <= L <= 64;
- * 32 <= d_h <= 1024 with d_h % 32 == 0; 1 <= d_e <= 8192; 1 <= V < 2^31.
+ * 32 <= d_h <= 1024 with d_h % 32 == 0; 1 <= d_e <= 8192; 1 <= V < 2^31;
+ * 14 * ceil(V / 10240) * M + 8 * M <= 98304 (bytes of the per-row merge
+ * buffer); the
+ * expansion kernel's LDS must fit the device (checked by dt_plan_create).
  */
 #ifndef DOMINOTREE_H
 #define DOMINOTREE_H
@@ -75,6 +78,8 @@ typedef enum {
                                  hundreds of exactly tied scores can cause it.  The tree
                                  is still a valid best-first tree but exact ties may be
                                  resolved differently from insertion order. */
+#define DT_TREE_TIMEOUT 0x4   /* a cross-workgroup wait gave up after its spin limit;
+                                 the tree's contents are then unspecified */
 
 /* normalisation of the corrected slice (dt_options.norm_mode) */
 #define DT_NORM_TAIL 0  /* logZ includes the uncorrected out-of-slice mass R_d */
@@ -163,9 +168,9 @@ void dt_plan_destroy(dt_plan *plan);
 
 /* Stage timing (measurement aid).  When enabled, dt_build_tree records a HIP
  * event on its stream before its first kernel and after each kernel:
- * stage 0 = scan of the logit chunks, 1 = per-row merge, 2 = expansion and
+ * stage 0 = top-M scan of the logit chunks, 1 = per-row merge, expansion and
  * emission.  dt_plan_stage_ms waits for the last call's final event and writes
- * the 3 stage durations in milliseconds to ms[0..2].
+ * the 2 stage durations in milliseconds to ms[0..1].
  * Returns DT_ERR_SHAPE if no profiled call has been made yet. */
 dt_status dt_plan_set_profiling(dt_plan *plan, int enable);
 dt_status dt_plan_stage_ms(dt_plan *plan, float *ms);

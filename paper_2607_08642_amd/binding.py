@@ -21,6 +21,7 @@ DT_NORM_TAIL = 0
 DT_NORM_SLICE = 1
 DT_TREE_NONFINITE = 0x1
 DT_TREE_TRUNCATED = 0x2
+DT_TREE_TIMEOUT = 0x4
 ABI_VERSION = 1
 
 STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
@@ -30,7 +31,7 @@ STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
 EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_create",
            "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
            "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm")
-STAGES = ("scan_chunks", "scan_merge", "expand")
+STAGES = ("scan", "expand")
 
 
 class DTError(RuntimeError):
@@ -210,7 +211,7 @@ class Plan:
 
     def stage_ms(self) -> dict:
         """Durations (ms) of the last profiled call's kernels (waits for it)."""
-        ms = (ctypes.c_float * 3)()
+        ms = (ctypes.c_float * 2)()
         _check(self._lib.dt_plan_stage_ms(self.handle, ms))
         return dict(zip(STAGES, list(ms)))
 

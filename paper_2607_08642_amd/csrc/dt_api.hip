@@ -9,10 +9,6 @@
 
 #include "dt_internal.h"
 
-namespace dt {
-size_t expand_lds_bytes(int dh, int M);
-}
-
 namespace {
 
 thread_local std::string g_last_error;
@@ -56,6 +52,8 @@ Workspace carve(const dt_plan *p, int batch, char *base) {
   };
   ws.ecap = ecap_for(p);
   ws.states = at((size_t)batch * ws.ecap * p->d_h * sizeof(float));
+  ws.part = at(expand_part_bytes(p, batch));
+  ws.bar = reinterpret_cast<int32_t *>(at((size_t)batch * kBarStride * sizeof(int32_t)));
   ws.bytes = o;
   return ws;
 }
@@ -118,9 +116,21 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return hip_fail(e, "device query");
-  if ((int)dt::expand_lds_bytes(d_h, M) > maxlds)
-    return fail(DT_ERR_UNSUPPORTED, "expansion needs %zu bytes of LDS, device has %d",
-                dt::expand_lds_bytes(d_h, M), maxlds);
+  const int nchunks = dt::scan_geom(1, V, M).nchunks;
+  if (dt::merge_lds_bytes(dt::scan_geom(1, V, M)) > (size_t)dt::kMergeLdsMax)
+    return fail(DT_ERR_UNSUPPORTED, "14 * ceil(V/%d) * M + 8 * M must stay within %d bytes",
+                dt::kScanChunk, dt::kMergeLdsMax);
+  // the expansion's LDS for every group size a batch in [1, max_batch] can use
+  size_t lds_need = 0;
+  for (int G = dt::expand_group_size(d_h, ncu, max_batch);; G *= 2) {
+    const size_t b = dt::expand_lds_bytes(d_h, G, M, nchunks);
+    lds_need = b > lds_need ? b : lds_need;
+    if (G == dt::expand_group_size(d_h, ncu, 1)) break;
+  }
+  if (lds_need > (size_t)maxlds)
+    return fail(DT_ERR_UNSUPPORTED,
+                "expansion needs %zu bytes of LDS (d_h=%d, M=%d, max_batch=%d), device has %d",
+                lds_need, d_h, M, max_batch, maxlds);
 
   dt_plan *p = new (std::nothrow) dt_plan();
   if (!p) return fail(DT_ERR_HIP, "host allocation failed");
@@ -171,7 +181,7 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
 dt_status dt_plan_set_profiling(dt_plan *p, int enable) {
   if (!p) return fail(DT_ERR_NULL, "plan is required");
   if (enable && !p->ev[0]) {
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 3; ++i) {
       hipError_t e = hipEventCreate(&p->ev[i]);
       if (e != hipSuccess) return hip_fail(e, "event create");
     }
@@ -185,15 +195,15 @@ dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
   if (!p || !ms) return fail(DT_ERR_NULL, "plan and ms are required");
   if (!p->ev[0] || p->profiled_calls == 0)
     return fail(DT_ERR_SHAPE, "no profiled dt_build_tree call yet");
-  hipError_t e = hipEventSynchronize(p->ev[3]);
-  for (int i = 0; i < 3 && e == hipSuccess; ++i) e = hipEventElapsedTime(&ms[i], p->ev[i], p->ev[i + 1]);
+  hipError_t e = hipEventSynchronize(p->ev[2]);
+  for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipEventElapsedTime(&ms[i], p->ev[i], p->ev[i + 1]);
   if (e != hipSuccess) return hip_fail(e, "event timing");
   return DT_OK;
 }
 
 void dt_plan_destroy(dt_plan *p) {
   if (!p) return;
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 3; ++i)
     if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
   if (p->wfold) (void)hipFree(p->wfold);
   if (p->b_ih) (void)hipFree(p->b_ih);
@@ -237,13 +247,15 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
   const bool prof = plan->profiling != 0;
   hipError_t e = prof ? hipEventRecord(plan->ev[0], s) : hipSuccess;
-  if (e == hipSuccess) e = dt::launch_scan(logits, plan->ldt, g, inv_tau, ws, s, prof ? plan->ev[1] : nullptr);
+  // the scan kernel also clears the expansion kernel's barrier counters
+  if (e == hipSuccess)
+    e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, batch * dt::kBarStride, s);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
-  if (prof) e = hipEventRecord(plan->ev[2], s);
+  if (prof) e = hipEventRecord(plan->ev[1], s);
   if (e == hipSuccess) e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   if (prof) {
-    e = hipEventRecord(plan->ev[3], s);
+    e = hipEventRecord(plan->ev[2], s);
     if (e != hipSuccess) return hip_fail(e, "event record");
     plan->profiled_calls++;
   }
@@ -254,6 +266,8 @@ dt_status dt_scan_workspace_size(int rows, int V, int M, size_t *bytes) {
   if (!bytes) return fail(DT_ERR_NULL, "bytes is required");
   if (rows < 1 || V < 1 || M < 1 || M > V) return fail(DT_ERR_SHAPE, "need rows, V >= 1 and 1 <= M <= V");
   if (M > dt::kMaxM) return fail(DT_ERR_UNSUPPORTED, "M must be <= 256");
+  if (dt::merge_lds_bytes(dt::scan_geom(rows, V, M)) > (size_t)dt::kMergeLdsMax)
+    return fail(DT_ERR_UNSUPPORTED, "V and M too large for the row merge");
   *bytes = dt::scan_bytes(dt::scan_geom(rows, V, M));
   return DT_OK;
 }
@@ -268,6 +282,8 @@ dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, in
   if (M > dt::kMaxM) return fail(DT_ERR_UNSUPPORTED, "M must be <= 256");
   if (!(T == T)) return fail(DT_ERR_SHAPE, "temperature is NaN");
   const dt::ScanGeom g = dt::scan_geom(rows, V, M);
+  if (dt::merge_lds_bytes(g) > (size_t)dt::kMergeLdsMax)
+    return fail(DT_ERR_UNSUPPORTED, "V and M too large for the row merge");
   const size_t need = dt::scan_bytes(g);
   if (!workspace || ws_bytes < need)
     return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
@@ -282,7 +298,9 @@ dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, in
   ws.tail = tail_lse;
   ws.row_flag = row_flags;
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
-  hipError_t e = dt::launch_scan(logits, logits_dtype, g, inv_tau, ws, static_cast<hipStream_t>(stream));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = dt::launch_scan_chunks(logits, logits_dtype, g, inv_tau, ws, nullptr, 0, s);
+  if (e == hipSuccess) e = dt::launch_scan_merge(g, inv_tau, ws, s);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
   return DT_OK;
 }

@@ -1,28 +1,36 @@
 // S3-S5: best-first conditional expansion and emission (Alg. 1 steps 2-4;
-// section 3.1 conditional children; section 3.5 verification mask).
+// section 3.1 conditional children; section 3.5 verification mask), preceded
+// by the per-row merge of the scan (Alg. 1 step 1).
 //
-// One workgroup (1024 threads) builds one tree.  The heap of Alg. 1 pops nodes
-// in non-increasing score order, and a child never scores above its parent
-// (log-probs are <= 0), so the popped set is the top-B of the candidate tree
-// (the frontier argument of Appendix B).  A node whose score is below the B-th
-// best score already known can therefore never be popped.  The kernel uses this
-// in two phases:
+// The heap of Alg. 1 pops nodes in non-increasing score order, and a child
+// never scores above its parent (log-probs are <= 0), so the popped set is the
+// top-B of the candidate tree (the frontier argument of Appendix B).  A node
+// scoring below the B-th best score already known can never be popped.  The
+// kernel uses this in two phases:
 //
-//  A. Speculative, depth-synchronous expansion.  Starting from the root's
-//     children, every known node that is not expanded, is above depth L, and
-//     scores at least the current B-th best known score is expanded, a batch of
-//     up to 16 nodes at a time: the GRU advances its path state (split-bf16
-//     MFMA against the packed W_hh, fp32 accumulation), the correction of the
-//     next depth's slice is one fp32 MFMA against the folded U rows, and the
-//     top-k children are appended.  This repeats until no node qualifies; every
-//     node the heap can pop below depth L is then expanded.
+//  A. Speculative, depth-synchronous expansion.  Starting from the root,
+//     every known node that is not expanded, is above depth L and scores at
+//     least the current B-th best known score is expanded, up to 16 nodes at a
+//     time: the GRU advances its path state (split-bf16 MFMA against W_hh,
+//     fp32 accumulation; fp32 MFMA for fp32 weights), the correction of the next
+//     depth's slice is an fp32 MFMA against the gathered rows U[v] = W_c^T E[v],
+//     and the top-k children are appended.  This repeats until no node
+//     qualifies; every node the heap can pop below depth L is then expanded.
 //  B. Exact replay of the heap: B pops by (score desc, insertion order asc),
 //     where insertion order is (parent's pop index, child rank) -- the order in
 //     which Alg. 1 pushes.  Ties therefore resolve exactly as in the heap.
 //
-// Emission writes the popped nodes in pop order with parent pop indices,
-// depths, position ids, scores and the ancestor-or-self mask.
-#include "dt_internal.h"
+// A tree is built by a group of G workgroups.  Member j owns hidden units
+// [j*d_h/G, (j+1)*d_h/G): it advances those units of every path state and
+// forms the part of each correction dot product that runs over them.  The
+// parts meet through global memory with device-scope (sc1) stores and
+// vectorised device-scope buffer loads, after a relaxed-atomic counter barrier
+// per expansion step; every member then
+// sums the parts in the same order and runs the same bookkeeping, so all
+// members hold identical node tables without further exchange.  The members
+// of a group are placed on one XCD (blocks are dealt to XCDs round-robin).
+// Member 0 replays the heap and emits the tree.
+#include "dt_select.h"
 
 namespace dt {
 
@@ -35,22 +43,28 @@ constexpr int NT = kExpThreads;
 constexpr int NW = NT / 64;
 constexpr int NC = kNodeCap;
 constexpr int CH = kChunkNodes;
+constexpr int kSpinLimit = 1 << 18;  // ~0.3 s: a wait this long means a fault
 static_assert(CH == 16, "MFMA column count");
 
 struct ExpArgs {
-  int L, M, B, k, dh, norm_mode, pos_offset, ecap, batch;
-  float inv_tau;
-  const int32_t *cand;
-  const float *candv;
-  const float *tail;
-  const int32_t *rflag;
+  int L, M, B, k, dh, G, norm_mode, pos_offset, ecap, batch, nchunks, nxcd;
+  float inv_tau, c2;  // c2 = log2(e) / tau
+  const uint64_t *ckeys;
+  const float2 *ctail;
+  const int32_t *cflag;
+  int32_t *cand;   // [rows][M] merged rows (written by the group, read by all members)
+  float *candv;    // [rows][M]
+  float *tailR;    // [rows]
+  int32_t *rflag;  // [rows]
   const float *P_all;  // [V][3dh] W_ih E[v] + b_ih
   const float *U_all;  // [V][dh]  W_c^T E[v]
   const float *c_all;  // [V]      E[v] . b_c
   const void *whh;
   const float *b_hh;
   const float *h0;
-  float *states;
+  float *states;   // [batch][ecap][dh]
+  float *part;     // [batch][2][G][CH][MP] partial corrections
+  int32_t *bar;    // [batch][kBarStride] barrier counters (zeroed by the scan kernel)
   dt_tree out;
 };
 
@@ -58,17 +72,23 @@ struct ExpArgs {
 struct Lds {
   int ng, ntok, nparent, nstate, nslot, ndepth, nrank, nexp, newidx, elist;
   int ins, popd, ppi, order, anc;
-  int Sp, Sn, part, ell, rnk, chunk, scal, total;
+  int rcand, rcandv;  // the merged row of the depth being expanded
+  int gpart, Sp, Sn, ell, rnk, chunk, scal, total;
+  int sortbuf;  // aliases gpart.. (prologue only)
 };
 
-__host__ __device__ inline Lds lds_layout(int dh, int M) {
+__host__ __device__ inline int mp_of(int M) { return (M + 63) / 64 * 64; }
+
+__host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks) {
   Lds l;
   int o = 0;
   auto take = [&](int bytes) {
-    int r = o;
+    const int r = o;
     o += (bytes + 15) / 16 * 16;
     return r;
   };
+  const int MP = mp_of(M);
+  const int UW = dh / G;
   l.ng = take(NC * 4);
   l.ntok = take(NC * 4);
   l.nparent = take(NC * 2);
@@ -84,20 +104,26 @@ __host__ __device__ inline Lds lds_layout(int dh, int M) {
   l.ppi = take(NC * 2);
   l.order = take(kMaxB * 2);
   l.anc = take(kMaxB * 8 * 4);
-  l.Sp = take(CH * dh * 4);
-  l.Sn = take(CH * dh * 4);
-  l.part = take(NW * 16 * CH * 4);
-  const int MP = (M + 63) / 64 * 64;
-  l.ell = take(CH * MP * 4);
-  l.rnk = take(CH * MP * 2);
+  l.rcand = take(MP * 4);
+  l.rcandv = take(MP * 4);
   l.chunk = take(CH * 2);
   l.scal = take(64 * 4);
+  // region reused by the prologue's merge
+  const int reuse = o;
+  l.gpart = take(UW / 16 < NW ? NW * 3 * 256 * 4 : 0);  // k-split partial gates
+  l.Sp = take(CH * dh * 4);
+  l.Sn = take(CH * UW * 4);
+  l.ell = take(CH * MP * 4);
+  l.rnk = take(CH * MP * 2);
+  const int sortb = sel::merge_buf_bytes(nchunks, M);  // merge_row's buffer
+  l.sortbuf = reuse;
+  if (reuse + sortb > o) o = reuse + sortb;
   l.total = o;
   return l;
 }
 
 // scalar slots in LDS
-enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_CNT0 };
+enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_CNT0 };
 
 __device__ inline uint16_t f2bf(float x) {
   uint32_t u = __float_as_uint(x);
@@ -113,38 +139,72 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+template <typename T>
+__device__ inline T ld_dev(const T *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ inline void st_dev(T *p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Device-scope (sc1) vector loads of data other workgroups wrote.  Plain
+// (non-atomic) buffer loads, so the compiler batches them; `base` must be
+// uniform across the wave, the byte offset may vary per lane.
+__device__ inline __amdgpu_buffer_rsrc_t dev_rsrc(const void *base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7FFFFFF0, 0x00020000);
+}
+constexpr int kSc1 = 16;  // cache-policy bit: device scope
+__device__ inline float4 ld_dev16(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kSc1));
+}
+__device__ inline float ld_dev4(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, kSc1));
+}
+
 __device__ inline uint64_t wave_max_u64(uint64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    uint64_t p = __shfl_xor(v, o);
+    const uint64_t p = __shfl_xor(v, o);
     v = p > v ? p : v;
   }
   return v;
 }
+// Wave-wide reductions with DPP inside each row of 16 lanes (quad swaps, half
+// mirror, mirror) and four lane reads across rows; every lane gets the same
+// value.  The whole wave must be active.
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xF, 0xF, false));
+}
+template <typename Op>
+__device__ inline float wave_reduce(float v, Op op) {
+  v = op(v, dpp_f<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = op(v, dpp_f<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = op(v, dpp_f<0x141>(v));  // row_half_mirror
+  v = op(v, dpp_f<0x140>(v));  // row_mirror
+  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return op(op(a, b), op(c, d));
+}
 __device__ inline float wave_max_f(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  return wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
 }
 __device__ inline float wave_sum_f(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  return wave_reduce(v, [](float x, float y) { return x + y; });
 }
 __device__ inline float wave_min_f(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
-  return v;
+  return wave_reduce(v, [](float x, float y) { return fminf(x, y); });
 }
 
-// ordered, exclusive prefix over a predicate evaluated for i = tid + NT*r;
-// returns the position of element i among the true ones and the total
+// ordered exclusive prefix of a predicate over the block (wcnt: NW ints in LDS)
 struct Compact {
   int pos;
   int total;
 };
-
-__device__ inline Compact block_compact(bool pred, int *wcnt /* NW+1 ints in LDS */) {
+__device__ inline Compact block_compact(bool pred, int *wcnt) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const uint64_t b = __ballot(pred);
   const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
@@ -157,73 +217,103 @@ __device__ inline Compact block_compact(bool pred, int *wcnt /* NW+1 ints in LDS
     tot += c;
   }
   __syncthreads();
-  Compact r;
-  r.pos = base + __popcll(b & below);
-  r.total = tot;
-  return r;
+  return Compact{base + (int)__popcll(b & below), tot};
 }
 
-template <typename TW>
-struct WhhOps;
+// Relaxed-atomic barrier of the G members of a tree.  Each thread first waits
+// for its own stores (device-scope stores are then visible at device scope).
+__device__ inline void group_barrier(int32_t *ctr, int G, int &nbar, int *status) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  ++nbar;
+  if (G > 1 && threadIdx.x == 0) {
+    __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int target = G * nbar;
+    int spins = 0;
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (++spins > kSpinLimit) {
+        *status |= DT_TREE_TIMEOUT;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+}
 
-// bf16 weights: 16x16x32 bf16 MFMA, path state split as hi + mid + lo
+// W_hh . S for one group of 16 hidden units (gates r, z, n) over ks in [ks0, ks1).
+// B operand: lane l holds S[node l%16][32 ks + 8 (l/16) + e] from the LDS
+// staging of the parent states (row stride dh).
+template <typename TW>
+struct Gates;
+
 template <>
-struct WhhOps<uint16_t> {
-  static __device__ inline void gates(const ExpArgs &a, const float *Sp, int u, f32x4 (&acc)[3]) {
+struct Gates<uint16_t> {  // bf16 W_hh: 16x16x32 bf16 MFMA, S split as hi + mid + lo
+  static __device__ inline void run(const ExpArgs &a, const float *Sp, int u, int ks0, int ks1,
+                                    f32x4 (&acc)[3]) {
     const int lane = threadIdx.x & 63;
-    const int dh = a.dh, nks = dh / 32;
+    const int nks = a.dh / 32;
     const uint4 *W = static_cast<const uint4 *>(a.whh);
-    const int c = lane & 15, kq = (lane >> 4) * 8;
+    const float *srow = Sp + (lane & 15) * a.dh + (lane >> 4) * 8;
 #pragma unroll
     for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < nks; ++ks) {
-      const float *s = Sp + c * dh + ks * 32 + kq;
-      const float4 s0 = *reinterpret_cast<const float4 *>(s);
-      const float4 s1 = *reinterpret_cast<const float4 *>(s + 4);
-      const float x[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-      bf16x8 hi, mi, lo;
+    constexpr int PF = 2;  // k-steps of weights in flight at once
+    for (int k0 = ks0; k0 < ks1; k0 += PF) {
+      uint4 wv[PF][3];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint16_t h = f2bf(x[e]);
-        const float r1 = x[e] - bf2f(h);
-        const uint16_t m = f2bf(r1);
-        const float r2 = r1 - bf2f(m);
-        const uint16_t l = f2bf(r2);
-        hi[e] = __builtin_bit_cast(__bf16, h);
-        mi[e] = __builtin_bit_cast(__bf16, m);
-        lo[e] = __builtin_bit_cast(__bf16, l);
-      }
+      for (int kk = 0; kk < PF; ++kk)
 #pragma unroll
-      for (int g = 0; g < 3; ++g) {
-        const uint4 wv = W[((size_t)(u * 3 + g) * nks + ks) * 64 + lane];
-        const bf16x8 wa = __builtin_bit_cast(bf16x8, wv);
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, lo, acc[g], 0, 0, 0);
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, mi, acc[g], 0, 0, 0);
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, hi, acc[g], 0, 0, 0);
+        for (int g = 0; g < 3; ++g)
+          if (k0 + kk < ks1) wv[kk][g] = W[((size_t)(u * 3 + g) * nks + k0 + kk) * 64 + lane];
+#pragma unroll
+      for (int kk = 0; kk < PF; ++kk) {
+        if (k0 + kk >= ks1) break;
+        const int ks = k0 + kk;
+        const float4 s0 = *reinterpret_cast<const float4 *>(srow + ks * 32);
+        const float4 s1 = *reinterpret_cast<const float4 *>(srow + ks * 32 + 4);
+        const float x[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        bf16x8 hi, mi, lo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint16_t h = f2bf(x[e]);
+          const float r1 = x[e] - bf2f(h);
+          const uint16_t m = f2bf(r1);
+          const uint16_t l = f2bf(r1 - bf2f(m));
+          hi[e] = __builtin_bit_cast(__bf16, h);
+          mi[e] = __builtin_bit_cast(__bf16, m);
+          lo[e] = __builtin_bit_cast(__bf16, l);
+        }
+#pragma unroll
+        for (int g = 0; g < 3; ++g) {
+          const bf16x8 wa = __builtin_bit_cast(bf16x8, wv[kk][g]);
+          acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, lo, acc[g], 0, 0, 0);
+          acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, mi, acc[g], 0, 0, 0);
+          acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, hi, acc[g], 0, 0, 0);
+        }
       }
     }
   }
 };
 
-// fp32 weights: 16x16x4 fp32 MFMA, four per k-group of 16
 template <>
-struct WhhOps<float> {
-  static __device__ inline void gates(const ExpArgs &a, const float *Sp, int u, f32x4 (&acc)[3]) {
+struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per ks
+  static __device__ inline void run(const ExpArgs &a, const float *Sp, int u, int ks0, int ks1,
+                                    f32x4 (&acc)[3]) {
     const int lane = threadIdx.x & 63;
-    const int dh = a.dh, nq = dh / 16;
+    const int nq = a.dh / 16;
     const float4 *W = static_cast<const float4 *>(a.whh);
-    const int c = lane & 15, kq = (lane >> 4) * 4;
+    const float *srow = Sp + (lane & 15) * a.dh + (lane >> 4) * 4;
 #pragma unroll
     for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int q = 0; q < nq; ++q) {
-      const float4 b = *reinterpret_cast<const float4 *>(Sp + c * dh + q * 16 + kq);
+    for (int q = 2 * ks0; q < 2 * ks1; ++q) {
+      const float4 x = *reinterpret_cast<const float4 *>(srow + q * 16);
 #pragma unroll
       for (int g = 0; g < 3; ++g) {
         const float4 wv = W[((size_t)(u * 3 + g) * nq + q) * 64 + lane];
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.x, b.x, acc[g], 0, 0, 0);
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.y, b.y, acc[g], 0, 0, 0);
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.z, b.z, acc[g], 0, 0, 0);
-        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.w, b.w, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.x, x.x, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.y, x.y, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.z, x.z, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv.w, x.w, acc[g], 0, 0, 0);
       }
     }
   }
@@ -232,7 +322,7 @@ struct WhhOps<float> {
 template <typename TW>
 __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const Lds ly = lds_layout(a.dh, a.M);
+  const Lds ly = lds_layout(a.dh, a.G, a.M, a.nchunks);
   float *ng = reinterpret_cast<float *>(smem + ly.ng);
   int32_t *ntok = reinterpret_cast<int32_t *>(smem + ly.ntok);
   int16_t *nparent = reinterpret_cast<int16_t *>(smem + ly.nparent);
@@ -248,24 +338,69 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int16_t *ppi = reinterpret_cast<int16_t *>(smem + ly.ppi);
   int16_t *order = reinterpret_cast<int16_t *>(smem + ly.order);
   uint32_t *anc = reinterpret_cast<uint32_t *>(smem + ly.anc);
+  float *gpart = reinterpret_cast<float *>(smem + ly.gpart);
   float *Sp = reinterpret_cast<float *>(smem + ly.Sp);
   float *Sn = reinterpret_cast<float *>(smem + ly.Sn);
-  float *part = reinterpret_cast<float *>(smem + ly.part);
   float *ell = reinterpret_cast<float *>(smem + ly.ell);
   int16_t *rnk = reinterpret_cast<int16_t *>(smem + ly.rnk);
+  int32_t *rcand = reinterpret_cast<int32_t *>(smem + ly.rcand);
+  float *rcandv = reinterpret_cast<float *>(smem + ly.rcandv);
   int16_t *cl = reinterpret_cast<int16_t *>(smem + ly.chunk);
   int *scal = reinterpret_cast<int *>(smem + ly.scal);
   float *scalf = reinterpret_cast<float *>(smem + ly.scal);
-  int *wcnt = scal + 32;
+  int *wcnt = scal + 48;
+  uint64_t *sortbuf = reinterpret_cast<uint64_t *>(smem + ly.sortbuf);
+  float2 *red = reinterpret_cast<float2 *>(scal + 32);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t = blockIdx.x;
-  const int L = a.L, M = a.M, B = a.B, dh = a.dh;
-  const int MP = (M + 63) / 64 * 64;
+  const int L = a.L, M = a.M, B = a.B, dh = a.dh, G = a.G;
+  const int MP = mp_of(M);
+  const int UW = dh / G;       // hidden units of this member
+  const int NG = UW / 16;      // unit groups of this member
   const float NEG_INF = -__builtin_huge_valf();
-  // nodes per chunk, so that one chunk's children (<= k each) fit the table
+
+  // ---- which tree, which member (members of a tree share an XCD) ------------
+  int t, member;
+  if (G > 1) {
+    const int xcd = blockIdx.x % a.nxcd, kk = blockIdx.x / a.nxcd;
+    t = xcd + a.nxcd * (kk / G);
+    member = kk % G;
+  } else {
+    t = blockIdx.x;
+    member = 0;
+  }
+  if (t >= a.batch) return;
+  int32_t *ctr = a.bar + t * kBarStride;
+  int nbar = 0;
+  const int u0 = member * NG;  // first unit group of this member
+
   int chunk_cap = (NC - B - 64) / a.k;
   chunk_cap = chunk_cap > CH ? CH : (chunk_cap < 1 ? 1 : chunk_cap);
+
+  if (tid == 0) {
+    scal[S_STATUS] = 0;
+    scal[S_NN] = 0;
+    scalf[S_VB] = NEG_INF;
+    scal[S_NEXP] = 0;
+    scal[S_STOP] = 0;
+  }
+  __syncthreads();
+
+  // ---- prologue: merge this member's rows of the scan ------------------------
+  for (int d = member; d < L; d += G) {
+    const int row = t * L + d;
+    sel::merge_row<NT, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+                             a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
+                             a.c2, a.inv_tau, sortbuf, red, &scal[S_MERGEFLAG],
+                             a.cand + (size_t)row * M, a.candv + (size_t)row * M, a.tailR + row,
+                             a.rflag + row, a.c_all);
+  }
+  group_barrier(ctr, G, nbar, &scal[S_STATUS]);
+  {
+    const int f = tid < L ? ld_dev(a.rflag + (size_t)t * L + tid) : 0;
+    if (f) atomicOr(&scal[S_STATUS], f);
+  }
+  __syncthreads();
 
   dt_tree o = a.out;
   int32_t *otok = o.tokens + (size_t)t * B;
@@ -275,18 +410,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   float *osc = o.scores + (size_t)t * B;
   uint8_t *omask = o.mask + (size_t)t * B * B;
 
-  // ---- per-tree data errors -------------------------------------------------
-  if (tid == 0) {
-    int f = 0;
-    for (int d = 0; d < L; ++d) f |= a.rflag[t * L + d];
-    scal[S_STATUS] = f;
-    scal[S_NN] = 0;
-    scalf[S_VB] = NEG_INF;
-    scal[S_NEXP] = 0;
-    scal[S_STOP] = 0;
-  }
-  __syncthreads();
   if (scal[S_STATUS] & DT_TREE_NONFINITE) {
+    if (member != 0) return;
     for (int i = tid; i < B; i += NT) {
       otok[i] = -1;
       opar[i] = -1;
@@ -302,90 +427,159 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     return;
   }
 
-  // ---- expand one chunk of nodes (all at depth d; d = 0 is the root) -------
+  // ---- one expansion step: up to 16 nodes, all at depth d (d = 0: the root) ---
+  int pb = 0;  // partial-buffer parity
   auto expand_chunk = [&](const int16_t *cn, int nc, int d) {
-    // 1. path states of the parents (root: h0)
-    for (int idx = tid; idx < CH * dh; idx += NT) {
-      const int c = idx / dh, j = idx % dh;
-      float v = 0.0f;
-      if (c < nc) {
-        const int par = (d == 0) ? -1 : nparent[cn[c]];
-        if (par < 0)
-          v = a.h0 ? a.h0[(size_t)t * dh + j] : 0.0f;
-        else
-          v = a.states[((size_t)t * a.ecap + nstate[par]) * dh + j];
+    // one batched round trip: the merged row of depth d (the children's
+    // candidates and tail) and the parent path states of the chunk's nodes
+    const int32_t *ccand = rcand;
+    const float *ccandv = rcandv;
+    if (tid == 0 && d > 0)
+      for (int c = 0; c < nc; ++c) nstate[cn[c]] = (int16_t)(scal[S_NEXP] + c);
+    {
+      // all loads are issued before the first LDS write (one wait)
+      const size_t row = (size_t)t * L + (d < L ? d : 0);
+      const __amdgpu_buffer_rsrc_t rc = dev_rsrc(a.cand + row * M);
+      const __amdgpu_buffer_rsrc_t rv = dev_rsrc(a.candv + row * M);
+      const __amdgpu_buffer_rsrc_t rs = dev_rsrc(a.states + (size_t)t * a.ecap * dh);
+      const bool rowld = d < L && tid < M;
+      int32_t cid = 0;
+      float cval = NEG_INF, rt = NEG_INF;
+      if (rowld) {
+        cid = __builtin_bit_cast(int32_t, ld_dev4(rc, tid * 4));
+        cval = ld_dev4(rv, tid * 4);
       }
-      Sp[idx] = v;
-    }
-    if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
-    __syncthreads();
-    // 2. GRU along each node's own path (Domino's causal encoder); each wave
-    //    owns whole groups of 16 hidden units, so it can finish a group alone
-    const float *Scur = Sp;  // state the children are scored from
-    if (d > 0) {
-      const int ngr = dh / 16;
-      const int c = lane & 15;
-      const int node = c < nc ? cn[c] : 0;
-      const float *prow = a.P_all + (size_t)(c < nc ? ntok[node] : 0) * (3 * dh);
-      float *srow = a.states + ((size_t)t * a.ecap + (c < nc ? nstate[node] : 0)) * dh;
-      for (int u = wave; u < ngr; u += NW) {
-        f32x4 gh[3];
-        WhhOps<TW>::gates(a, Sp, u, gh);
-        if (c < nc) {
+      if (d < L && tid == NT - 1) rt = ld_dev(a.tailR + row);
+      constexpr int kSpPer = CH * kMaxDh / 4 / NT;  // float4 per thread, at most
+      const int nv = d > 0 ? CH * dh / 4 : 0;
+      float4 v[kSpPer];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int j = 16 * u + (lane >> 4) * 4 + i;
-            const float hr = gh[0][i] + a.b_hh[j];
-            const float hz = gh[1][i] + a.b_hh[dh + j];
-            const float hn = gh[2][i] + a.b_hh[2 * dh + j];
-            const float r = sigmoidf_(prow[j] + hr);
-            const float z = sigmoidf_(prow[dh + j] + hz);
-            const float n = tanhf(prow[2 * dh + j] + r * hn);
-            const float sv = (1.0f - z) * n + z * Sp[c * dh + j];
-            Sn[c * dh + j] = sv;
-            srow[j] = sv;
+      for (int j = 0; j < kSpPer; ++j) {
+        const int i = tid + j * NT;
+        v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i < nv) {
+          const int c = (i * 4) / dh, k = (i * 4) % dh;
+          if (c < nc) {
+            const int par = nparent[cn[c]];
+            if (par >= 0)
+              v[j] = ld_dev16(rs, (nstate[par] * dh + k) * 4);
+            else if (a.h0)
+              v[j] = *reinterpret_cast<const float4 *>(a.h0 + (size_t)t * dh + k);
           }
         }
       }
-      __syncthreads();
-      Scur = Sn;
+      if (tid < MP) {
+        rcand[tid] = rowld ? cid : 0;
+        rcandv[tid] = rowld ? cval : NEG_INF;
+      }
+      if (tid == NT - 1) scalf[S_R] = rt;
+#pragma unroll
+      for (int j = 0; j < kSpPer; ++j) {
+        const int i = tid + j * NT;
+        if (i < nv) *reinterpret_cast<float4 *>(Sp + i * 4) = v[j];
+      }
     }
+    __syncthreads();
+    // 1. path states of this member's units: S = GRU(S_parent, E[token]) (section 2.3)
+    if (d == 0) {
+      for (int u = tid; u < UW; u += NT) {
+        const int j = member * UW + u;
+        for (int c = 0; c < CH; ++c) Sn[c * UW + u] = (c == 0 && a.h0) ? a.h0[(size_t)t * dh + j] : 0.0f;
+      }
+    } else {
+      const int c = lane & 15;
+      const int node = c < nc ? cn[c] : -1;
+      const float *prow = a.P_all + (size_t)(node >= 0 ? ntok[node] : 0) * (3 * dh);
+      float *srow = a.states + ((size_t)t * a.ecap + (node >= 0 ? nstate[node] : 0)) * dh;
+      auto apply = [&](int gi, const f32x4 (&gh)[3]) {
+        if (node < 0) return;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ul = gi * 16 + (lane >> 4) * 4 + i;  // unit within this member
+          const int j = member * UW + ul;
+          const float hr = gh[0][i] + a.b_hh[j];
+          const float hz = gh[1][i] + a.b_hh[dh + j];
+          const float hn = gh[2][i] + a.b_hh[2 * dh + j];
+          const float r = sigmoidf_(prow[j] + hr);
+          const float z = sigmoidf_(prow[dh + j] + hz);
+          const float n = tanhf(prow[2 * dh + j] + r * hn);
+          const float hprev = Sp[c * dh + j];
+          const float sv = (1.0f - z) * n + z * hprev;
+          Sn[c * UW + ul] = sv;
+          st_dev(srow + j, sv);
+        }
+      };
+      const int nks = dh / 32;
+      if (NG >= NW) {
+        for (int gi = wave; gi < NG; gi += NW) {
+          f32x4 gh[3];
+          Gates<TW>::run(a, Sp, u0 + gi, 0, nks, gh);
+          apply(gi, gh);
+        }
+      } else {
+        // WPG waves split the k range of one unit group; partial sums meet in LDS
+        const int WPG = NW / NG;
+        if (wave < NG * WPG) {
+          const int gi = wave % NG, f = wave / NG;
+          f32x4 gh[3];
+          Gates<TW>::run(a, Sp, u0 + gi, (nks * f) / WPG, (nks * (f + 1)) / WPG, gh);
+#pragma unroll
+          for (int g = 0; g < 3; ++g)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) gpart[((wave * 3 + g) * 64 + lane) * 4 + i] = gh[g][i];
+        }
+        __syncthreads();
+        if (wave < NG) {
+          f32x4 sum[3];
+#pragma unroll
+          for (int g = 0; g < 3; ++g)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              float s = 0.0f;
+              for (int ff = 0; ff < WPG; ++ff) s += gpart[(((ff * NG + wave) * 3 + g) * 64 + lane) * 4 + i];
+              sum[g][i] = s;
+            }
+          apply(wave, sum);
+        }
+      }
+    }
+    __syncthreads();
     if (d >= L) return;
-    // 3. correction of depth d+1's slice: delta[m][c] = U[m] . S_c (fp32 MFMA)
+    // 2. this member's part of delta[c][m] = U[cand[m]] . S_c over its units (fp32 MFMA)
     const int RT = (M + 15) / 16;
-    const int F = NW / RT;
-    const int nq = dh / 16;
-    const size_t rbase = (size_t)(t * L + d) * M;  // depth d+1 rows
-    if (wave < RT * F) {
-      const int rt = wave % RT, f = wave / RT;
-      const int q0 = (nq * f) / F, q1 = (nq * (f + 1)) / F;
+    const int nq = UW / 16;
+    float *mypart = a.part + (((size_t)t * 2 + pb) * CH) * MP * G + member;
+    for (int rt = wave; rt < RT; rt += NW) {
       const int m = rt * 16 + (lane & 15);
       const int c = lane & 15, kq = (lane >> 4) * 4;
-      const float *urow = a.U_all + (size_t)(m < M ? a.cand[rbase + m] : 0) * dh;
+      const float *urow = a.U_all + (size_t)(m < M ? ccand[m] : 0) * dh + member * UW;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int q = q0; q < q1; ++q) {
+      for (int q = 0; q < nq; ++q) {
         float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
         if (m < M) av = *reinterpret_cast<const float4 *>(urow + q * 16 + kq);
-        const float4 bv = *reinterpret_cast<const float4 *>(Scur + c * dh + q * 16 + kq);
+        const float4 bv = *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
       }
       // lane l, register i: slot rt*16 + (l/16)*4 + i, node l%16
+      if (c < nc)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int slot = rt * 16 + (lane >> 4) * 4 + i;
-        part[(f * RT * 16 + slot) * CH + c] = acc[i];
-      }
+        for (int i = 0; i < 4; ++i)
+          st_dev(mypart + ((size_t)c * MP + rt * 16 + (lane >> 4) * 4 + i) * G, acc[i]);
     }
-    __syncthreads();
-    // 4. children of node `wave`: normalise, rank, keep the top-k above vB
+    group_barrier(ctr, G, nbar, &scal[S_STATUS]);
+    // 3. children of each node: normalise, rank, keep the top-k above vB
     const float vB = scalf[S_VB];
-    const float R = a.tail[t * L + d];
-    int kc = 0;
-    if (wave < nc) {
-      const int c = wave;
+    const float R = scalf[S_R];
+    const __amdgpu_buffer_rsrc_t rp = dev_rsrc(a.part + ((size_t)t * 2 + pb) * CH * MP * G);
+    pb ^= 1;
+    for (int c = wave; c < CH; c += NW) {
+      if (c >= nc) {
+        if (lane == 0) wcnt[c] = 0;
+        continue;
+      }
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
       float zv[4];
       float mx = NEG_INF;
@@ -393,11 +587,32 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         const int m = lane + 64 * s;
         float z = NEG_INF;
         if (m < M) {
-          const float x = a.candv[rbase + m];
+          const float x = ccandv[m];
           if (x > NEG_INF) {
-            float dl = a.c_all[a.cand[rbase + m]];
-            for (int f = 0; f < F; ++f) dl += part[(f * RT * 16 + m) * CH + c];
-            z = (x + dl) * a.inv_tau;
+            // the G parts of this slot are contiguous: load them all, then sum in order
+            float pv[16];
+            const int off = ((c * MP + m) * G) * 4;
+            if (G >= 4) {
+#pragma unroll
+              for (int q4 = 0; q4 < 4; ++q4)
+                if (q4 * 4 < G) {
+                  const float4 v4 = ld_dev16(rp, off + q4 * 16);
+                  pv[q4 * 4] = v4.x;
+                  pv[q4 * 4 + 1] = v4.y;
+                  pv[q4 * 4 + 2] = v4.z;
+                  pv[q4 * 4 + 3] = v4.w;
+                }
+            } else {
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                if (j < G) pv[j] = ld_dev4(rp, off + j * 4);
+            }
+            // x already holds logit + E[v] . b_c (added by the row merge)
+            float dl = x;
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+              if (j < G) dl += pv[j];
+            z = dl * a.inv_tau;
           }
         }
         zv[s] = z;
@@ -411,48 +626,52 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       sum = wave_sum_f(sum);
       if (tail) sum += expf(R - mx);
       const float logZ = mx + logf(sum);
+      float lv[4];
       for (int s = 0; s < MP / 64; ++s) {
         const int m = lane + 64 * s;
-        ell[c * MP + m] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
+        lv[s] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
+        ell[c * MP + m] = lv[s];
       }
       wave_sync();
-      // rank of each live slot by (ell desc, slot asc); keep ranks < k with g >= vB
+      int kc = 0;
+      const float4 *e4 = reinterpret_cast<const float4 *>(ell + c * MP);
       for (int s = 0; s < MP / 64; ++s) {
         const int m = lane + 64 * s;
-        const float lm = ell[c * MP + m];
+        const float lm = lv[s];
+        // rank = slots ahead of m by (log-prob desc, slot asc); slots >= M hold -inf
         int rank = 0;
-        if (lm > NEG_INF) {
-          for (int m2 = 0; m2 < M; ++m2) {
-            const float l2 = ell[c * MP + m2];
-            rank += (l2 > lm) || (l2 == lm && m2 < m);
-          }
+#pragma unroll 16
+        for (int q = 0; q < MP / 4; ++q) {
+          const float4 v = e4[q];
+          const int m2 = 4 * q;
+          rank += (v.x > lm) | ((v.x == lm) & (m2 < m));
+          rank += (v.y > lm) | ((v.y == lm) & (m2 + 1 < m));
+          rank += (v.z > lm) | ((v.z == lm) & (m2 + 2 < m));
+          rank += (v.w > lm) | ((v.w == lm) & (m2 + 3 < m));
         }
         const bool keep = lm > NEG_INF && rank < a.k && gpar + lm >= vB;
         kc += __popcll(__ballot(keep));
         rnk[c * MP + m] = keep ? (int16_t)rank : (int16_t)-1;
       }
       if (lane == 0) wcnt[c] = kc;
-    } else if (wave < CH && lane == 0) {
-      wcnt[wave] = 0;
     }
     __syncthreads();
-    // 5. append children (node order, then rank order) to the node table
-    int base = scal[S_NN];
+    // 4. append children (node order, then rank order) to the node table
+    const int base = scal[S_NN];
     int tot = 0;
-    for (int c = 0; c < CH; ++c) tot += (c < nc) ? wcnt[c] : 0;
-    if (wave < nc) {
-      const int c = wave;
+    for (int c = 0; c < nc; ++c) tot += wcnt[c];
+    for (int c = wave; c < nc; c += NW) {
       int off = base;
       for (int c2 = 0; c2 < c; ++c2) off += wcnt[c2];
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
       for (int s = 0; s < MP / 64; ++s) {
         const int m = lane + 64 * s;
-        const int rk = rnk[c * MP + m];
-        if (m < M && rk >= 0) {
+        const int rk = m < M ? rnk[c * MP + m] : -1;
+        if (rk >= 0) {
           const int pos = off + rk;
           if (pos < NC) {
             ng[pos] = gpar + ell[c * MP + m];
-            ntok[pos] = a.cand[rbase + m];
+            ntok[pos] = ccand[m];
             nslot[pos] = (int16_t)m;
             ndepth[pos] = (uint8_t)(d + 1);
             nparent[pos] = (d == 0) ? (int16_t)-1 : cn[c];
@@ -471,9 +690,11 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         scal[S_STATUS] |= DT_TREE_TRUNCATED;  // table overflow (massive exact ties)
       }
       scal[S_NN] = nn;
-      if (d > 0) scal[S_NEXP] += nc;
+      if (d > 0) {
+        scal[S_NEXP] += nc;
+        for (int c = 0; c < nc; ++c) nexp[cn[c]] = 1;
+      }
     }
-    if (d > 0 && tid < nc) nexp[cn[tid]] = 1;
     __syncthreads();
   };
 
@@ -482,10 +703,17 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     const int nn = scal[S_NN];
     if (nn >= B) {
       float best = __builtin_huge_valf();
+      const float4 *g4 = reinterpret_cast<const float4 *>(ng);
+      const int n4 = nn >> 2;
       for (int i = tid; i < nn; i += NT) {
         const float gi = ng[i];
         int cnt = 0;
-        for (int j = 0; j < nn; ++j) cnt += ng[j] > gi;
+#pragma unroll 8
+        for (int j = 0; j < n4; ++j) {
+          const float4 v = g4[j];
+          cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
+        }
+        for (int j = n4 * 4; j < nn; ++j) cnt += ng[j] > gi;
         if (cnt < B) best = fminf(best, gi);
       }
       best = wave_min_f(best);
@@ -500,26 +728,28 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     }
     if (!compact || nn < B) return;
     const float vB = scalf[S_VB];
-    // keep g >= vB (parents always score at least their children, so links stay valid)
+    // keep g >= vB (parents always score at least their children: links stay valid)
     for (int r0 = 0; r0 < nn; r0 += NT) {
       const int i = r0 + tid;
       const bool keep = i < nn && ng[i] >= vB;
-      Compact cp = block_compact(keep, wcnt);
-      if (i < nn) newidx[i] = keep ? (int16_t)(cp.pos + (r0 ? scal[S_TOT] : 0)) : (int16_t)-1;
+      const Compact cp = block_compact(keep, wcnt);
+      const int off = r0 ? scal[S_TOT] : 0;
+      if (i < nn) newidx[i] = keep ? (int16_t)(cp.pos + off) : (int16_t)-1;
       __syncthreads();
-      if (tid == 0) scal[S_TOT] = (r0 ? scal[S_TOT] : 0) + cp.total;
+      if (tid == 0) scal[S_TOT] = off + cp.total;
       __syncthreads();
     }
     const int kept = scal[S_TOT];
-    // move (each thread owns at most two entries; read all, then write)
-    float rg[2];
-    int rt[2], rp[2], rs[2], rsl[2], rd[2], rr[2], re[2], dst[2];
-    for (int q = 0; q < 2; ++q) {
+    constexpr int PER = (NC + NT - 1) / NT;
+    float rg[PER];
+    int rt_[PER], rp[PER], rs[PER], rsl[PER], rd[PER], rr[PER], re[PER], dst[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
       const int i = tid + q * NT;
       dst[q] = (i < nn) ? newidx[i] : -1;
       if (dst[q] >= 0) {
         rg[q] = ng[i];
-        rt[q] = ntok[i];
+        rt_[q] = ntok[i];
         rp[q] = nparent[i] >= 0 ? newidx[nparent[i]] : -1;
         rs[q] = nstate[i];
         rsl[q] = nslot[i];
@@ -529,11 +759,12 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
     }
     __syncthreads();
-    for (int q = 0; q < 2; ++q) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
       if (dst[q] >= 0) {
         const int j = dst[q];
         ng[j] = rg[q];
-        ntok[j] = rt[q];
+        ntok[j] = rt_[q];
         nparent[j] = (int16_t)rp[q];
         nstate[j] = (int16_t)rs[q];
         nslot[j] = (int16_t)rsl[q];
@@ -548,7 +779,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   };
 
   // ---- phase A ---------------------------------------------------------------
-  expand_chunk(nullptr, 1, 0);  // root: children at depth 1 scored from h0
+  expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
   update_vb(false);
   for (int iter = 0; iter < L; ++iter) {
     // eligible: known, unexpanded, above depth L, score >= vB (index order)
@@ -557,7 +788,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     for (int r0 = 0; r0 < nn; r0 += NT) {
       const int i = r0 + tid;
       const bool e = i < nn && !nexp[i] && ndepth[i] < L && ng[i] >= vB;
-      Compact cp = block_compact(e, wcnt);
+      const Compact cp = block_compact(e, wcnt);
       const int off = r0 ? scal[S_NE] : 0;
       if (e) elist[off + cp.pos] = (int16_t)i;
       __syncthreads();
@@ -569,20 +800,36 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     int pos = 0;
     while (pos < ne) {
       __syncthreads();  // everyone has read the previous chunk's scalars
-      // next chunk: up to chunk_cap nodes that still score >= vB
-      if (tid == 0) {
+      if (wave == 0) {
+        // the next up-to-chunk_cap entries of elist that still score >= vB, in order
         const float v = scalf[S_VB];
-        int c = 0;
-        int p = pos;
+        int c = 0, p = pos;
         while (p < ne && c < chunk_cap) {
-          const int i = elist[p++];
-          if (i >= 0 && ng[i] >= v) cl[c++] = (int16_t)i;
+          const int idx = p + lane;
+          const int i = idx < ne ? elist[idx] : -1;
+          const bool ok = i >= 0 && ng[i] >= v;
+          const uint64_t bal = __ballot(ok);
+          const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+          const int need = chunk_cap - c, have = __popcll(bal);
+          if (ok && before < need) cl[c + before] = (int16_t)i;
+          if (have >= need) {
+            // stop right after the need-th qualifying entry
+            const uint64_t last = __ballot(ok && before == need - 1);
+            p += __builtin_ctzll(last) + 1;
+            c = chunk_cap;
+          } else {
+            p = (p + 64 < ne) ? p + 64 : ne;
+            c += have;
+          }
         }
-        scal[S_NC] = c;
-        scal[S_TOT] = p;
-        if (c && scal[S_NEXP] + c > a.ecap) {
-          scal[S_STATUS] |= DT_TREE_TRUNCATED;
-          scal[S_STOP] = 1;
+        if (lane == 0) {
+          scal[S_NC] = c;
+          scal[S_TOT] = p;
+          if (c && scal[S_NEXP] + c > a.ecap) {
+            scal[S_STATUS] |= DT_TREE_TRUNCATED;
+            scal[S_STOP] = 1;
+          }
         }
       }
       __syncthreads();
@@ -590,11 +837,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       pos = scal[S_TOT];
       if (scal[S_STOP]) break;
       if (nc == 0) continue;
-      // make room for the children of this chunk
-      const bool need = scal[S_NN] + nc * a.k > NC - CH;
-      if (need) {
+      if (scal[S_NN] + nc * a.k > NC - CH) {
+        // make room for this chunk's children
         update_vb(true);
-        // remap the rest of the eligible list and the chunk
         for (int p = tid; p < ne; p += NT) {
           const int i = elist[p];
           elist[p] = (i >= 0) ? newidx[i] : (int16_t)-1;
@@ -617,50 +862,126 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     }
     if (scal[S_STOP]) break;
   }
+  if (member != 0) return;
 
   // ---- phase B: exact replay of the heap --------------------------------------
+  // Only nodes scoring >= vB (the B-th best score in the table) can be among
+  // the first B pops: their ancestors score at least as much, so while fewer
+  // than B have been popped one of them is always in the heap and outranks every
+  // node below vB.  When at most 64 such nodes exist, one wave replays the heap
+  // with a node per lane in registers; otherwise it scans the node table.
+  // (vB is current: it is refreshed after every expansion step.)
   const int nn = scal[S_NN];
   if (wave == 0) {
-    for (int i = lane; i < nn; i += 64) {
-      ins[i] = nparent[i] < 0;
-      popd[i] = 0;
-      ppi[i] = -1;
+    const float vB = scalf[S_VB];
+    int ncand = 0;
+    for (int r0 = 0; r0 < nn; r0 += 64) {
+      const int i = r0 + lane;
+      const bool in = i < nn && ng[i] >= vB;
+      const uint64_t bal = __ballot(in);
+      const int at = ncand + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+      if (in && at < 64) elist[at] = (int16_t)i;
+      ncand += __popcll(bal);
     }
     wave_sync();
     int npop = 0;
-    while (npop < B) {
-      uint64_t best = 0;
-      for (int i = lane; i < nn; i += 64) {
-        if (ins[i] && !popd[i]) {
-          const uint64_t key = ((uint64_t)ordered_bits(ng[i]) << 32) |
-                               ((uint64_t)((~(uint32_t)(ppi[i] + 1)) & 0x1FFu) << 19) |
-                               ((uint64_t)((~(uint32_t)nrank[i]) & 0xFFu) << 11) | (uint64_t)i;
-          best = key > best ? key : best;
-        }
-      }
-      best = wave_max_u64(best);
-      if (best == 0) break;
-      const int p = (int)(best & 0x7FF);
-      if (lane == 0) {
-        popd[p] = 1;
-        order[npop] = (int16_t)p;
-      }
-      for (int i = lane; i < nn; i += 64)
-        if (nparent[i] == p) {
-          ins[i] = 1;
-          ppi[i] = (int16_t)npop;
-        }
-      ++npop;
+    bool done = false;
+    if (ncand <= 64) {
+      // Without exact score ties the pops are simply the candidates by score
+      // (a parent scores strictly above its children, so it is popped first).
+      const bool have = lane < ncand;
+      const int me = have ? elist[lane] : -1;
+      const float gm = have ? ng[me] : NEG_INF;
+      Sn[lane] = gm;
       wave_sync();
+      int rank = 0, eq = 0;
+      const float4 *s4 = reinterpret_cast<const float4 *>(Sn);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const float4 v = s4[q];
+        rank += (v.x > gm) + (v.y > gm) + (v.z > gm) + (v.w > gm);
+        eq += (v.x == gm) + (v.y == gm) + (v.z == gm) + (v.w == gm);
+      }
+      if (__ballot(have && eq > 1) == 0) {
+        npop = ncand < B ? ncand : B;
+        if (have) newidx[me] = (int16_t)rank;
+        wave_sync();
+        if (have && rank < B) {
+          const int par = nparent[me];
+          order[rank] = (int16_t)me;
+          ppi[me] = (int16_t)(par >= 0 ? newidx[par] : -1);
+        }
+        done = true;
+      }
+    }
+    if (!done && ncand <= 64) {
+      const bool have = lane < ncand;
+      const int me = have ? elist[lane] : -1;
+      const int par = have ? nparent[me] : -2;
+      const uint64_t gkey = have ? ((uint64_t)ordered_bits(ng[me]) << 32) |
+                                       ((uint64_t)((~(uint32_t)nrank[me]) & 0xFFu) << 11) |
+                                       (uint64_t)me
+                                 : 0ull;
+      bool ins_ = have && par < 0, popd_ = false;
+      int ppi_ = -1;
+      while (npop < B) {
+        const uint64_t key =
+            (ins_ && !popd_) ? gkey | ((uint64_t)((~(uint32_t)(ppi_ + 1)) & 0x1FFu) << 19) : 0ull;
+        const uint64_t best = wave_max_u64(key);
+        if (best == 0) break;
+        const int p = (int)(best & 0x7FF);
+        if (me == p) popd_ = true;
+        if (par == p) {
+          ins_ = true;
+          ppi_ = npop;
+        }
+        if (lane == 0) order[npop] = (int16_t)p;
+        ++npop;
+      }
+      if (have) ppi[me] = (int16_t)ppi_;
+    } else if (!done) {
+      for (int i = lane; i < nn; i += 64) {
+        ins[i] = nparent[i] < 0;
+        popd[i] = 0;
+        ppi[i] = -1;
+      }
+      wave_sync();
+      while (npop < B) {
+        uint64_t best = 0;
+        for (int i = lane; i < nn; i += 64) {
+          if (ins[i] && !popd[i]) {
+            const uint64_t key = ((uint64_t)ordered_bits(ng[i]) << 32) |
+                                 ((uint64_t)((~(uint32_t)(ppi[i] + 1)) & 0x1FFu) << 19) |
+                                 ((uint64_t)((~(uint32_t)nrank[i]) & 0xFFu) << 11) | (uint64_t)i;
+            best = key > best ? key : best;
+          }
+        }
+        best = wave_max_u64(best);
+        if (best == 0) break;
+        const int p = (int)(best & 0x7FF);
+        if (lane == 0) {
+          popd[p] = 1;
+          order[npop] = (int16_t)p;
+        }
+        for (int i = lane; i < nn; i += 64)
+          if (nparent[i] == p) {
+            ins[i] = 1;
+            ppi[i] = (int16_t)npop;
+          }
+        ++npop;
+        wave_sync();
+      }
     }
     if (lane == 0) scal[S_NPOP] = npop;
   }
   __syncthreads();
 
-  // ---- emission -----------------------------------------------------------------
+  // ---- emission ---------------------------------------------------------------
   const int npop = scal[S_NPOP];
   const int W32 = (B + 31) / 32;
   for (int i = tid; i < B; i += NT) {
+    for (int w = 0; w < W32; ++w) anc[i * 8 + w] = 0;
     if (i < npop) {
       const int node = order[i];
       otok[i] = ntok[node];
@@ -668,7 +989,6 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       odep[i] = ndepth[node];
       opos[i] = a.pos_offset + ndepth[node];
       osc[i] = ng[node];
-      for (int w = 0; w < W32; ++w) anc[i * 8 + w] = 0;
       // parents pop strictly earlier, so the walk ends within depth <= L steps
       int j = i;
       for (int step = 0; j >= 0 && step <= L; ++step) {
@@ -682,7 +1002,6 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       odep[i] = 0;
       opos[i] = a.pos_offset;
       osc[i] = NEG_INF;
-      for (int w = 0; w < W32; ++w) anc[i * 8 + w] = 0;
     }
   }
   __syncthreads();
@@ -698,24 +1017,48 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 
 }  // namespace
 
-size_t expand_lds_bytes(int dh, int M) { return (size_t)lds_layout(dh, M).total; }
+int expand_group_size(int d_h, int num_cus, int batch) {
+  // largest power-of-two group (<= 16, >= 32 units per member) whose grid fits
+  // one workgroup per CU for a cooperative launch
+  int G = 16;
+  while (G > 1 && (d_h / G < 32 || (d_h / G) % 16 != 0 || 8 * G * ((batch + 7) / 8) > num_cus))
+    G >>= 1;
+  return G;
+}
+
+size_t expand_lds_bytes(int dh, int G, int M, int nchunks) {
+  return (size_t)lds_layout(dh, G, M, nchunks).total;
+}
+
+size_t expand_part_bytes(const dt_plan *p, int batch) {
+  const int G = expand_group_size(p->d_h, p->num_cus, batch);
+  return (size_t)batch * 2 * G * CH * mp_of(p->M) * sizeof(float);
+}
 
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s) {
   ExpArgs a;
+  const ScanGeom g = scan_geom(batch * p->L, p->V, p->M);
   a.L = p->L;
   a.M = p->M;
   a.B = p->B;
   a.k = p->k;
   a.dh = p->d_h;
+  a.G = expand_group_size(p->d_h, p->num_cus, batch);
   a.norm_mode = p->norm_mode;
   a.pos_offset = p->pos_offset;
   a.ecap = ws.ecap;
   a.batch = batch;
+  a.nchunks = g.nchunks;
+  a.nxcd = 8;
   a.inv_tau = inv_tau;
+  a.c2 = 1.4426950408889634f * inv_tau;
+  a.ckeys = ws.chunk_keys;
+  a.ctail = ws.chunk_tail;
+  a.cflag = ws.chunk_flag;
   a.cand = ws.cand;
   a.candv = ws.candv;
-  a.tail = ws.tail;
+  a.tailR = ws.tail;
   a.rflag = ws.row_flag;
   a.P_all = p->P_all;
   a.U_all = p->U_all;
@@ -724,17 +1067,23 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.b_hh = p->b_hh;
   a.h0 = h0;
   a.states = ws.states;
+  a.part = ws.part;
+  a.bar = ws.bar;
   a.out = *out;
-  const size_t lds = expand_lds_bytes(p->d_h, p->M);
-  if (p->wdt == DT_BF16) {
-    hipFuncSetAttribute((const void *)expand_kernel<uint16_t>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(expand_kernel<uint16_t>, dim3(batch), dim3(NT), lds, s, a);
-  } else {
-    hipFuncSetAttribute((const void *)expand_kernel<float>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(expand_kernel<float>, dim3(batch), dim3(NT), lds, s, a);
+  const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks);
+  const void *fn = p->wdt == DT_BF16 ? (const void *)expand_kernel<uint16_t>
+                                     : (const void *)expand_kernel<float>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  if (a.G > 1) {
+    const int grid = 8 * a.G * ((batch + 7) / 8);
+    void *args[] = {&a};
+    return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NT), args, (unsigned)lds, s);
   }
+  if (p->wdt == DT_BF16)
+    hipLaunchKernelGGL(expand_kernel<uint16_t>, dim3(batch), dim3(NT), lds, s, a);
+  else
+    hipLaunchKernelGGL(expand_kernel<float>, dim3(batch), dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 

@@ -18,10 +18,13 @@ constexpr int kMaxL = 64;
 constexpr int kMaxDh = 1024;
 constexpr int kMaxDe = 8192;
 
-// scan: one workgroup of 256 threads per (row, chunk)
+// scan: one workgroup of 256 threads per (row, chunk of kScanChunk elements)
 constexpr int kScanThreads = 256;
+constexpr int kScanPerThread = 40;                         // elements held per thread
+constexpr int kScanChunk = kScanThreads * kScanPerThread;  // 10240
 constexpr int kScanSortCap = 4096;   // bitonic sort buffer (keys) per workgroup
-constexpr int kScanFlushAt = 256;    // flush the candidate buffer beyond this many keys
+constexpr int kScanFlushAt = 256;    // fallback: flush the candidate buffer beyond this
+constexpr int kMergeLdsMax = 96 * 1024;  // row merge buffer: 14 n + 8 M bytes, n = ceil(V/kScanChunk) M
 
 // fold GEMM tile (bf16 MFMA path)
 constexpr int kFoldBM = 128;
@@ -29,9 +32,10 @@ constexpr int kFoldBN = 128;
 constexpr int kFoldBK = 64;
 
 // expansion kernel
-constexpr int kExpThreads = 1024;
+constexpr int kExpThreads = 512;
 constexpr int kNodeCap = 1536;       // live nodes per tree kept in LDS
 constexpr int kChunkNodes = 16;      // nodes expanded together (shared weight pass)
+constexpr int kBarStride = 64;       // ints per tree of barrier counters (own cache lines)
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -87,7 +91,7 @@ struct dt_plan {
   int num_cus;
   int profiling;            // record stage events in dt_build_tree
   int profiled_calls;       // calls recorded since profiling was enabled
-  hipEvent_t ev[4];         // stage boundaries of the last profiled call
+  hipEvent_t ev[3];         // stage boundaries of the last profiled call
 };
 
 namespace dt {
@@ -103,22 +107,29 @@ struct Workspace {
   int32_t *row_flag;      // [rows]
   // expansion
   float *states;          // [batch][ecap][dh]
+  float *part;            // [batch][2][G][16][MP] partial corrections
+  int32_t *bar;           // [batch][kBarStride] barrier counters
   int ecap;
   size_t bytes;
 };
 
 ScanGeom scan_geom(int rows, int V, int M);
+size_t merge_lds_bytes(const ScanGeom &g);  // LDS of the per-row merge (<= kMergeLdsMax)
 size_t scan_bytes(const ScanGeom &g);
 // carve the scan part of a workspace; returns bytes used
 size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws);
 Workspace carve(const dt_plan *p, int batch, char *base);
 
 // kernel launchers (return hipError_t of the launch)
-hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
-                       const Workspace &ws, hipStream_t s, hipEvent_t between = nullptr);
+hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
+                              const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s);
+hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s);
 hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s);
+int expand_group_size(int d_h, int num_cus, int batch);
+size_t expand_lds_bytes(int dh, int G, int M, int nchunks);
+size_t expand_part_bytes(const dt_plan *p, int batch);
 hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);
 
 }  // namespace dt

@@ -1,30 +1,35 @@
 // S1: per-depth marginal top-M and the tail log-sum-exp (Alg. 1 step 1;
 // section 3.2, candidate restriction).
 //
-// Every logit row [V] is split into chunks; one 256-thread workgroup streams a
-// chunk through an exact top-M selector and writes the chunk's M best keys plus
-// the (max, sum-exp) of every other element of the chunk.  A second kernel runs
-// the same selector over the chunk candidates of a row and folds the chunk
-// tails, giving the row's top-M and R = log sum_{v not in top-M} exp(x_v/tau).
-//
-// Keys are 64-bit (order-preserving value bits, ~index), so the total order
-// (value desc, id asc) is a plain integer order with no ties.  The selector
-// keeps a sorted list of the best M keys in LDS and a buffer of new candidates
-// that beat the current threshold; when the buffer grows past a bound the
-// union is bitonic-sorted and cut back to M.  The first threshold is an exact
-// lower bound on the chunk's M-th best key: every wave sorts its 64 per-lane
-// maxima and takes the ceil(M/4)-th, and the minimum over the 4 waves leaves at
-// least M elements at or above it.  Elements below the threshold go straight
-// into the running tail sum; keys evicted by a flush join it then.
-#include "dt_internal.h"
+// Each logit row [V] is cut into chunks of 10240 elements.  One 256-thread
+// workgroup loads its whole chunk into registers (40 values per thread, all
+// loads in flight at once) and selects the chunk's M best elements exactly:
+//   * keys are 64-bit (order-preserving value bits, ~index), so the order
+//     (value desc, id asc) is a plain integer order without ties;
+//   * every wave sorts its 64 per-lane maximum keys and takes the ceil(M/4)-th;
+//     the minimum over the 4 waves leaves at least M elements at or above it,
+//     so it is an exact lower bound on the chunk's M-th best key;
+//   * elements below that bound go straight into the running tail sum
+//     (max, sum exp((x - max)/tau)); the survivors (about 1% of the chunk on
+//     drafter-like rows) are compacted into LDS and bitonic-sorted once; the
+//     best M are the chunk's list, the rest join the tail.
+// If the survivors overflow the sort buffer (adversarial rows: long runs of
+// equal or monotone values), they are streamed through a bounded selector that
+// keeps a sorted list of M and flushes a candidate buffer instead.
+// The per-row merge (merge_row) sorts the chunk lists of a row together and
+// folds the chunk tails; it runs inside the expansion kernel, or in a small
+// kernel of its own for dt_scan_topm.
+#include "dt_select.h"
 
 namespace dt {
 
 namespace {
 
+using sel::Tail;
+
 constexpr int kWaves = kScanThreads / 64;
 
-struct SelLDS {
+struct ScanLDS {
   uint64_t buf[kScanSortCap];
   uint64_t wthr[kWaves];
   float2 red[kWaves];
@@ -34,162 +39,54 @@ struct SelLDS {
   uint64_t thr;
 };
 
-struct Tail {
-  float m, s;
-};
-
-__device__ inline void tail_init(Tail &t) {
-  t.m = -3.402823466e38f;
-  t.s = 0.0f;
-}
-
-// fold a group of values (already masked to -inf where not counted)
-template <int N>
-__device__ inline void tail_add_group(Tail &t, const float (&x)[N], float c) {
-  float mx = t.m;
-#pragma unroll
-  for (int j = 0; j < N; ++j) mx = fmaxf(mx, x[j]);
-  float s = t.s * exp2f((t.m - mx) * c);
-#pragma unroll
-  for (int j = 0; j < N; ++j) s += exp2f((x[j] - mx) * c);
-  t.m = mx;
-  t.s = s;
-}
-
-__device__ inline void tail_add1(Tail &t, float x, float c) {
-  float xs[1] = {x};
-  tail_add_group<1>(t, xs, c);
-}
-
-__device__ inline Tail tail_merge(Tail a, Tail b, float c) {
-  Tail r;
-  r.m = fmaxf(a.m, b.m);
-  r.s = a.s * exp2f((a.m - r.m) * c) + b.s * exp2f((b.m - r.m) * c);
-  return r;
-}
-
-__device__ inline Tail block_tail(SelLDS &sh, Tail t, float c) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    Tail u;
-    u.m = __shfl_xor(t.m, o);
-    u.s = __shfl_xor(t.s, o);
-    t = tail_merge(t, u, c);
-  }
-  if (lane == 0) sh.red[w] = make_float2(t.m, t.s);
-  __syncthreads();
-  Tail r;
-  r.m = sh.red[0].x;
-  r.s = sh.red[0].y;
-  for (int i = 1; i < kWaves; ++i) {
-    Tail u;
-    u.m = sh.red[i].x;
-    u.s = sh.red[i].y;
-    r = tail_merge(r, u, c);
-  }
-  __syncthreads();
-  return r;
-}
-
-// descending bitonic sort of a wave's 64 values (one per lane)
-__device__ inline uint64_t wave_sort_desc(uint64_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      uint64_t p = __shfl_xor(v, j);
-      bool desc = (lane & k) == 0;
-      bool lower = (lane & j) == 0;
-      v = (desc == lower) ? (v > p ? v : p) : (v < p ? v : p);
-    }
-  }
-  return v;
-}
-
-__device__ inline int next_pow2(int n) {
-  int p = 64;
-  while (p < n) p <<= 1;
-  return p;
-}
-
-// sort buf[0..nbuf) descending, keep the best M as the list, evict the rest
-__device__ void flush(SelLDS &sh, int M, Tail &tail, float c) {
+// ---------------------------------------------------------------------------
+// bounded streaming selector (fallback for chunks whose survivors overflow):
+// buf[0..nlist) is the sorted best-M list, buf[nlist..nbuf) new candidates
+// ---------------------------------------------------------------------------
+__device__ void flush(ScanLDS &sh, int M, Tail &tail, float c) {
   const int tid = threadIdx.x;
   const int n = sh.nbuf;
-  const int P = next_pow2(n);
+  const int P = sel::pow2_at_least(n, 64);
   for (int i = n + tid; i < P; i += kScanThreads) sh.buf[i] = 0;
   __syncthreads();
-  for (int k = 2; k <= P; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int p = tid; p < P / 2; p += kScanThreads) {
-        int i = 2 * p - (p & (j - 1));
-        int ixj = i + j;
-        uint64_t a = sh.buf[i], b = sh.buf[ixj];
-        bool desc = (i & k) == 0;
-        if (desc ? (a < b) : (a > b)) {
-          sh.buf[i] = b;
-          sh.buf[ixj] = a;
-        }
-      }
-      __syncthreads();
-    }
-  }
-  for (int i = M + tid; i < n; i += kScanThreads) tail_add1(tail, key_value(sh.buf[i]), c);
+  sel::block_sort_desc<kScanThreads>(sh.buf, P);
+  for (int i = M + tid; i < n; i += kScanThreads) sel::tail_add1(tail, key_value(sh.buf[i]), c);
   __syncthreads();
   if (tid == 0) {
-    int nl = n < M ? n : M;
+    const int nl = n < M ? n : M;
     sh.nlist = nl;
     sh.nbuf = nl;
     if (nl == M) {
-      uint64_t t = sh.buf[M - 1] + 1;
+      const uint64_t t = sh.buf[M - 1] + 1;
       if (t > sh.thr) sh.thr = t;
     }
   }
   __syncthreads();
 }
 
-// One sub-batch: EPT keys per thread (0 = no element).  `first` computes the
-// initial threshold from the per-lane maxima.
+// one group of EPT keys per thread (0 = none); keys below the running
+// threshold join the tail, the others the candidate buffer
 template <int EPT>
-__device__ void select_batch(SelLDS &sh, const uint64_t (&key)[EPT], const float (&val)[EPT],
-                             bool first, int M, Tail &tail, float c) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (first) {
-    uint64_t mx = 0;
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) mx = key[j] > mx ? key[j] : mx;
-    uint64_t srt = wave_sort_desc(mx);
-    int q = (M + kWaves - 1) / kWaves;  // <= 64 since M <= 256
-    uint64_t tq = __shfl(srt, q - 1);
-    if (lane == 0) sh.wthr[w] = tq;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint64_t t = sh.wthr[0];
-      for (int i = 1; i < kWaves; ++i) t = sh.wthr[i] < t ? sh.wthr[i] : t;
-      if (t == 0) t = 1;  // fewer than M elements so far: accept everything
-      if (t > sh.thr) sh.thr = t;
-    }
-    __syncthreads();
-  }
+__device__ void stream_batch(ScanLDS &sh, const uint64_t (&key)[EPT], const float (&val)[EPT],
+                             int M, Tail &tail, float c) {
+  const int lane = threadIdx.x & 63;
   const uint64_t thr = sh.thr;
   float tv[EPT];
   uint64_t bal[EPT];
   int tot = 0;
 #pragma unroll
   for (int j = 0; j < EPT; ++j) {
-    bool pass = key[j] != 0 && key[j] >= thr;
+    const bool pass = key[j] != 0 && key[j] >= thr;
     tv[j] = (key[j] != 0 && !pass) ? val[j] : -__builtin_huge_valf();
     bal[j] = __ballot(pass);
     tot += __popcll(bal[j]);
   }
-  tail_add_group<EPT>(tail, tv, c);
+  sel::tail_add_group<EPT>(tail, tv, c);
   if (tot) {
     int base = 0;
     if (lane == 0) base = atomicAdd(&sh.nbuf, tot);
     base = __shfl(base, 0);
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
       if ((bal[j] >> lane) & 1ull) sh.buf[base + __popcll(bal[j] & below)] = key[j];
@@ -200,27 +97,15 @@ __device__ void select_batch(SelLDS &sh, const uint64_t (&key)[EPT], const float
   if (sh.nbuf - sh.nlist > kScanFlushAt) flush(sh, M, tail, c);
 }
 
-__device__ inline void init_sel(SelLDS &sh) {
-  if (threadIdx.x == 0) {
-    sh.nbuf = 0;
-    sh.nlist = 0;
-    sh.flag = 0;
-    sh.thr = 1;
-  }
-  __syncthreads();
-}
-
-__device__ inline bool nonfinite(float v) { return v != v || v == __builtin_huge_valf(); }
-
 template <typename T>
 struct Elem;
 template <>
 struct Elem<uint16_t> {
-  static constexpr int EPT = 8;
+  static constexpr int EPL = 8;  // elements per 16-byte load
 };
 template <>
 struct Elem<float> {
-  static constexpr int EPT = 4;
+  static constexpr int EPL = 4;
 };
 
 template <typename T>
@@ -234,139 +119,231 @@ __device__ inline float to_f32<float>(float x) {
   return x;
 }
 
-// K1: top-M of one chunk of one row
+// fp32 class test: NaN or +inf (v_cmp_class)
+__device__ inline bool nonfinite(float v) { return __builtin_amdgcn_class(v, 0x203); }
+
+// descending bitonic sort of a wave's 64 floats (one per lane)
+__device__ inline float wave_sort_desc_f(float v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const float p = __shfl_xor(v, j);
+      const bool desc = (lane & k) == 0;
+      const bool lower = (lane & j) == 0;
+      v = (desc == lower) ? fmaxf(v, p) : fminf(v, p);
+    }
+  }
+  return v;
+}
+
+// inclusive prefix sum over a wave
+__device__ inline int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// K1: exact top-M of one chunk (kScanChunk elements) of one row, plus the tail
+// of the rest.  Also clears `zero_n` ints at `zero_ptr` (barrier counters of
+// the expansion kernel that follows on the stream).
 template <typename T, bool VEC>
-__global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(const T *__restrict__ logits,
-                                                                  ScanGeom g, float c,
-                                                                  uint64_t *__restrict__ ckeys,
-                                                                  float2 *__restrict__ ctail,
-                                                                  int32_t *__restrict__ cflag) {
-  constexpr int EPT = Elem<T>::EPT;
-  constexpr int UNR = 4;  // sub-batches whose loads are issued together
-  __shared__ SelLDS sh;
-  const int tid = threadIdx.x;
+__global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
+    const T *__restrict__ logits, ScanGeom g, float c, uint64_t *__restrict__ ckeys,
+    float2 *__restrict__ ctail, int32_t *__restrict__ cflag, int32_t *__restrict__ zero_ptr,
+    int zero_n) {
+  constexpr int EPL = Elem<T>::EPL;
+  constexpr int NL = kScanPerThread / EPL;  // 16-byte loads per thread
+  constexpr int STEP = kScanThreads * EPL;  // elements per load round
+  constexpr float NINF = -__builtin_huge_valf();
+  __shared__ ScanLDS sh;
+  __shared__ uint64_t list[kMaxM];
+  __shared__ float wthr[kWaves];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int row = blockIdx.y, chunk = blockIdx.x;
   const int start = chunk * g.chunk;
   const int n = min(g.chunk, g.V - start);
   const T *base = logits + (size_t)row * g.V + start;
-  init_sel(sh);
-  Tail tail;
-  tail_init(tail);
-  int bad = 0;
-  const int step = kScanThreads * EPT;
-  bool first = true;
-  for (int b0 = 0; b0 < n; b0 += step * UNR) {
-    float v[UNR][EPT];
+  if (zero_ptr && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = tid; i < zero_n; i += kScanThreads) zero_ptr[i] = 0;
+
+  // 1. the whole chunk into registers: element (j, e) of this thread has
+  //    chunk offset j*STEP + tid*EPL + e; slots past the end hold -inf
+  float v[NL][EPL];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int off = b0 + u * step + tid * EPT;
-      if (VEC && off + EPT <= n) {
-        if constexpr (EPT == 8) {
-          uint4 r = *reinterpret_cast<const uint4 *>(base + off);
-          uint32_t w4[4] = {r.x, r.y, r.z, r.w};
+  for (int j = 0; j < NL; ++j) {
+    const int off = j * STEP + tid * EPL;
+    if (VEC && off + EPL <= n) {
+      if constexpr (EPL == 8) {
+        const uint4 r = *reinterpret_cast<const uint4 *>(base + off);
+        const uint32_t w4[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            v[u][2 * q] = __uint_as_float(w4[q] << 16);
-            v[u][2 * q + 1] = __uint_as_float(w4[q] & 0xFFFF0000u);
-          }
-        } else {
-          float4 r = *reinterpret_cast<const float4 *>(base + off);
-          v[u][0] = r.x;
-          v[u][1] = r.y;
-          v[u][2] = r.z;
-          v[u][3] = r.w;
+        for (int q = 0; q < 4; ++q) {
+          v[j][2 * q] = __uint_as_float(w4[q] << 16);
+          v[j][2 * q + 1] = __uint_as_float(w4[q] & 0xFFFF0000u);
         }
       } else {
-#pragma unroll
-        for (int j = 0; j < EPT; ++j)
-          v[u][j] = (off + j < n) ? to_f32<T>(base[off + j]) : __builtin_nanf("");
+        const float4 r = *reinterpret_cast<const float4 *>(base + off);
+        v[j][0] = r.x;
+        v[j][1] = r.y;
+        v[j][2] = r.z;
+        v[j][3] = r.w;
       }
-    }
+    } else {
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      if (b0 + u * step >= n) break;  // uniform
-      const int off = b0 + u * step + tid * EPT;
-      uint64_t key[EPT];
-      float val[EPT];
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        const bool in = off + j < n;
-        float x = v[u][j];
-        if (in && nonfinite(x)) bad = 1;
-        // NaN / +inf make the row invalid; keep them out of the arithmetic
-        if (!in || nonfinite(x)) {
-          key[j] = 0;
-          val[j] = 0.0f;
-        } else {
-          key[j] = make_key(x, (uint32_t)(start + off + j));
-          val[j] = x;
-        }
-      }
-      select_batch<EPT>(sh, key, val, first, g.M, tail, c);
-      first = false;
+      for (int e = 0; e < EPL; ++e) v[j][e] = (off + e < n) ? to_f32<T>(base[off + e]) : NINF;
     }
   }
-  if (sh.nbuf > sh.nlist) flush(sh, g.M, tail, c);
+  if (tid == 0) {
+    sh.nbuf = 0;
+    sh.nlist = 0;
+    sh.flag = 0;
+  }
+  // 2. NaN / +inf flag the row and leave the arithmetic as -inf; thread max
+  int bad = 0;
+  float tmax = NINF;
+#pragma unroll
+  for (int j = 0; j < NL; ++j)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      if (nonfinite(v[j][e])) {
+        bad = 1;
+        v[j][e] = NINF;
+      }
+      tmax = fmaxf(tmax, v[j][e]);
+    }
+  // 3. value threshold: every wave has >= ceil(M/4) lanes whose max is at least
+  //    its ceil(M/4)-th largest lane max, so at least M elements of the chunk
+  //    are >= the minimum over the waves: no top-M element lies below it
+  {
+    const float srt = wave_sort_desc_f(tmax);
+    const int q = (g.M + kWaves - 1) / kWaves;  // <= 64 since M <= 256
+    const float tq = __shfl(srt, q - 1);
+    if (lane == 0) wthr[w] = tq;
+  }
+  __syncthreads();
+  float thr = wthr[0];
+  for (int i = 1; i < kWaves; ++i) thr = fminf(thr, wthr[i]);
+  // 4. count survivors (v >= thr); the others go into this thread's tail, with
+  //    the thread max as reference
+  Tail tail;
+  tail.m = fmaxf(tmax, -3.402823466e38f);
+  float s = 0.0f;
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < NL; ++j)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const int off = j * STEP + tid * EPL + e;
+      const bool in = off < n;
+      const bool pass = in && v[j][e] >= thr;
+      cnt += pass;
+      const float ex = exp2f((v[j][e] - tail.m) * c);
+      s += (in && !pass) ? ex : 0.0f;
+    }
+  tail.s = s;
   if (bad) atomicOr(&sh.flag, 1);
-  Tail t = block_tail(sh, tail, c);
+  // 5. survivor slots: wave prefix of the per-thread counts, one LDS atomic per wave
+  const int incl = wave_incl_scan(cnt);
+  int wbase = 0;
+  if (lane == 63 && incl) wbase = atomicAdd(&sh.nbuf, incl);
+  wbase = __shfl(wbase, 63);
+  __syncthreads();
+  const int nsurv = sh.nbuf;
+  const int M = g.M;
+  if (nsurv <= kScanSortCap) {
+    int pos = wbase + incl - cnt;
+    if (cnt) {
+#pragma unroll
+      for (int j = 0; j < NL; ++j)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          const int off = j * STEP + tid * EPL + e;
+          if (off < n && v[j][e] >= thr) sh.buf[pos++] = make_key(v[j][e], (uint32_t)(start + off));
+        }
+    }
+    __syncthreads();
+    if (nsurv <= 2 * kScanThreads) {
+      // 6a. rank sort: each survivor's rank is the number of larger keys
+      for (int i = tid; i < M; i += kScanThreads) list[i] = 0ull;
+      __syncthreads();
+      for (int i = tid; i < nsurv; i += kScanThreads) {
+        const uint64_t k = sh.buf[i];
+        int rank = 0;
+        for (int q = 0; q < nsurv; ++q) rank += sh.buf[q] > k;
+        if (rank < M)
+          list[rank] = k;
+        else
+          sel::tail_add1(tail, key_value(k), c);
+      }
+      if (tid == 0) sh.nlist = nsurv < M ? nsurv : M;
+      __syncthreads();
+    } else {
+      // 6b. bitonic sort of the survivors
+      const int P = sel::pow2_at_least(nsurv, 64);
+      for (int i = nsurv + tid; i < P; i += kScanThreads) sh.buf[i] = 0;
+      __syncthreads();
+      sel::block_sort_desc<kScanThreads>(sh.buf, P);
+      for (int i = M + tid; i < nsurv; i += kScanThreads) sel::tail_add1(tail, key_value(sh.buf[i]), c);
+      for (int i = tid; i < M; i += kScanThreads) list[i] = i < nsurv ? sh.buf[i] : 0ull;
+      if (tid == 0) sh.nlist = nsurv < M ? nsurv : M;
+      __syncthreads();
+    }
+  } else {
+    // 6c. fallback (adversarial rows): stream the survivors through the
+    //     bounded selector, starting from the value threshold
+    __syncthreads();
+    if (tid == 0) {
+      sh.nbuf = 0;
+      sh.nlist = 0;
+      sh.thr = 1;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      uint64_t key[EPL];
+      float val[EPL];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const int off = j * STEP + tid * EPL + e;
+        key[e] = (off < n && v[j][e] >= thr) ? make_key(v[j][e], (uint32_t)(start + off)) : 0ull;
+        val[e] = v[j][e];
+      }
+      stream_batch<EPL>(sh, key, val, M, tail, c);
+    }
+    if (sh.nbuf > sh.nlist) flush(sh, M, tail, c);
+    for (int i = tid; i < M; i += kScanThreads) list[i] = i < sh.nlist ? sh.buf[i] : 0ull;
+    __syncthreads();
+  }
+  const Tail t = sel::block_tail<kScanThreads>(tail, c, sh.red);
   const size_t cidx = (size_t)row * g.nchunks + chunk;
-  uint64_t *out = ckeys + cidx * g.M;
-  for (int i = tid; i < g.M; i += kScanThreads) out[i] = i < sh.nlist ? sh.buf[i] : 0ull;
+  uint64_t *out = ckeys + cidx * M;
+  for (int i = tid; i < M; i += kScanThreads) out[i] = list[i];
   if (tid == 0) {
     ctail[cidx] = make_float2(t.m, t.s);
     cflag[cidx] = sh.flag ? DT_TREE_NONFINITE : 0;
   }
 }
 
-// K2: merge the chunk candidates of one row
+// K2 (dt_scan_topm only): merge the chunk lists of one row
 __global__ __launch_bounds__(kScanThreads) void scan_merge_kernel(
     ScanGeom g, float c, float inv_tau, const uint64_t *__restrict__ ckeys,
     const float2 *__restrict__ ctail, const int32_t *__restrict__ cflag, int32_t *__restrict__ cand,
     float *__restrict__ candv, float *__restrict__ tailR, int32_t *__restrict__ rflag) {
-  constexpr int EPT = 8;
-  __shared__ SelLDS sh;
-  const int tid = threadIdx.x;
+  extern __shared__ uint64_t sortbuf[];  // merge_buf_bytes(nchunks, M)
+  __shared__ float2 red[kWaves];
+  __shared__ int flag;
   const int row = blockIdx.x;
-  init_sel(sh);
-  Tail tail;
-  tail_init(tail);
-  int bad = 0;
-  for (int i = tid; i < g.nchunks; i += kScanThreads) {
-    const float2 ct = ctail[(size_t)row * g.nchunks + i];
-    Tail u;
-    u.m = ct.x;
-    u.s = ct.y;
-    tail = tail_merge(tail, u, c);
-    bad |= cflag[(size_t)row * g.nchunks + i];
-  }
-  const uint64_t *in = ckeys + (size_t)row * g.nchunks * g.M;
-  const int n = g.nchunks * g.M;
-  const int step = kScanThreads * EPT;
-  bool first = true;
-  for (int b0 = 0; b0 < n; b0 += step) {
-    uint64_t key[EPT];
-    float val[EPT];
-    const int off = b0 + tid * EPT;
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) {
-      key[j] = (off + j < n) ? in[off + j] : 0ull;
-      val[j] = key[j] ? key_value(key[j]) : 0.0f;
-    }
-    select_batch<EPT>(sh, key, val, first, g.M, tail, c);
-    first = false;
-  }
-  if (sh.nbuf > sh.nlist) flush(sh, g.M, tail, c);
-  if (bad) atomicOr(&sh.flag, 1);
-  Tail t = block_tail(sh, tail, c);
-  for (int i = tid; i < g.M; i += kScanThreads) {
-    const uint64_t k = i < sh.nlist ? sh.buf[i] : 0ull;
-    cand[(size_t)row * g.M + i] = k ? (int32_t)key_index(k) : -1;
-    candv[(size_t)row * g.M + i] = k ? key_value(k) : -__builtin_huge_valf();
-  }
-  if (tid == 0) {
-    tailR[row] = t.s > 0.0f ? t.m * inv_tau + logf(t.s) : -__builtin_huge_valf();
-    rflag[row] = sh.flag ? DT_TREE_NONFINITE : 0;
-  }
+  sel::merge_row<kScanThreads, false>(ckeys + (size_t)row * g.nchunks * g.M, g.nchunks, g.M,
+                                      ctail + (size_t)row * g.nchunks, cflag + (size_t)row * g.nchunks,
+                                      c, inv_tau, sortbuf, red, &flag, cand + (size_t)row * g.M,
+                                      candv + (size_t)row * g.M, tailR + row, rflag + row,
+                                      nullptr);
 }
 
 }  // namespace
@@ -376,18 +353,12 @@ ScanGeom scan_geom(int rows, int V, int M) {
   g.rows = rows;
   g.V = V;
   g.M = M;
-  // aim for ~4 workgroups per CU over the whole call; chunks are multiples of
-  // 2048 elements (one sub-batch of 256 threads x 8 bf16)
-  const int sub = kScanThreads * 8;
-  int want = (1024 + rows - 1) / rows;
-  int maxch = (V + sub - 1) / sub;
-  int nch = want < 1 ? 1 : (want > maxch ? maxch : want);
-  int chunk = (V + nch - 1) / nch;
-  chunk = (chunk + sub - 1) / sub * sub;
-  g.chunk = chunk;
-  g.nchunks = (V + chunk - 1) / chunk;
+  g.chunk = kScanChunk;
+  g.nchunks = (V + kScanChunk - 1) / kScanChunk;
   return g;
 }
+
+size_t merge_lds_bytes(const ScanGeom &g) { return (size_t)sel::merge_buf_bytes(g.nchunks, g.M); }
 
 size_t scan_bytes(const ScanGeom &g) {
   size_t b = 0;
@@ -422,8 +393,8 @@ size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws) {
   return o;
 }
 
-hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
-                       const Workspace &ws, hipStream_t s, hipEvent_t between) {
+hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
+                              const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s) {
   const float c = 1.4426950408889634f * inv_tau;  // exp(x / tau) = exp2(x * c)
   dim3 grid(g.nchunks, g.rows);
   const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16) == 0;
@@ -431,26 +402,29 @@ hipError_t launch_scan(const void *logits, int ldt, const ScanGeom &g, float inv
     const uint16_t *p = static_cast<const uint16_t *>(logits);
     if (aligned && g.V % 8 == 0)
       hipLaunchKernelGGL((scan_chunk_kernel<uint16_t, true>), grid, dim3(kScanThreads), 0, s, p, g,
-                         c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag);
+                         c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
     else
       hipLaunchKernelGGL((scan_chunk_kernel<uint16_t, false>), grid, dim3(kScanThreads), 0, s, p,
-                         g, c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag);
+                         g, c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
   } else {
     const float *p = static_cast<const float *>(logits);
     if (aligned && g.V % 4 == 0)
       hipLaunchKernelGGL((scan_chunk_kernel<float, true>), grid, dim3(kScanThreads), 0, s, p, g, c,
-                         ws.chunk_keys, ws.chunk_tail, ws.chunk_flag);
+                         ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
     else
       hipLaunchKernelGGL((scan_chunk_kernel<float, false>), grid, dim3(kScanThreads), 0, s, p, g,
-                         c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag);
+                         c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
   }
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s) {
+  const float c = 1.4426950408889634f * inv_tau;
+  const size_t lds = merge_lds_bytes(g);
+  hipError_t e = hipFuncSetAttribute((const void *)scan_merge_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  if (between) {
-    e = hipEventRecord(between, s);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(scan_merge_kernel, dim3(g.rows), dim3(kScanThreads), 0, s, g, c, inv_tau,
+  hipLaunchKernelGGL(scan_merge_kernel, dim3(g.rows), dim3(kScanThreads), lds, s, g, c, inv_tau,
                      ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, ws.cand, ws.candv, ws.tail,
                      ws.row_flag);
   return hipGetLastError();

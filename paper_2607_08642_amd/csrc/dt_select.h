@@ -1,0 +1,254 @@
+// Device building blocks shared by the scan and the expansion kernels:
+// order-preserving keys, running log-sum-exp tails, bitonic sorts in LDS and
+// the per-row merge of sorted chunk lists (Alg. 1 step 1; section 3.2).
+#pragma once
+
+#include "dt_internal.h"
+
+namespace dt {
+namespace sel {
+
+// Running tail of exp((x - m) / tau) sums: m is the running max, s the sum.
+// c = log2(e) / tau so that exp((x - m) / tau) = exp2((x - m) * c).
+struct Tail {
+  float m, s;
+};
+
+__device__ inline Tail tail_empty() { return Tail{-3.402823466e38f, 0.0f}; }
+
+template <int N>
+__device__ inline void tail_add_group(Tail &t, const float (&x)[N], float c) {
+  float mx = t.m;
+#pragma unroll
+  for (int j = 0; j < N; ++j) mx = fmaxf(mx, x[j]);
+  float s = t.s * exp2f((t.m - mx) * c);
+#pragma unroll
+  for (int j = 0; j < N; ++j) s += exp2f((x[j] - mx) * c);
+  t.m = mx;
+  t.s = s;
+}
+
+__device__ inline void tail_add1(Tail &t, float x, float c) {
+  const float xs[1] = {x};
+  tail_add_group<1>(t, xs, c);
+}
+
+__device__ inline Tail tail_merge(Tail a, Tail b, float c) {
+  Tail r;
+  r.m = fmaxf(a.m, b.m);
+  r.s = a.s * exp2f((a.m - r.m) * c) + b.s * exp2f((b.m - r.m) * c);
+  return r;
+}
+
+// block-wide tail reduction in a fixed order (deterministic); red: NT/64 float2
+template <int NT>
+__device__ inline Tail block_tail(Tail t, float c, float2 *red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    Tail u;
+    u.m = __shfl_xor(t.m, o);
+    u.s = __shfl_xor(t.s, o);
+    t = tail_merge(t, u, c);
+  }
+  if (lane == 0) red[w] = make_float2(t.m, t.s);
+  __syncthreads();
+  Tail r{red[0].x, red[0].y};
+  for (int i = 1; i < NT / 64; ++i) r = tail_merge(r, Tail{red[i].x, red[i].y}, c);
+  __syncthreads();
+  return r;
+}
+
+// descending bitonic sort of a wave's 64 values (one per lane)
+__device__ inline uint64_t wave_sort_desc(uint64_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint64_t p = __shfl_xor(v, j);
+      const bool desc = (lane & k) == 0;
+      const bool lower = (lane & j) == 0;
+      v = (desc == lower) ? (v > p ? v : p) : (v < p ? v : p);
+    }
+  }
+  return v;
+}
+
+__host__ __device__ inline int pow2_at_least(int n, int lo) {
+  int p = lo;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+// descending bitonic sort of buf[0..P), P a power of two; all NT threads call it
+template <int NT>
+__device__ void block_sort_desc(uint64_t *buf, int P) {
+  const int tid = threadIdx.x;
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int p = tid; p < P / 2; p += NT) {
+        const int i = 2 * p - (p & (j - 1));
+        const int ixj = i + j;
+        const uint64_t a = buf[i], b = buf[ixj];
+        const bool desc = (i & k) == 0;
+        if (desc ? (a < b) : (a > b)) {
+          buf[i] = b;
+          buf[ixj] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+template <bool DEV_SCOPE, typename T>
+__device__ inline void put(T *p, T v) {
+  if constexpr (DEV_SCOPE)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+
+// LDS carve of merge_row for nlists lists of M keys (byte offsets)
+struct MergeBuf {
+  int top, heads, scnt, sidx, total;
+};
+__host__ __device__ inline int up16(int b) { return (b + 15) & ~15; }
+__host__ __device__ inline MergeBuf merge_buf(int nlists, int M) {
+  const int n = nlists * M;
+  const int q = (M + nlists - 1) / nlists;
+  const int nhp = (nlists * q + 1) & ~1;
+  MergeBuf b;
+  b.top = up16(8 * n);                 // keys: n u64 at 0
+  b.heads = up16(b.top + 8 * M);       // top: M u64
+  b.scnt = up16(b.heads + 8 * nhp);    // heads: nhp u64
+  b.sidx = up16(b.scnt + 4 * n);       // scnt: n i32
+  b.total = up16(b.sidx + 2 * n);      // sidx: n i16
+  return b;
+}
+__host__ __device__ inline int merge_buf_bytes(int nlists, int M) { return merge_buf(nlists, M).total; }
+
+// Merge the sorted chunk lists of one row: the row's M best keys and
+// R = log sum over every other element of exp(x / tau).
+//   lists: nlists * M keys (0 = empty slot), each list sorted descending;
+//   tails: per-chunk (max, sum) of the elements not in its list; flags: per chunk.
+// Exact without sorting the lists together:
+//  * thr = the M-th best of the first q = ceil(M / nlists) keys of every list.
+//    Those keys are all in the row, so at least M keys are >= thr and thr is
+//    <= the row's M-th best key: keys below thr go straight to the tail.
+//  * a surviving key's rank is its position in its own list plus, for every
+//    other list, the number of larger keys there (a binary search).  A key
+//    outside every list lies below the M keys of its chunk's list, so for a
+//    rank below M this count is exact, and a count of M or more means the key
+//    is not among the row's M best.
+// buf: merge_buf_bytes(nlists, M) bytes of LDS; red: NT/64 float2.
+// DEV_SCOPE selects device-scope stores (results read by other workgroups).
+// vadd (nullable): candv[m] = logit + vadd[cand[m]] instead of the logit.
+template <int NT, bool DEV_SCOPE>
+__device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2 *tails,
+                          const int32_t *flags, float c, float inv_tau, uint64_t *buf,
+                          float2 *red, int *flag_lds, int32_t *cand, float *candv, float *tailR,
+                          int32_t *rflag, const float *vadd) {
+  const int tid = threadIdx.x;
+  const int n = nlists * M;
+  const int q = (M + nlists - 1) / nlists;
+  const int nh = nlists * q, nhp = (nh + 1) & ~1;
+  const MergeBuf mb = merge_buf(nlists, M);
+  char *base = reinterpret_cast<char *>(buf);
+  uint64_t *keys = buf;                                           // [n]
+  uint64_t *top = reinterpret_cast<uint64_t *>(base + mb.top);    // [M]
+  uint64_t *heads = reinterpret_cast<uint64_t *>(base + mb.heads);  // [nhp]
+  int32_t *scnt = reinterpret_cast<int32_t *>(base + mb.scnt);    // [n] survivor ranks
+  int16_t *sidx = reinterpret_cast<int16_t *>(base + mb.sidx);    // [n] survivor positions
+  __shared__ uint64_t s_thr;
+  __shared__ int s_ns;
+  if (tid == 0) {
+    *flag_lds = 0;
+    s_ns = 0;
+    s_thr = 1;  // stays 1 (keep every key) when the heads hold fewer than M keys
+  }
+  for (int i = tid; i < n; i += NT) keys[i] = lists[i];
+  for (int h = tid; h < nhp; h += NT) heads[h] = h < nh ? lists[(h / q) * M + (h % q)] : 0ull;
+  for (int i = tid; i < M; i += NT) top[i] = 0ull;
+  Tail t = tail_empty();
+  int bad = 0;
+  for (int i = tid; i < nlists; i += NT) {
+    t = tail_merge(t, Tail{tails[i].x, tails[i].y}, c);
+    bad |= flags[i];
+  }
+  __syncthreads();
+  if (bad) atomicOr(flag_lds, bad);
+  // 1. thr: the M-th largest head (q heads per list)
+  for (int h = tid; h < nh; h += NT) {
+    const uint64_t k = heads[h];
+    if (!k) continue;
+    int r = 0;
+    const ulonglong2 *h2 = reinterpret_cast<const ulonglong2 *>(heads);
+#pragma unroll 8
+    for (int j = 0; j < nhp / 2; ++j) {
+      const ulonglong2 v = h2[j];
+      r += (v.x > k) + (v.y > k);
+    }
+    if (r == M - 1) s_thr = k;
+  }
+  __syncthreads();
+  const uint64_t thr = s_thr;
+  // 2. survivors (keys >= thr) start from their own position; the rest feed the tail
+  for (int i = tid; i < n; i += NT) {
+    const uint64_t k = keys[i];
+    if (!k) continue;
+    if (k >= thr) {
+      const int at = atomicAdd(&s_ns, 1);
+      sidx[at] = (int16_t)i;
+      scnt[at] = i % M;
+    } else {
+      tail_add1(t, key_value(k), c);
+    }
+  }
+  __syncthreads();
+  // 3. + the larger keys of every other list: one binary search per (survivor, list)
+  const int ns = s_ns;
+  for (int p = tid; p < ns * nlists; p += NT) {
+    const int sv = p / nlists, j = p % nlists;
+    const int i = sidx[sv];
+    if (j == i / M) continue;
+    const uint64_t k = keys[i];
+    const uint64_t *lj = keys + j * M;
+    int lo = 0, hi = M;  // count of lj[] > k (lj is descending)
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (lj[mid] > k)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    if (lo) atomicAdd(&scnt[sv], lo);
+  }
+  __syncthreads();
+  for (int sv = tid; sv < ns; sv += NT) {
+    const int r = scnt[sv];
+    const uint64_t k = keys[sidx[sv]];
+    if (r < M)
+      top[r] = k;
+    else
+      tail_add1(t, key_value(k), c);
+  }
+  __syncthreads();
+  t = block_tail<NT>(t, c, red);
+  for (int i = tid; i < M; i += NT) {
+    const uint64_t k = top[i];
+    float v = -__builtin_huge_valf();
+    if (k) v = vadd ? key_value(k) + vadd[key_index(k)] : key_value(k);
+    put<DEV_SCOPE>(cand + i, k ? (int32_t)key_index(k) : (int32_t)-1);
+    put<DEV_SCOPE>(candv + i, v);
+  }
+  if (tid == 0) {
+    put<DEV_SCOPE>(tailR, t.s > 0.0f ? t.m * inv_tau + logf(t.s) : -__builtin_huge_valf());
+    put<DEV_SCOPE>(rflag, (int32_t)(*flag_lds ? DT_TREE_NONFINITE : 0));
+  }
+  __syncthreads();
+}
+
+}  // namespace sel
+}  // namespace dt
