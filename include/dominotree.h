@@ -159,7 +159,12 @@ dt_status dt_workspace_size(const dt_plan *plan, int batch, size_t *bytes);
  *   T:  temperature (T <= 0 scores with tau = 1);
  *   workspace: >= dt_workspace_size bytes, 256-byte aligned, caller-owned;
  *   out: output arrays as documented in dt_tree.
- * Launches on `stream` and returns without waiting. */
+ * Launches on `stream` and returns without waiting.  For small batches several
+ * workgroups (at most one per CU in total) build each tree together and wait
+ * on one another; they rely on being resident at the same time, which holds on
+ * a device that other work does not fill.  Each wait is bounded: a tree whose
+ * workgroups could not meet carries DT_TREE_TIMEOUT.  A workspace must not be
+ * shared by calls that can overlap. */
 dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, const float *h0,
                         float T, void *workspace, size_t ws_bytes, dt_tree *out, void *stream);
 

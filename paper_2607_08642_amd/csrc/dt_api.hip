@@ -53,7 +53,8 @@ Workspace carve(const dt_plan *p, int batch, char *base) {
   ws.ecap = ecap_for(p);
   ws.states = at((size_t)batch * ws.ecap * p->d_h * sizeof(float));
   ws.part = at(expand_part_bytes(p, batch));
-  ws.bar = reinterpret_cast<int32_t *>(at((size_t)batch * kBarStride * sizeof(int32_t)));
+  // per tree: barrier counters; then the member-slot counters of the launch
+  ws.bar = reinterpret_cast<int32_t *>(at((size_t)(batch + 2) * kBarStride * sizeof(int32_t)));
   ws.bytes = o;
   return ws;
 }
@@ -249,7 +250,7 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   hipError_t e = prof ? hipEventRecord(plan->ev[0], s) : hipSuccess;
   // the scan kernel also clears the expansion kernel's barrier counters
   if (e == hipSuccess)
-    e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, batch * dt::kBarStride, s);
+    e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, (batch + 2) * dt::kBarStride, s);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
   if (prof) e = hipEventRecord(plan->ev[1], s);
   if (e == hipSuccess) e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);

@@ -45,6 +45,7 @@ constexpr int NC = kNodeCap;
 constexpr int CH = kChunkNodes;
 constexpr int kSpinLimit = 1 << 18;  // ~0.3 s: a wait this long means a fault
 static_assert(CH == 16, "MFMA column count");
+static_assert(CH == 2 * NW, "children step: two nodes per wave");
 
 struct ExpArgs {
   int L, M, B, k, dh, G, norm_mode, pos_offset, ecap, batch, nchunks, nxcd;
@@ -62,9 +63,9 @@ struct ExpArgs {
   const void *whh;
   const float *b_hh;
   const float *h0;
-  float *states;   // [batch][ecap][dh]
+  float *states;   // [batch][ecap][dh] path states of expanded nodes; slot ecap-1: the root
   float *part;     // [batch][2][G][CH][MP] partial corrections
-  int32_t *bar;    // [batch][kBarStride] barrier counters (zeroed by the scan kernel)
+  int32_t *bar;    // [batch + 2][kBarStride] barrier and slot counters (zeroed by the scan kernel)
   dt_tree out;
 };
 
@@ -123,7 +124,7 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks) {
 }
 
 // scalar slots in LDS
-enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_CNT0 };
+enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CNT0 };
 
 __device__ inline uint16_t f2bf(float x) {
   uint32_t u = __float_as_uint(x);
@@ -159,6 +160,38 @@ __device__ inline float4 ld_dev16(__amdgpu_buffer_rsrc_t r, int byte_off) {
 }
 __device__ inline float ld_dev4(__amdgpu_buffer_rsrc_t r, int byte_off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, kSc1));
+}
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// the G (<= 16) partial corrections of one slot
+struct Parts {
+  float4 q[4];
+};
+__device__ inline float part_at(const Parts &p, int j) {
+  const float4 v = p.q[j >> 2];
+  switch (j & 3) {
+    case 0: return v.x;
+    case 1: return v.y;
+    case 2: return v.z;
+    default: return v.w;
+  }
+}
+
+// GRU inputs of 4 consecutive hidden units j0..j0+3 of one node: P of gates
+// r, z, n (P = the token's folded input projection) and b_hn
+struct GruIn {
+  float4 r, z, n, b;
+};
+__device__ inline GruIn load_gru_in(const float *prow, const float *b_hh, int dh, int j0) {
+  GruIn g;
+  g.r = *reinterpret_cast<const float4 *>(prow + j0);
+  g.z = *reinterpret_cast<const float4 *>(prow + dh + j0);
+  g.n = *reinterpret_cast<const float4 *>(prow + 2 * dh + j0);
+  g.b = *reinterpret_cast<const float4 *>(b_hh + 2 * dh + j0);
+  return g;
+}
+__device__ inline void st_dev16(__amdgpu_buffer_rsrc_t r, int byte_off, float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, kSc1);
 }
 
 __device__ inline uint64_t wave_max_u64(uint64_t v) {
@@ -360,9 +393,18 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   const float NEG_INF = -__builtin_huge_valf();
 
   // ---- which tree, which member (members of a tree share an XCD) ------------
+  // Workgroups take member slots in the order they start running, from one
+  // counter per XCD class (blocks are dealt to XCDs round-robin): complete
+  // groups form first, so members never wait for a workgroup that cannot be
+  // scheduled while the rest of the grid holds the CUs.
   int t, member;
   if (G > 1) {
-    const int xcd = blockIdx.x % a.nxcd, kk = blockIdx.x / a.nxcd;
+    const int xcd = blockIdx.x % a.nxcd;
+    if (tid == 0)
+      scal[S_SLOT] = __hip_atomic_fetch_add(a.bar + a.batch * kBarStride + xcd * 16, 1,
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const int kk = scal[S_SLOT];
     t = xcd + a.nxcd * (kk / G);
     member = kk % G;
   } else {
@@ -394,6 +436,14 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
                              a.c2, a.inv_tau, sortbuf, red, &scal[S_MERGEFLAG],
                              a.cand + (size_t)row * M, a.candv + (size_t)row * M, a.tailR + row,
                              a.rflag + row, a.c_all);
+  }
+  {
+    // the root's path state (h0 or zeros) in slot ecap-1: this member's units
+    float *root = a.states + ((size_t)t * a.ecap + a.ecap - 1) * dh;
+    for (int u = tid; u < UW; u += NT) {
+      const int j = member * UW + u;
+      st_dev(root + j, a.h0 ? a.h0[(size_t)t * dh + j] : 0.0f);
+    }
   }
   group_barrier(ctr, G, nbar, &scal[S_STATUS]);
   {
@@ -434,10 +484,18 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // candidates and tail) and the parent path states of the chunk's nodes
     const int32_t *ccand = rcand;
     const float *ccandv = rcandv;
-    if (tid == 0 && d > 0)
-      for (int c = 0; c < nc; ++c) nstate[cn[c]] = (int16_t)(scal[S_NEXP] + c);
+    if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
+    // GRU inputs of the first unit group this wave finishes (unit group gi =
+    // wave): P of gates r, z, n and b_hn for units 4 (lane/16) .. +3 of node lane%16
+    GruIn pre;
+    pre.r = pre.z = pre.n = pre.b = make_float4(0.f, 0.f, 0.f, 0.f);
     {
       // all loads are issued before the first LDS write (one wait)
+      if (d > 0 && wave < NG && (lane & 15) < nc) {
+        const float *prow = a.P_all + (size_t)ntok[cn[lane & 15]] * (3 * dh);
+        const int j0 = member * UW + wave * 16 + (lane >> 4) * 4;
+        pre = load_gru_in(prow, a.b_hh, dh, j0);
+      }
       const size_t row = (size_t)t * L + (d < L ? d : 0);
       const __amdgpu_buffer_rsrc_t rc = dev_rsrc(a.cand + row * M);
       const __amdgpu_buffer_rsrc_t rv = dev_rsrc(a.candv + row * M);
@@ -450,22 +508,21 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         cval = ld_dev4(rv, tid * 4);
       }
       if (d < L && tid == NT - 1) rt = ld_dev(a.tailR + row);
-      constexpr int kSpPer = CH * kMaxDh / 4 / NT;  // float4 per thread, at most
-      const int nv = d > 0 ? CH * dh / 4 : 0;
-      float4 v[kSpPer];
-#pragma unroll
-      for (int j = 0; j < kSpPer; ++j) {
-        const int i = tid + j * NT;
-        v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (i < nv) {
-          const int c = (i * 4) / dh, k = (i * 4) % dh;
+      // parent states straight into LDS (16 bytes per lane, 256 floats per
+      // wave instruction); unused columns read the root slot
+      if (d > 0) {
+        const int root_slot = a.ecap - 1;
+        for (int i = wave; i < CH * dh / 256; i += NW) {
+          const int e = i * 256 + 4 * lane;
+          const int c = e / dh, k = e - c * dh;
+          int slot = root_slot;
           if (c < nc) {
             const int par = nparent[cn[c]];
-            if (par >= 0)
-              v[j] = ld_dev16(rs, (nstate[par] * dh + k) * 4);
-            else if (a.h0)
-              v[j] = *reinterpret_cast<const float4 *>(a.h0 + (size_t)t * dh + k);
+            if (par >= 0) slot = nstate[par];
           }
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rs, (__attribute__((address_space(3))) void *)(Sp + i * 256), 16,
+              (slot * dh + k) * 4, 0, 0, kSc1);
         }
       }
       if (tid < MP) {
@@ -473,11 +530,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         rcandv[tid] = rowld ? cval : NEG_INF;
       }
       if (tid == NT - 1) scalf[S_R] = rt;
-#pragma unroll
-      for (int j = 0; j < kSpPer; ++j) {
-        const int i = tid + j * NT;
-        if (i < nv) *reinterpret_cast<float4 *>(Sp + i * 4) = v[j];
-      }
+      __builtin_amdgcn_s_waitcnt(0);  // includes the LDS writes of the loads above
     }
     __syncthreads();
     // 1. path states of this member's units: S = GRU(S_parent, E[token]) (section 2.3)
@@ -490,31 +543,34 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       const int c = lane & 15;
       const int node = c < nc ? cn[c] : -1;
       const float *prow = a.P_all + (size_t)(node >= 0 ? ntok[node] : 0) * (3 * dh);
-      float *srow = a.states + ((size_t)t * a.ecap + (node >= 0 ? nstate[node] : 0)) * dh;
-      auto apply = [&](int gi, const f32x4 (&gh)[3]) {
+      // r = sig(P_r + W_hr h), z = sig(P_z + W_hz h), n = tanh(P_n + r (W_hn h + b_hn)),
+      // S = (1 - z) n + z h  (P_r, P_z carry b_hr, b_hz)
+      auto apply = [&](int gi, const f32x4 (&gh)[3], GruIn in) {
         if (node < 0) return;
+        const int u4 = gi * 16 + (lane >> 4) * 4;  // first of this lane's 4 units (in the member)
+        const int j0 = member * UW + u4;
+        const float xr[4] = {in.r.x, in.r.y, in.r.z, in.r.w}, xz[4] = {in.z.x, in.z.y, in.z.z, in.z.w};
+        const float xn[4] = {in.n.x, in.n.y, in.n.z, in.n.w}, xb[4] = {in.b.x, in.b.y, in.b.z, in.b.w};
+        float sv[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int ul = gi * 16 + (lane >> 4) * 4 + i;  // unit within this member
-          const int j = member * UW + ul;
-          const float hr = gh[0][i] + a.b_hh[j];
-          const float hz = gh[1][i] + a.b_hh[dh + j];
-          const float hn = gh[2][i] + a.b_hh[2 * dh + j];
-          const float r = sigmoidf_(prow[j] + hr);
-          const float z = sigmoidf_(prow[dh + j] + hz);
-          const float n = tanhf(prow[2 * dh + j] + r * hn);
-          const float hprev = Sp[c * dh + j];
-          const float sv = (1.0f - z) * n + z * hprev;
-          Sn[c * UW + ul] = sv;
-          st_dev(srow + j, sv);
+          const float r = sigmoidf_(xr[i] + gh[0][i]);
+          const float z = sigmoidf_(xz[i] + gh[1][i]);
+          const float n = tanhf(xn[i] + r * (gh[2][i] + xb[i]));
+          const float hprev = Sp[c * dh + j0 + i];
+          sv[i] = (1.0f - z) * n + z * hprev;
+          Sn[c * UW + u4 + i] = sv[i];
         }
+        const __amdgpu_buffer_rsrc_t rsw = dev_rsrc(a.states + (size_t)t * a.ecap * dh);
+        st_dev16(rsw, (nstate[node] * dh + j0) * 4, make_float4(sv[0], sv[1], sv[2], sv[3]));
       };
       const int nks = dh / 32;
       if (NG >= NW) {
         for (int gi = wave; gi < NG; gi += NW) {
           f32x4 gh[3];
           Gates<TW>::run(a, Sp, u0 + gi, 0, nks, gh);
-          apply(gi, gh);
+          apply(gi, gh, gi == wave ? pre
+                                   : load_gru_in(prow, a.b_hh, dh, member * UW + gi * 16 + (lane >> 4) * 4));
         }
       } else {
         // WPG waves split the k range of one unit group; partial sums meet in LDS
@@ -539,7 +595,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
               for (int ff = 0; ff < WPG; ++ff) s += gpart[(((ff * NG + wave) * 3 + g) * 64 + lane) * 4 + i];
               sum[g][i] = s;
             }
-          apply(wave, sum);
+          apply(wave, sum, pre);
         }
       }
     }
@@ -575,46 +631,36 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     const float R = scalf[S_R];
     const __amdgpu_buffer_rsrc_t rp = dev_rsrc(a.part + ((size_t)t * 2 + pb) * CH * MP * G);
     pb ^= 1;
-    for (int c = wave; c < CH; c += NW) {
-      if (c >= nc) {
-        if (lane == 0) wcnt[c] = 0;
-        continue;
+    // the G parts of a slot are contiguous: all loads are issued, then summed in order
+    auto load_parts = [&](int c, int m) -> Parts {
+      Parts p;
+      const int off = ((c * MP + m) * G) * 4;
+      if (G >= 4) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          if (q4 * 4 < G) p.q[q4] = ld_dev16(rp, off + q4 * 16);
+      } else {
+        p.q[0].x = ld_dev4(rp, off);
+        if (G > 1) p.q[0].y = ld_dev4(rp, off + 4);
       }
+      return p;
+    };
+    auto node_children = [&](int c, const Parts &p0) {
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
       float zv[4];
       float mx = NEG_INF;
-      for (int s = 0; s < MP / 64; ++s) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s >= MP / 64) break;
         const int m = lane + 64 * s;
-        float z = NEG_INF;
-        if (m < M) {
-          const float x = ccandv[m];
-          if (x > NEG_INF) {
-            // the G parts of this slot are contiguous: load them all, then sum in order
-            float pv[16];
-            const int off = ((c * MP + m) * G) * 4;
-            if (G >= 4) {
+        const Parts p = s == 0 ? p0 : load_parts(c, m);
+        // x already holds logit + E[v] . b_c (added by the row merge)
+        const float x = ccandv[m];
+        float dl = x;
 #pragma unroll
-              for (int q4 = 0; q4 < 4; ++q4)
-                if (q4 * 4 < G) {
-                  const float4 v4 = ld_dev16(rp, off + q4 * 16);
-                  pv[q4 * 4] = v4.x;
-                  pv[q4 * 4 + 1] = v4.y;
-                  pv[q4 * 4 + 2] = v4.z;
-                  pv[q4 * 4 + 3] = v4.w;
-                }
-            } else {
-#pragma unroll
-              for (int j = 0; j < 4; ++j)
-                if (j < G) pv[j] = ld_dev4(rp, off + j * 4);
-            }
-            // x already holds logit + E[v] . b_c (added by the row merge)
-            float dl = x;
-#pragma unroll
-            for (int j = 0; j < 16; ++j)
-              if (j < G) dl += pv[j];
-            z = dl * a.inv_tau;
-          }
-        }
+        for (int j = 0; j < 16; ++j)
+          if (j < G) dl += part_at(p, j);
+        const float z = x > NEG_INF ? dl * a.inv_tau : NEG_INF;  // slots >= M hold -inf
         zv[s] = z;
         mx = fmaxf(mx, z);
       }
@@ -622,12 +668,16 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       const bool tail = (a.norm_mode == DT_NORM_TAIL) && R > NEG_INF;
       if (tail) mx = fmaxf(mx, R);
       float sum = 0.0f;
-      for (int s = 0; s < MP / 64; ++s) sum += (zv[s] > NEG_INF) ? expf(zv[s] - mx) : 0.0f;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        if (s < MP / 64) sum += (zv[s] > NEG_INF) ? expf(zv[s] - mx) : 0.0f;
       sum = wave_sum_f(sum);
       if (tail) sum += expf(R - mx);
       const float logZ = mx + logf(sum);
       float lv[4];
-      for (int s = 0; s < MP / 64; ++s) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s >= MP / 64) break;
         const int m = lane + 64 * s;
         lv[s] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
         ell[c * MP + m] = lv[s];
@@ -635,12 +685,14 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       wave_sync();
       int kc = 0;
       const float4 *e4 = reinterpret_cast<const float4 *>(ell + c * MP);
-      for (int s = 0; s < MP / 64; ++s) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s >= MP / 64) break;
         const int m = lane + 64 * s;
         const float lm = lv[s];
         // rank = slots ahead of m by (log-prob desc, slot asc); slots >= M hold -inf
         int rank = 0;
-#pragma unroll 16
+#pragma unroll 4
         for (int q = 0; q < MP / 4; ++q) {
           const float4 v = e4[q];
           const int m2 = 4 * q;
@@ -654,7 +706,20 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         rnk[c * MP + m] = keep ? (int16_t)rank : (int16_t)-1;
       }
       if (lane == 0) wcnt[c] = kc;
-    }
+    };
+    // two nodes per wave: the second node's loads are in flight during the first
+    const int c0 = wave, c1 = wave + NW;
+    Parts p0, p1;
+    if (c0 < nc) p0 = load_parts(c0, lane);
+    if (c1 < nc) p1 = load_parts(c1, lane);
+    if (c0 < nc)
+      node_children(c0, p0);
+    else if (lane == 0)
+      wcnt[c0] = 0;
+    if (c1 < nc)
+      node_children(c1, p1);
+    else if (lane == 0)
+      wcnt[c1] = 0;
     __syncthreads();
     // 4. append children (node order, then rank order) to the node table
     const int base = scal[S_NN];
@@ -664,7 +729,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       int off = base;
       for (int c2 = 0; c2 < c; ++c2) off += wcnt[c2];
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
-      for (int s = 0; s < MP / 64; ++s) {
+      #pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s >= MP / 64) break;
         const int m = lane + 64 * s;
         const int rk = m < M ? rnk[c * MP + m] : -1;
         if (rk >= 0) {
@@ -708,7 +775,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       for (int i = tid; i < nn; i += NT) {
         const float gi = ng[i];
         int cnt = 0;
-#pragma unroll 8
+#pragma unroll 4
         for (int j = 0; j < n4; ++j) {
           const float4 v = g4[j];
           cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
@@ -826,7 +893,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         if (lane == 0) {
           scal[S_NC] = c;
           scal[S_TOT] = p;
-          if (c && scal[S_NEXP] + c > a.ecap) {
+          if (c && scal[S_NEXP] + c > a.ecap - 1) {
             scal[S_STATUS] |= DT_TREE_TRUNCATED;
             scal[S_STOP] = 1;
           }
@@ -1019,7 +1086,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 
 int expand_group_size(int d_h, int num_cus, int batch) {
   // largest power-of-two group (<= 16, >= 32 units per member) whose grid fits
-  // one workgroup per CU for a cooperative launch
+  // one workgroup per CU
   int G = 16;
   while (G > 1 && (d_h / G < 32 || (d_h / G) % 16 != 0 || 8 * G * ((batch + 7) / 8) > num_cus))
     G >>= 1;
@@ -1075,15 +1142,14 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
                                      : (const void *)expand_kernel<float>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  if (a.G > 1) {
-    const int grid = 8 * a.G * ((batch + 7) / 8);
-    void *args[] = {&a};
-    return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NT), args, (unsigned)lds, s);
-  }
+  // G > 1: the grid is at most one workgroup per CU (expand_group_size), so
+  // every member is resident on an otherwise idle device; members take their
+  // slots in start order and every wait is bounded (DT_TREE_TIMEOUT).
+  const int grid = a.G > 1 ? 8 * a.G * ((batch + 7) / 8) : batch;
   if (p->wdt == DT_BF16)
-    hipLaunchKernelGGL(expand_kernel<uint16_t>, dim3(batch), dim3(NT), lds, s, a);
+    hipLaunchKernelGGL(expand_kernel<uint16_t>, dim3(grid), dim3(NT), lds, s, a);
   else
-    hipLaunchKernelGGL(expand_kernel<float>, dim3(batch), dim3(NT), lds, s, a);
+    hipLaunchKernelGGL(expand_kernel<float>, dim3(grid), dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 

@@ -4,7 +4,8 @@
 // correction that the top-M candidates need.  Here the rows are model-only
 // quantities, so they are computed once per plan for the whole vocabulary and
 // every call just gathers them:
-//   P[v] = W_ih E[v] + b_ih   (GRU input projection of token v, 3*d_h)
+//   P[v] = W_ih E[v] + b_ih (+ b_hh on the r and z gates, which only ever
+//          appear summed with it; GRU input projection of token v, 3*d_h)
 //   U[v] = W_c^T E[v]         (so delta(v) = U[v] . S + c[v] = E[v] . (W_c S + b_c))
 //   c[v] = E[v] . b_c
 // This is one GEMM of the embedding table against the packed matrix
@@ -213,6 +214,12 @@ __global__ void widen_kernel(const TW *__restrict__ in, int n, float *__restrict
     out[i] = in ? wval<TW>(in, i) : 0.0f;
 }
 
+// dst[i] += src[i]: folds b_hh's r and z parts into the input-side bias
+__global__ void add_kernel(float *__restrict__ dst, const float *__restrict__ src, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    dst[i] += src[i];
+}
+
 // W_hh packed in MFMA A-fragment order for the expansion kernel.
 // bf16 (16x16x32 MFMA): fragment (u, g, ks) is 64 lanes x 8 bf16; lane l holds
 //   W_hh[g*d_h + 16u + l%16][ks*32 + (l/16)*8 + e], e = 0..7.
@@ -288,6 +295,7 @@ hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipS
     hipLaunchKernelGGL(pack_whh_f32_kernel, dim3(grid_for((size_t)3 * d_h * d_h)), dim3(256), 0, s,
                        (const float *)gru->w_hh, d_h, (float *)p->whh_t);
   }
+  hipLaunchKernelGGL(add_kernel, dim3(grid_for(2 * d_h)), dim3(256), 0, s, p->b_ih, p->b_hh, 2 * d_h);
   return hipGetLastError();
 }
 

@@ -79,11 +79,11 @@ struct dt_plan {
   const void *emb;
   void *wfold;      // [nf_pad, d_e] (weights dtype): rows [0,3dh) = W_ih, [3dh,4dh) = W_c^T;
                     // only alive while the plan is created
-  float *P_all;     // [V][3dh]  W_ih E[v] + b_ih
+  float *P_all;     // [V][3dh]  W_ih E[v] + b_ih + (b_hh on gates r, z)
   float *U_all;     // [V][dh]   W_c^T E[v]
   float *c_all;     // [V]       E[v] . b_c
   int nf, nf_pad;   // nf = 4*d_h
-  float *b_ih;      // [3dh] fp32 (zeros when absent)
+  float *b_ih;      // [3dh] fp32 b_ih + (b_hh on gates r, z); zeros when absent
   float *b_hh;      // [3dh] fp32
   float *b_c;       // [d_e] fp32 (zeros when absent)
   int has_bc;
