@@ -202,34 +202,14 @@ __device__ inline uint64_t wave_max_u64(uint64_t v) {
   }
   return v;
 }
-// Wave-wide reductions with DPP inside each row of 16 lanes (quad swaps, half
-// mirror, mirror) and four lane reads across rows; every lane gets the same
-// value.  The whole wave must be active.
-template <int CTRL>
-__device__ inline float dpp_f(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
-                                                               0xF, 0xF, false));
-}
-template <typename Op>
-__device__ inline float wave_reduce(float v, Op op) {
-  v = op(v, dpp_f<0xB1>(v));   // quad_perm [1,0,3,2]
-  v = op(v, dpp_f<0x4E>(v));   // quad_perm [2,3,0,1]
-  v = op(v, dpp_f<0x141>(v));  // row_half_mirror
-  v = op(v, dpp_f<0x140>(v));  // row_mirror
-  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
-  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
-  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
-  return op(op(a, b), op(c, d));
-}
 __device__ inline float wave_max_f(float v) {
-  return wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
+  return sel::wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
 }
 __device__ inline float wave_sum_f(float v) {
-  return wave_reduce(v, [](float x, float y) { return x + y; });
+  return sel::wave_reduce(v, [](float x, float y) { return x + y; });
 }
 __device__ inline float wave_min_f(float v) {
-  return wave_reduce(v, [](float x, float y) { return fminf(x, y); });
+  return sel::wave_reduce(v, [](float x, float y) { return fminf(x, y); });
 }
 
 // ordered exclusive prefix of a predicate over the block (wcnt: NW ints in LDS)

@@ -23,6 +23,8 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPerThread = 40;                         // elements held per thread
 constexpr int kScanChunk = kScanThreads * kScanPerThread;  // 10240
 constexpr int kScanSortCap = 4096;   // bitonic sort buffer (keys) per workgroup
+constexpr int kScanTargetGroups = 1024;  // scan workgroups worth launching (4 per CU)
+constexpr int kScanMaxBatches = 8;       // batches of kScanChunk per segment, at most
 constexpr int kScanFlushAt = 256;    // fallback: flush the candidate buffer beyond this
 constexpr int kMergeLdsMax = 96 * 1024;  // row merge buffer: 14 n + 8 M bytes, n = ceil(V/kScanChunk) M
 
@@ -68,7 +70,9 @@ __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint3
 // plan
 // ---------------------------------------------------------------------------
 struct ScanGeom {
-  int rows, V, M, chunk, nchunks;
+  int rows, V, M;
+  int chunk;    // elements per segment (a multiple of kScanChunk)
+  int nchunks;  // segments (= sorted lists) per row
 };
 
 }  // namespace dt

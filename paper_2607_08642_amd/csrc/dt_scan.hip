@@ -6,19 +6,21 @@
 // loads in flight at once) and selects the chunk's M best elements exactly:
 //   * keys are 64-bit (order-preserving value bits, ~index), so the order
 //     (value desc, id asc) is a plain integer order without ties;
-//   * every wave sorts its 64 per-lane maximum keys and takes the ceil(M/4)-th;
-//     the minimum over the 4 waves leaves at least M elements at or above it,
-//     so it is an exact lower bound on the chunk's M-th best key;
-//   * elements below that bound go straight into the running tail sum
-//     (max, sum exp((x - max)/tau)); the survivors (about 1% of the chunk on
-//     drafter-like rows) are compacted into LDS and bitonic-sorted once; the
-//     best M are the chunk's list, the rest join the tail.
-// If the survivors overflow the sort buffer (adversarial rows: long runs of
-// equal or monotone values), they are streamed through a bounded selector that
-// keeps a sorted list of M and flushes a candidate buffer instead.
-// The per-row merge (merge_row) sorts the chunk lists of a row together and
-// folds the chunk tails; it runs inside the expansion kernel, or in a small
-// kernel of its own for dt_scan_topm.
+//   * every wave finds the ceil(M/4)-th largest of its 64 per-lane maxima (a
+//     bitwise search with one ballot per bit); the minimum over the 4 waves
+//     leaves at least M elements at or above it, so it is an exact lower bound
+//     on the chunk's M-th best element;
+//   * a pass over the registers sends elements below that bound into the
+//     running tail sum (max, sum exp((x - max)/tau)); the survivors (about 1%
+//     of the chunk on drafter-like rows) go to a per-wave region of LDS;
+//     each survivor is ranked by counting the larger ones, the best M are the
+//     chunk's list and the rest join the tail.
+// Many survivors are bitonic-sorted instead; if a wave's survivors overflow
+// its region (adversarial rows: long runs of equal or monotone values), they
+// are streamed through a bounded selector that keeps a sorted list of M.
+// The per-row merge (merge_row) combines the chunk lists and tails of a row;
+// it runs inside the expansion kernel, or in a small kernel of its own for
+// dt_scan_topm.
 #include "dt_select.h"
 
 namespace dt {
@@ -29,10 +31,14 @@ using sel::Tail;
 
 constexpr int kWaves = kScanThreads / 64;
 
+constexpr int kRegion = kScanSortCap / kWaves;       // candidate keys per wave
+constexpr int kRegionCap = kRegion - kMaxM / kWaves;  // fill limit: the list fits beside them
+
 struct ScanLDS {
-  uint64_t buf[kScanSortCap];
-  uint64_t wthr[kWaves];
+  alignas(16) uint64_t buf[kScanSortCap];
   float2 red[kWaves];
+  int wcnt[kWaves];
+  int wprev[kWaves];
   int nbuf;
   int nlist;
   int flag;
@@ -119,189 +125,336 @@ __device__ inline float to_f32<float>(float x) {
   return x;
 }
 
-// fp32 class test: NaN or +inf (v_cmp_class)
-__device__ inline bool nonfinite(float v) { return __builtin_amdgcn_class(v, 0x203); }
-
-// descending bitonic sort of a wave's 64 floats (one per lane)
-__device__ inline float wave_sort_desc_f(float v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const float p = __shfl_xor(v, j);
-      const bool desc = (lane & k) == 0;
-      const bool lower = (lane & j) == 0;
-      v = (desc == lower) ? fmaxf(v, p) : fminf(v, p);
-    }
-  }
-  return v;
-}
-
-// inclusive prefix sum over a wave
+// inclusive prefix sum over a wave: shifted adds inside rows of 16 lanes (DPP
+// row_shr 1, 2, 4, 8), then the totals of the rows below
 __device__ inline int wave_incl_scan(int x) {
   const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  return x;
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
+  const int r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = lane >> 4;
+  return x + (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
 }
 
-// K1: exact top-M of one chunk (kScanChunk elements) of one row, plus the tail
-// of the rest.  Also clears `zero_n` ints at `zero_ptr` (barrier counters of
-// the expansion kernel that follows on the stream).
+// Raw registers of one batch: kScanPerThread elements per thread as 16-byte loads
+template <typename T>
+struct Raw {
+  static constexpr int NL = kScanPerThread / Elem<T>::EPL;
+  uint4 q[NL];
+};
+
+// Issue the loads of one batch (element (j, e) of this thread sits at batch
+// offset j*STEP + tid*EPL + e); nothing waits for them here.
+template <typename T, bool VEC>
+__device__ inline void load_batch(Raw<T> &r, const T *base, int bn) {
+  constexpr int EPL = Elem<T>::EPL;
+  constexpr int STEP = kScanThreads * EPL;
+  int lb = threadIdx.x * EPL;
+  asm volatile("" : "+v"(lb));
+#pragma unroll
+  for (int j = 0; j < Raw<T>::NL; ++j) {
+    const int off = lb + j * STEP;
+    if (VEC && off + EPL <= bn) {
+      r.q[j] = *reinterpret_cast<const uint4 *>(base + off);
+    } else {
+      uint32_t w[4] = {0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};  // bf16 -inf pairs
+      if constexpr (EPL == 8) {
+        const uint16_t *b16 = reinterpret_cast<const uint16_t *>(base);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t h = off + e < bn ? (uint32_t)b16[off + e] : 0xFF80u;
+          w[e >> 1] = (e & 1) ? ((w[e >> 1] & 0xFFFFu) | (h << 16)) : ((w[e >> 1] & 0xFFFF0000u) | h);
+        }
+      } else {
+        const float *f = reinterpret_cast<const float *>(base);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = __float_as_uint(off + e < bn ? f[off + e] : -__builtin_huge_valf());
+      }
+      r.q[j] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
+// Opaque to the compiler: each pass unpacks the elements again (one ALU op each)
+// instead of keeping every unpacked value live across the passes.
+template <typename T>
+__device__ inline void fence_regs(Raw<T> &r) {
+#pragma unroll
+  for (int j = 0; j < Raw<T>::NL; ++j) asm volatile("" : "+v"(r.q[j].x), "+v"(r.q[j].y), "+v"(r.q[j].z), "+v"(r.q[j].w));
+}
+
+// element e of 16-byte load j (unpacked from the raw registers on each use)
+template <typename T>
+__device__ inline float elem(const Raw<T> &r, int j, int e) {
+  const uint4 q = r.q[j];
+  if constexpr (Elem<T>::EPL == 8) {
+    const uint32_t wd = (e >> 1) == 0 ? q.x : (e >> 1) == 1 ? q.y : (e >> 1) == 2 ? q.z : q.w;
+    return (e & 1) ? __uint_as_float(wd & 0xFFFF0000u) : __uint_as_float(wd << 16);
+  } else {
+    return __uint_as_float(e == 0 ? q.x : e == 1 ? q.y : e == 2 ? q.z : q.w);
+  }
+}
+
+// K1: exact top-M of one segment (g.chunk elements: one or more batches of
+// kScanChunk) of one row, plus the tail of the rest.  The segment's batches
+// stream through registers (the next batch loads while this one is processed)
+// against a running top-M list:
+//   first batch  the value threshold above, then a rank pass;
+//   later ones   only elements above the list's M-th value can enter (later
+//                elements lose ties on the index); they are ranked into the list
+//                and whatever drops out joins the tail.
+// The tail of the elements below the threshold is summed against `ref`, the
+// largest value seen so far (never below them, so nothing overflows).
+// Also clears `zero_n` ints at `zero_ptr` (barrier counters of the expansion
+// kernel that follows on the stream).
 template <typename T, bool VEC>
 __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     const T *__restrict__ logits, ScanGeom g, float c, uint64_t *__restrict__ ckeys,
     float2 *__restrict__ ctail, int32_t *__restrict__ cflag, int32_t *__restrict__ zero_ptr,
     int zero_n) {
   constexpr int EPL = Elem<T>::EPL;
-  constexpr int NL = kScanPerThread / EPL;  // 16-byte loads per thread
-  constexpr int STEP = kScanThreads * EPL;  // elements per load round
+  constexpr int NL = Raw<T>::NL;
+  constexpr int STEP = kScanThreads * EPL;
   constexpr float NINF = -__builtin_huge_valf();
   __shared__ ScanLDS sh;
-  __shared__ uint64_t list[kMaxM];
-  __shared__ float wthr[kWaves];
+  __shared__ uint64_t list[2][kMaxM];
+  __shared__ float wthr[kWaves], wmax[kWaves];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int row = blockIdx.y, chunk = blockIdx.x;
-  const int start = chunk * g.chunk;
-  const int n = min(g.chunk, g.V - start);
-  const T *base = logits + (size_t)row * g.V + start;
+  const int row = blockIdx.y, seg = blockIdx.x;
+  const int M = g.M;
+  const int seg_start = seg * g.chunk;
+  const int seg_n = min(g.chunk, g.V - seg_start);
+  const int nbat = (seg_n + kScanChunk - 1) / kScanChunk;
+  const T *rowp = logits + (size_t)row * g.V + seg_start;
   if (zero_ptr && blockIdx.x == 0 && blockIdx.y == 0)
     for (int i = tid; i < zero_n; i += kScanThreads) zero_ptr[i] = 0;
 
-  // 1. the whole chunk into registers: element (j, e) of this thread has
-  //    chunk offset j*STEP + tid*EPL + e; slots past the end hold -inf
-  float v[NL][EPL];
+  Raw<T> ra, rb;
+  load_batch<T, VEC>(ra, rowp, min(kScanChunk, seg_n));
+  if (tid == 0) sh.flag = 0;
+  for (int i = tid; i < M; i += kScanThreads) list[0][i] = 0ull;
+
+  int cur = 0, nl = 0;    // running list: list[cur][0..nl), sorted descending
+  float thr = NINF;       // after the first merge: only values above thr can enter
+  int wbase = 0;          // candidates of this wave since the last merge
+  Tail tail = sel::tail_empty();
+
+  // Merge the candidates in the regions (wc[r] keys each, all >= the list's
+  // threshold) into the running list; the keys that drop out join the tail.
+  auto merge_regions = [&](const int (&wc)[kWaves]) {
+    int nc = 0;
 #pragma unroll
-  for (int j = 0; j < NL; ++j) {
-    const int off = j * STEP + tid * EPL;
-    if (VEC && off + EPL <= n) {
-      if constexpr (EPL == 8) {
-        const uint4 r = *reinterpret_cast<const uint4 *>(base + off);
-        const uint32_t w4[4] = {r.x, r.y, r.z, r.w};
+    for (int i = 0; i < kWaves; ++i) nc += wc[i];
+    if (nc == 0) return;
+    const uint64_t *L0 = list[cur];
+    uint64_t *L1 = list[cur ^ 1];
+    if (nc + nl <= 4 * kScanThreads) {
+      // a candidate's rank is the number of larger candidates (paired reads
+      // over the regions) plus the number of larger list keys (binary search);
+      // a list key's rank is its position plus the number of larger candidates
+      for (int it = tid; it < nc + nl; it += kScanThreads) {
+        uint64_t k;
+        int rank;
+        if (it < nc) {
+          int r = 0, o = it;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          v[j][2 * q] = __uint_as_float(w4[q] << 16);
-          v[j][2 * q + 1] = __uint_as_float(w4[q] & 0xFFFF0000u);
+          for (int i = 0; i < kWaves - 1; ++i)
+            if (r == i && o >= wc[i]) {
+              o -= wc[i];
+              r = i + 1;
+            }
+          k = sh.buf[r * kRegion + o];
+          int lo = 0, hi = nl;
+          while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (L0[mid] > k)
+              lo = mid + 1;
+            else
+              hi = mid;
+          }
+          rank = lo;
+        } else {
+          rank = it - nc;
+          k = L0[rank];
         }
-      } else {
-        const float4 r = *reinterpret_cast<const float4 *>(base + off);
-        v[j][0] = r.x;
-        v[j][1] = r.y;
-        v[j][2] = r.z;
-        v[j][3] = r.w;
+#pragma unroll
+        for (int r2 = 0; r2 < kWaves; ++r2) {
+          const ulonglong2 *p2 = reinterpret_cast<const ulonglong2 *>(sh.buf + r2 * kRegion);
+          const int np = (wc[r2] + 1) >> 1;
+#pragma unroll 4
+          for (int i = 0; i < np; ++i) {
+            const ulonglong2 kk = p2[i];
+            rank += (kk.x > k) + (kk.y > k);
+          }
+        }
+        if (rank < M)
+          L1[rank] = k;
+        else
+          sel::tail_add1(tail, key_value(k), c);
       }
     } else {
+      // many candidates: clear the unused part of every region, put the list
+      // keys into the free slots (the regions never fill past kRegionCap, so
+      // they fit), sort everything
+      for (int r = 0; r < kWaves; ++r)
+        for (int i = wc[r] + tid; i < kRegion; i += kScanThreads) sh.buf[r * kRegion + i] = 0ull;
+      __syncthreads();
+      for (int i = tid; i < nl; i += kScanThreads) {
+        int r = 0, o = i;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) v[j][e] = (off + e < n) ? to_f32<T>(base[off + e]) : NINF;
-    }
-  }
-  if (tid == 0) {
-    sh.nbuf = 0;
-    sh.nlist = 0;
-    sh.flag = 0;
-  }
-  // 2. NaN / +inf flag the row and leave the arithmetic as -inf; thread max
-  int bad = 0;
-  float tmax = NINF;
-#pragma unroll
-  for (int j = 0; j < NL; ++j)
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) {
-      if (nonfinite(v[j][e])) {
-        bad = 1;
-        v[j][e] = NINF;
+        for (int x = 0; x < kWaves - 1; ++x)
+          if (r == x && o >= kRegion - wc[x]) {
+            o -= kRegion - wc[x];
+            r = x + 1;
+          }
+        sh.buf[r * kRegion + wc[r] + o] = L0[i];
       }
-      tmax = fmaxf(tmax, v[j][e]);
+      __syncthreads();
+      sel::block_sort_desc<kScanThreads>(sh.buf, kScanSortCap);
+      const int tot = nc + nl;
+      for (int i = M + tid; i < tot; i += kScanThreads) sel::tail_add1(tail, key_value(sh.buf[i]), c);
+      for (int i = tid; i < M; i += kScanThreads) L1[i] = i < tot ? sh.buf[i] : 0ull;
     }
-  // 3. value threshold: every wave has >= ceil(M/4) lanes whose max is at least
-  //    its ceil(M/4)-th largest lane max, so at least M elements of the chunk
-  //    are >= the minimum over the waves: no top-M element lies below it
-  {
-    const float srt = wave_sort_desc_f(tmax);
-    const int q = (g.M + kWaves - 1) / kWaves;  // <= 64 since M <= 256
-    const float tq = __shfl(srt, q - 1);
-    if (lane == 0) wthr[w] = tq;
-  }
-  __syncthreads();
-  float thr = wthr[0];
-  for (int i = 1; i < kWaves; ++i) thr = fminf(thr, wthr[i]);
-  // 4. count survivors (v >= thr); the others go into this thread's tail, with
-  //    the thread max as reference
-  Tail tail;
-  tail.m = fmaxf(tmax, -3.402823466e38f);
-  float s = 0.0f;
-  int cnt = 0;
-#pragma unroll
-  for (int j = 0; j < NL; ++j)
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) {
-      const int off = j * STEP + tid * EPL + e;
-      const bool in = off < n;
-      const bool pass = in && v[j][e] >= thr;
-      cnt += pass;
-      const float ex = exp2f((v[j][e] - tail.m) * c);
-      s += (in && !pass) ? ex : 0.0f;
+    __syncthreads();
+    cur ^= 1;
+    nl = nc + nl < M ? nc + nl : M;
+  };
+
+  // after a merge: the threshold and the tail reference follow the list
+  auto after_merge = [&]() {
+    if (nl == M) thr = fmaxf(thr, key_value(list[cur][M - 1]));
+    const float top = nl ? key_value(list[cur][0]) : NINF;
+    if (top > tail.m) {
+      tail.s *= sel::fast_exp2((tail.m - top) * c);
+      tail.m = top;
     }
-  tail.s = s;
-  if (bad) atomicOr(&sh.flag, 1);
-  // 5. survivor slots: wave prefix of the per-thread counts, one LDS atomic per wave
-  const int incl = wave_incl_scan(cnt);
-  int wbase = 0;
-  if (lane == 63 && incl) wbase = atomicAdd(&sh.nbuf, incl);
-  wbase = __shfl(wbase, 63);
-  __syncthreads();
-  const int nsurv = sh.nbuf;
-  const int M = g.M;
-  if (nsurv <= kScanSortCap) {
-    int pos = wbase + incl - cnt;
-    if (cnt) {
+    wbase = 0;
+  };
+
+  // one batch: b = batch index in the segment, raw = its registers.  The
+  // candidates accumulate in the regions and are merged after batches 1, 2,
+  // 4, 8 and the last one, each merge raising the threshold.
+  auto process = [&](Raw<T> &raw, int b) {
+    const int bstart = b * kScanChunk;
+    const int bn = min(kScanChunk, seg_n - bstart);
+    const bool first = b == 0;
+    // this thread's first element offset, opaque so that the per-element
+    // offsets are formed at each use rather than hoisted (40 registers)
+    int lb = tid * EPL;
+    asm volatile("" : "+v"(lb));
+    if (first) {
+      // every wave has >= q = ceil(M/4) lanes whose max is at least its q-th
+      // largest lane max, so at least M elements of the batch are >= the
+      // minimum over the waves: no top-M element lies below it.  The q-th
+      // largest is found bit by bit on order-preserving codes, one ballot per bit.
+      float tmax = NINF;
+#pragma unroll
+      for (int j = 0; j < NL; ++j)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) tmax = fmaxf(tmax, elem<T>(raw, j, e));
+      const int q = (M + kWaves - 1) / kWaves;  // <= 64 since M <= 256
+      const uint32_t code = ordered_bits(tmax);
+      uint32_t pre = 0;
+#pragma unroll
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cand = pre | (1u << bit);
+        if (__popcll(__ballot(code >= cand)) >= q) pre = cand;
+      }
+      const float wm = sel::wave_reduce(tmax, [](float x, float y) { return fmaxf(x, y); });
+      if (lane == 0) {
+        wthr[w] = ordered_to_float(pre);
+        wmax[w] = wm;
+      }
+      __syncthreads();
+      thr = wthr[0];
+      float mx = wmax[0];
+#pragma unroll
+      for (int i = 1; i < kWaves; ++i) {
+        thr = fminf(thr, wthr[i]);
+        mx = fmaxf(mx, wmax[i]);
+      }
+      tail.m = fmaxf(mx, -3.402823466e38f);
+    }
+    const float tb = thr;  // this batch's threshold
+    // candidate test: the first batch keeps ties with its lower bound; later
+    // elements must beat the list's M-th value (they lose ties on the index)
+    auto is_cand = [&](float x, int off) { return first ? (off < bn && x >= tb) : (x > tb); };
+    // tail of the elements that cannot enter (against tail.m, which is >= all
+    // of them) and the count of the others, branch-free over the registers
+    fence_regs<T>(raw);
+    int cnt = 0;
+    {
+      float s = 0.0f;
 #pragma unroll
       for (int j = 0; j < NL; ++j)
 #pragma unroll
         for (int e = 0; e < EPL; ++e) {
-          const int off = j * STEP + tid * EPL + e;
-          if (off < n && v[j][e] >= thr) sh.buf[pos++] = make_key(v[j][e], (uint32_t)(start + off));
+          const float x = elem<T>(raw, j, e);
+          const bool pass = is_cand(x, lb + j * STEP + e);
+          const float ex = sel::fast_exp2((x - tail.m) * c);  // 0 for padding (-inf)
+          s += pass ? 0.0f : ex;
+          cnt += pass;
+        }
+      tail.s += s;
+    }
+    // candidates appended to this wave's region in (lane, element) order
+    uint64_t *region = sh.buf + w * kRegion;
+    const int incl = wave_incl_scan(cnt);
+    const int wn = __builtin_amdgcn_readlane(incl, 63);
+    fence_regs<T>(raw);
+    if (cnt) {
+      int pos = wbase + incl - cnt;
+#pragma unroll
+      for (int j = 0; j < NL; ++j)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          const int off = lb + j * STEP + e;
+          const float x = elem<T>(raw, j, e);
+          if (is_cand(x, off)) {
+            if (pos < kRegionCap) region[pos] = make_key(x, (uint32_t)(seg_start + bstart + off));
+            ++pos;
+          }
         }
     }
-    __syncthreads();
-    if (nsurv <= 2 * kScanThreads) {
-      // 6a. rank sort: each survivor's rank is the number of larger keys
-      for (int i = tid; i < M; i += kScanThreads) list[i] = 0ull;
-      __syncthreads();
-      for (int i = tid; i < nsurv; i += kScanThreads) {
-        const uint64_t k = sh.buf[i];
-        int rank = 0;
-        for (int q = 0; q < nsurv; ++q) rank += sh.buf[q] > k;
-        if (rank < M)
-          list[rank] = k;
-        else
-          sel::tail_add1(tail, key_value(k), c);
-      }
-      if (tid == 0) sh.nlist = nsurv < M ? nsurv : M;
-      __syncthreads();
-    } else {
-      // 6b. bitonic sort of the survivors
-      const int P = sel::pow2_at_least(nsurv, 64);
-      for (int i = nsurv + tid; i < P; i += kScanThreads) sh.buf[i] = 0;
-      __syncthreads();
-      sel::block_sort_desc<kScanThreads>(sh.buf, P);
-      for (int i = M + tid; i < nsurv; i += kScanThreads) sel::tail_add1(tail, key_value(sh.buf[i]), c);
-      for (int i = tid; i < M; i += kScanThreads) list[i] = i < nsurv ? sh.buf[i] : 0ull;
-      if (tid == 0) sh.nlist = nsurv < M ? nsurv : M;
-      __syncthreads();
+    const int wprev = wbase;
+    wbase += wn;
+    if (lane == 0) {
+      sh.wcnt[w] = wbase;
+      sh.wprev[w] = wprev;
+      if ((wbase & 1) && wbase < kRegionCap) region[wbase] = 0ull;  // pad for paired reads
     }
-  } else {
-    // 6c. fallback (adversarial rows): stream the survivors through the
-    //     bounded selector, starting from the value threshold
     __syncthreads();
+    int wc[kWaves], wp[kWaves];
+    bool overflow = false;
+#pragma unroll
+    for (int i = 0; i < kWaves; ++i) {
+      wc[i] = sh.wcnt[i];
+      wp[i] = sh.wprev[i];
+      overflow |= wc[i] > kRegionCap;
+    }
+    if (!overflow) {
+      if (((b + 1) & b) == 0 || b == nbat - 1) {
+        merge_regions(wc);
+        after_merge();
+      }
+      return;
+    }
+    // a region overflowed (adversarial rows): merge what the earlier batches
+    // left, then stream this batch's candidates through the bounded selector,
+    // starting from the list
+    merge_regions(wp);
+    after_merge();
+    const uint64_t *L0 = list[cur];
+    uint64_t *L1 = list[cur ^ 1];
+    for (int i = tid; i < nl; i += kScanThreads) sh.buf[i] = L0[i];
     if (tid == 0) {
-      sh.nbuf = 0;
-      sh.nlist = 0;
-      sh.thr = 1;
+      sh.nbuf = nl;
+      sh.nlist = nl;
+      sh.thr = nl == M ? L0[M - 1] + 1 : 1ull;
     }
     __syncthreads();
 #pragma unroll
@@ -310,20 +463,42 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
       float val[EPL];
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
-        const int off = j * STEP + tid * EPL + e;
-        key[e] = (off < n && v[j][e] >= thr) ? make_key(v[j][e], (uint32_t)(start + off)) : 0ull;
-        val[e] = v[j][e];
+        const int off = lb + j * STEP + e;
+        const float x = elem<T>(raw, j, e);
+        const bool pass = is_cand(x, off);
+        key[e] = pass ? make_key(x, (uint32_t)(seg_start + bstart + off)) : 0ull;
+        val[e] = pass ? x : NINF;  // the non-candidates are already in the tail
       }
       stream_batch<EPL>(sh, key, val, M, tail, c);
     }
     if (sh.nbuf > sh.nlist) flush(sh, M, tail, c);
-    for (int i = tid; i < M; i += kScanThreads) list[i] = i < sh.nlist ? sh.buf[i] : 0ull;
+    const int nn = sh.nlist;
+    for (int i = tid; i < M; i += kScanThreads) L1[i] = i < nn ? sh.buf[i] : 0ull;
     __syncthreads();
+    cur ^= 1;
+    nl = nn;
+    after_merge();
+  };
+
+  for (int b = 0; b < nbat; b += 2) {
+    if (b + 1 < nbat)
+      load_batch<T, VEC>(rb, rowp + (size_t)(b + 1) * kScanChunk, min(kScanChunk, seg_n - (b + 1) * kScanChunk));
+    process(ra, b);
+    if (b + 1 < nbat) {
+      if (b + 2 < nbat)
+        load_batch<T, VEC>(ra, rowp + (size_t)(b + 2) * kScanChunk,
+                           min(kScanChunk, seg_n - (b + 2) * kScanChunk));
+      process(rb, b + 1);
+    }
   }
+
+  // a NaN makes a tail sum NaN (it never passes a comparison); +inf heads the list
+  if (!(tail.s == tail.s) || (nl && key_value(list[cur][0]) == __builtin_huge_valf()))
+    atomicOr(&sh.flag, 1);
   const Tail t = sel::block_tail<kScanThreads>(tail, c, sh.red);
-  const size_t cidx = (size_t)row * g.nchunks + chunk;
+  const size_t cidx = (size_t)row * g.nchunks + seg;
   uint64_t *out = ckeys + cidx * M;
-  for (int i = tid; i < M; i += kScanThreads) out[i] = list[i];
+  for (int i = tid; i < M; i += kScanThreads) out[i] = i < nl ? list[cur][i] : 0ull;
   if (tid == 0) {
     ctail[cidx] = make_float2(t.m, t.s);
     cflag[cidx] = sh.flag ? DT_TREE_NONFINITE : 0;
@@ -353,8 +528,15 @@ ScanGeom scan_geom(int rows, int V, int M) {
   g.rows = rows;
   g.V = V;
   g.M = M;
-  g.chunk = kScanChunk;
-  g.nchunks = (V + kScanChunk - 1) / kScanChunk;
+  // segments of sb batches: enough workgroups to fill the device about four
+  // deep, the rest of the work amortised inside each segment
+  const int nb = (V + kScanChunk - 1) / kScanChunk;
+  long long total = (long long)rows * nb;
+  int sb = (int)((total + kScanTargetGroups - 1) / kScanTargetGroups);
+  sb = sb < 1 ? 1 : (sb > kScanMaxBatches ? kScanMaxBatches : sb);
+  if (sb > nb) sb = nb;
+  g.chunk = sb * kScanChunk;
+  g.nchunks = (V + g.chunk - 1) / g.chunk;
   return g;
 }
 

@@ -16,14 +16,18 @@ struct Tail {
 
 __device__ inline Tail tail_empty() { return Tail{-3.402823466e38f, 0.0f}; }
 
+// 2^x on the hardware unit (v_exp_f32): results below 2^-126 flush to zero,
+// which a sum of exponentials relative to its running max can ignore
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 template <int N>
 __device__ inline void tail_add_group(Tail &t, const float (&x)[N], float c) {
   float mx = t.m;
 #pragma unroll
   for (int j = 0; j < N; ++j) mx = fmaxf(mx, x[j]);
-  float s = t.s * exp2f((t.m - mx) * c);
+  float s = t.s * fast_exp2((t.m - mx) * c);
 #pragma unroll
-  for (int j = 0; j < N; ++j) s += exp2f((x[j] - mx) * c);
+  for (int j = 0; j < N; ++j) s += fast_exp2((x[j] - mx) * c);
   t.m = mx;
   t.s = s;
 }
@@ -36,27 +40,47 @@ __device__ inline void tail_add1(Tail &t, float x, float c) {
 __device__ inline Tail tail_merge(Tail a, Tail b, float c) {
   Tail r;
   r.m = fmaxf(a.m, b.m);
-  r.s = a.s * exp2f((a.m - r.m) * c) + b.s * exp2f((b.m - r.m) * c);
+  r.s = a.s * fast_exp2((a.m - r.m) * c) + b.s * fast_exp2((b.m - r.m) * c);
   return r;
 }
 
+// Wave-wide reductions with DPP inside each row of 16 lanes (quad swaps, half
+// mirror, mirror) and four lane reads across rows; every lane gets the same
+// value.  The whole wave must be active.
+__device__ inline float readlane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xF, 0xF, false));
+}
+template <typename Op>
+__device__ inline float wave_reduce(float v, Op op) {
+  v = op(v, dpp_f<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = op(v, dpp_f<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = op(v, dpp_f<0x141>(v));  // row_half_mirror
+  v = op(v, dpp_f<0x140>(v));  // row_mirror
+  return op(op(readlane_f(v, 0), readlane_f(v, 16)), op(readlane_f(v, 32), readlane_f(v, 48)));
+}
 // block-wide tail reduction in a fixed order (deterministic); red: NT/64 float2
 template <int NT>
 __device__ inline Tail block_tail(Tail t, float c, float2 *red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    Tail u;
-    u.m = __shfl_xor(t.m, o);
-    u.s = __shfl_xor(t.s, o);
-    t = tail_merge(t, u, c);
-  }
-  if (lane == 0) red[w] = make_float2(t.m, t.s);
+  t = tail_merge(t, Tail{dpp_f<0xB1>(t.m), dpp_f<0xB1>(t.s)}, c);
+  t = tail_merge(t, Tail{dpp_f<0x4E>(t.m), dpp_f<0x4E>(t.s)}, c);
+  t = tail_merge(t, Tail{dpp_f<0x141>(t.m), dpp_f<0x141>(t.s)}, c);
+  t = tail_merge(t, Tail{dpp_f<0x140>(t.m), dpp_f<0x140>(t.s)}, c);
+  Tail r{readlane_f(t.m, 0), readlane_f(t.s, 0)};
+  r = tail_merge(r, Tail{readlane_f(t.m, 16), readlane_f(t.s, 16)}, c);
+  r = tail_merge(r, Tail{readlane_f(t.m, 32), readlane_f(t.s, 32)}, c);
+  r = tail_merge(r, Tail{readlane_f(t.m, 48), readlane_f(t.s, 48)}, c);
+  if (lane == 0) red[w] = make_float2(r.m, r.s);
   __syncthreads();
-  Tail r{red[0].x, red[0].y};
-  for (int i = 1; i < NT / 64; ++i) r = tail_merge(r, Tail{red[i].x, red[i].y}, c);
+  Tail b{red[0].x, red[0].y};
+  for (int i = 1; i < NT / 64; ++i) b = tail_merge(b, Tail{red[i].x, red[i].y}, c);
   __syncthreads();
-  return r;
+  return b;
 }
 
 // descending bitonic sort of a wave's 64 values (one per lane)

@@ -97,3 +97,33 @@ def test_scan_nonfinite_flags():
     x[1, 17] = np.nan
     x[2, 2999] = np.inf
     _check(x, synth.DT_F32, 8, 0.0, case="nonfinite")
+
+
+def _mixed_rows(n_rows, V, seed):
+    """Rows of several kinds: normal, integer ties, rising and falling ramps,
+    constant, -inf blocks, a late spike."""
+    rng = np.random.default_rng(seed)
+    x = (rng.standard_normal((n_rows, V)) * 2).astype(np.float32)
+    kinds = np.arange(n_rows) % 7
+    ramp = np.arange(V, dtype=np.float32) / 64.0
+    x[kinds == 1] = np.round(x[kinds == 1] * 2)
+    x[kinds == 2] = ramp
+    x[kinds == 3] = ramp[::-1]
+    x[kinds == 4] = 0.5
+    blk = np.flatnonzero(kinds == 5)
+    x[blk, : V // 3] = -np.inf
+    late = np.flatnonzero(kinds == 6)
+    x[late, V - 5] = 40.0
+    return x
+
+
+@pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16])
+def test_scan_streaming_segments(dtype):
+    # enough rows that every workgroup streams several batches of a segment
+    # against its running list (ramps overflow the candidate regions)
+    x = _mixed_rows(1100, 20480 + 37, 21)
+    if dtype == synth.DT_BF16:
+        x = synth.f32_to_bf16_bits(x)
+    rows = list(range(0, 14)) + list(range(500, 507)) + [1099]
+    _check(x, dtype, 64, 0.8, rows=rows, case=f"streaming {dtype}")
+    _check(x, dtype, 200, 0.0, rows=rows[:7], case=f"streaming M=200 {dtype}")
