@@ -148,9 +148,14 @@ class Tree:
                     torch.empty(batch, **i32), torch.empty(batch, **i32))
 
     def as_c(self) -> dt_tree:
-        return dt_tree(*(x.data_ptr() for x in (self.tokens, self.parents, self.depth,
-                                                   self.position_ids, self.mask, self.scores,
-                                                   self.n_nodes, self.status)))
+        """The dt_tree view of these tensors (built once; the tensors never move)."""
+        c = self.__dict__.get("_c")
+        if c is None:
+            c = dt_tree(*(x.data_ptr() for x in (self.tokens, self.parents, self.depth,
+                                                    self.position_ids, self.mask, self.scores,
+                                                    self.n_nodes, self.status)))
+            self.__dict__["_c"] = c
+        return c
 
 
 class Plan:
@@ -200,10 +205,11 @@ class Plan:
         if out is None:
             out = Tree.empty(batch, self.B, logits.device)
         ws = self.workspace(batch) if workspace is None else workspace
-        c = out.as_c()
-        _check(self._lib.dt_build_tree(self.handle, _ptr(logits), batch, _ptr(h0),
-                                       ctypes.c_float(T), _ptr(ws), ws.numel(), ctypes.byref(c),
-                                       _stream(stream)))
+        st = self._lib.dt_build_tree(self.handle, logits.data_ptr(), batch,
+                                     None if h0 is None else h0.data_ptr(), T, ws.data_ptr(),
+                                     ws.numel(), ctypes.byref(out.as_c()), _stream(stream))
+        if st != 0:
+            _check(st)
         return out
 
     def set_profiling(self, enable: bool) -> None:

@@ -37,8 +37,10 @@ constexpr int kRegionCap = kRegion - kMaxM / kWaves;  // fill limit: the list fi
 struct ScanLDS {
   alignas(16) uint64_t buf[kScanSortCap];
   float2 red[kWaves];
-  int wcnt[kWaves];
-  int wprev[kWaves];
+  // per-wave candidate counts, by batch parity: a wave can start the next batch
+  // (and write its counts) while another still reads this batch's
+  int wcnt[2][kWaves];
+  int wprev[2][kWaves];
   int nbuf;
   int nlist;
   int flag;
@@ -179,6 +181,34 @@ __device__ inline void load_batch(Raw<T> &r, const T *base, int bn) {
   }
 }
 
+// 16-byte-aligned rows: straight-line buffer loads of batch `b` of a segment
+// (seg_bytes of data from `seg`); loads past the segment's end return zeros
+// (each 16-byte load lies wholly inside or outside it) and are made -inf by
+// pad_batch.  Nothing waits for the data here.
+template <typename T>
+__device__ inline void load_batch_vec(Raw<T> &r, __amdgpu_buffer_rsrc_t seg, int b) {
+  constexpr int EPL = Elem<T>::EPL;
+  constexpr int STEP = kScanThreads * EPL;
+  int lb = (int)threadIdx.x * EPL;
+  asm volatile("" : "+v"(lb));
+  const int base = (b * kScanChunk + lb) * (int)sizeof(T);
+#pragma unroll
+  for (int j = 0; j < Raw<T>::NL; ++j)
+    r.q[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           seg, base + j * STEP * (int)sizeof(T), 0, 0));
+}
+
+// the elements of a partial batch past its end become -inf
+template <typename T>
+__device__ inline void pad_batch(Raw<T> &r, int bn) {
+  constexpr int EPL = Elem<T>::EPL;
+  constexpr int STEP = kScanThreads * EPL;
+  const uint32_t ninf = EPL == 8 ? 0xFF80FF80u : 0xFF800000u;
+#pragma unroll
+  for (int j = 0; j < Raw<T>::NL; ++j)
+    if ((int)threadIdx.x * EPL + j * STEP >= bn) r.q[j] = make_uint4(ninf, ninf, ninf, ninf);
+}
+
 // Opaque to the compiler: each pass unpacks the elements again (one ALU op each)
 // instead of keeping every unpacked value live across the passes.
 template <typename T>
@@ -234,7 +264,15 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     for (int i = tid; i < zero_n; i += kScanThreads) zero_ptr[i] = 0;
 
   Raw<T> ra, rb;
-  load_batch<T, VEC>(ra, rowp, min(kScanChunk, seg_n));
+  const __amdgpu_buffer_rsrc_t segr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T *>(rowp), 0, seg_n * (int)sizeof(T), 0x00020000);
+  auto load = [&](Raw<T> &r, int b) {
+    if constexpr (VEC)
+      load_batch_vec<T>(r, segr, b);
+    else
+      load_batch<T, false>(r, rowp + (size_t)b * kScanChunk, min(kScanChunk, seg_n - b * kScanChunk));
+  };
+  load(ra, 0);
   if (tid == 0) sh.flag = 0;
   for (int i = tid; i < M; i += kScanThreads) list[0][i] = 0ull;
 
@@ -250,6 +288,25 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) nc += wc[i];
     if (nc == 0) return;
+    // the regions hold segment offsets: read the values back, form the keys
+    for (int it = tid; it < nc; it += kScanThreads) {
+      int r = 0, o = it;
+#pragma unroll
+      for (int i = 0; i < kWaves - 1; ++i)
+        if (r == i && o >= wc[i]) {
+          o -= wc[i];
+          r = i + 1;
+        }
+      const uint32_t off = (uint32_t)sh.buf[r * kRegion + o];
+      // (an offset is always inside the segment; the guard keeps a wrong one
+      // from reading outside it)
+      sh.buf[r * kRegion + o] =
+          off < (uint32_t)seg_n ? make_key(to_f32<T>(rowp[off]), (uint32_t)seg_start + off) : 0ull;
+    }
+#pragma unroll
+    for (int i = 0; i < kWaves; ++i)
+      if (tid == i && (wc[i] & 1)) sh.buf[i * kRegion + wc[i]] = 0ull;  // pad for paired reads
+    __syncthreads();
     const uint64_t *L0 = list[cur];
     uint64_t *L1 = list[cur ^ 1];
     if (nc + nl <= 4 * kScanThreads) {
@@ -336,12 +393,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
   };
 
   // one batch: b = batch index in the segment, raw = its registers.  The
-  // candidates accumulate in the regions and are merged after batches 1, 2,
-  // 4, 8 and the last one, each merge raising the threshold.
+  // candidates accumulate in the regions; they are merged after the first
+  // batch (which sets the threshold), once about 2M have gathered (each merge
+  // raises the threshold), and at the end.
   auto process = [&](Raw<T> &raw, int b) {
     const int bstart = b * kScanChunk;
     const int bn = min(kScanChunk, seg_n - bstart);
     const bool first = b == 0;
+    if (VEC && bn < kScanChunk) pad_batch<T>(raw, bn);
     // this thread's first element offset, opaque so that the per-element
     // offsets are formed at each use rather than hoisted (40 registers)
     int lb = tid * EPL;
@@ -379,65 +438,103 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
       }
       tail.m = fmaxf(mx, -3.402823466e38f);
     }
-    const float tb = thr;  // this batch's threshold
-    // candidate test: the first batch keeps ties with its lower bound; later
-    // elements must beat the list's M-th value (they lose ties on the index)
-    auto is_cand = [&](float x, int off) { return first ? (off < bn && x >= tb) : (x > tb); };
-    // tail of the elements that cannot enter (against tail.m, which is >= all
+    // Candidate test: the first batch keeps ties with its lower bound; later
+    // elements must beat the list's M-th value (they lose ties on the index).
+    // With a lower bound of -inf (fewer than M finite elements) the first
+    // batch keeps everything in range.
+    const float tb = thr;
+    const bool all_in = first && !(tb > NINF);
+      // tail of the elements that cannot enter (against tail.m, which is >= all
     // of them) and the count of the others, branch-free over the registers
     fence_regs<T>(raw);
-    int cnt = 0;
-    {
+    // candidate flags, shifted in element by element: element k = j*EPL + e
+    // sits at bit 31 - k of lo (k < 32) or bit NE - 1 - k of hi (k >= 32)
+    constexpr int NE = NL * EPL;
+    static_assert(NE > 32 && NE <= 64, "flag words");
+    uint32_t lo = 0, hi = 0;
+    auto tail_pass = [&](auto cand) {
       float s = 0.0f;
+      const float m = tail.m;
 #pragma unroll
       for (int j = 0; j < NL; ++j)
 #pragma unroll
         for (int e = 0; e < EPL; ++e) {
           const float x = elem<T>(raw, j, e);
-          const bool pass = is_cand(x, lb + j * STEP + e);
-          const float ex = sel::fast_exp2((x - tail.m) * c);  // 0 for padding (-inf)
-          s += pass ? 0.0f : ex;
-          cnt += pass;
+          const bool pass = cand(x);
+          s += sel::fast_exp2(pass ? NINF : (x - m) * c);  // 0 for candidates and padding
+          if (j * EPL + e < 32)
+            lo = (lo << 1) | (uint32_t)pass;
+          else
+            hi = (hi << 1) | (uint32_t)pass;
         }
       tail.s += s;
+    };
+    // one comparison x > te: te = tb for later batches; for the first batch
+    // any value below tb does (a few extra candidates are ranked exactly)
+    const float te = first && tb > NINF ? tb - (fabsf(tb) * 0x1p-20f + 0x1p-126f) : tb;
+    tail_pass([=](float x) { return x > te; });
+    // the same candidate set, element by element (used by the fallback below)
+    auto is_cand = [&](float x, int off) { return x > te || (all_in && off < bn && x == NINF); };
+    if (all_in) {
+      // a lower bound of -inf: the -inf elements in range are candidates too
+      // (read again from memory; the tail pass gave them nothing)
+#pragma unroll 1
+      for (int k = 0; k < NE; ++k) {
+        const int off = lb + (k / EPL) * STEP + k % EPL;
+        if (off < bn && to_f32<T>(rowp[bstart + off]) == NINF) {
+          if (k < 32)
+            lo |= 1u << (31 - k);
+          else
+            hi |= 1u << (NE - 1 - k);
+        }
+      }
     }
-    // candidates appended to this wave's region in (lane, element) order
+    // candidates appended to this wave's region in (lane, element) order, as
+    // segment offsets (their keys are formed at the next merge)
+    const int cnt = __popc(lo) + __popc(hi);
     uint64_t *region = sh.buf + w * kRegion;
     const int incl = wave_incl_scan(cnt);
     const int wn = __builtin_amdgcn_readlane(incl, 63);
-    fence_regs<T>(raw);
-    if (cnt) {
+    {
       int pos = wbase + incl - cnt;
-#pragma unroll
-      for (int j = 0; j < NL; ++j)
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) {
-          const int off = lb + j * STEP + e;
-          const float x = elem<T>(raw, j, e);
-          if (is_cand(x, off)) {
-            if (pos < kRegionCap) region[pos] = make_key(x, (uint32_t)(seg_start + bstart + off));
-            ++pos;
-          }
-        }
+      auto put = [&](int k) {
+        if (pos < kRegionCap) region[pos] = (uint64_t)(uint32_t)(bstart + lb + (k / EPL) * STEP + k % EPL);
+        ++pos;
+      };
+      while (lo) {
+        const int bpos = 31 - __builtin_clz(lo);  // highest set bit: the lowest element
+        lo &= ~(1u << bpos);
+        put(31 - bpos);
+      }
+      while (hi) {
+        const int bpos = 31 - __builtin_clz(hi);
+        hi &= ~(1u << bpos);
+        put(NE - 1 - bpos);
+      }
     }
     const int wprev = wbase;
     wbase += wn;
+    const int par = b & 1;
     if (lane == 0) {
-      sh.wcnt[w] = wbase;
-      sh.wprev[w] = wprev;
-      if ((wbase & 1) && wbase < kRegionCap) region[wbase] = 0ull;  // pad for paired reads
+      sh.wcnt[par][w] = wbase;
+      sh.wprev[par][w] = wprev;
     }
     __syncthreads();
     int wc[kWaves], wp[kWaves];
-    bool overflow = false;
+    bool overflow = false, crowded = false;
+    int ncand = 0;
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) {
-      wc[i] = sh.wcnt[i];
-      wp[i] = sh.wprev[i];
+      wc[i] = sh.wcnt[par][i];
+      wp[i] = sh.wprev[par][i];
       overflow |= wc[i] > kRegionCap;
+      crowded |= wc[i] > kRegionCap / 2;
+      ncand += wc[i];
     }
     if (!overflow) {
-      if (((b + 1) & b) == 0 || b == nbat - 1) {
+      // a merge costs a fixed latency plus a term quadratic in the candidates:
+      // merge once about 2M have gathered
+      if (first || crowded || ncand >= 2 * M || b == nbat - 1) {
         merge_regions(wc);
         after_merge();
       }
@@ -457,14 +554,15 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
       sh.thr = nl == M ? L0[M - 1] + 1 : 1ull;
     }
     __syncthreads();
-#pragma unroll
+    // (the batch is read again from memory, one load group at a time)
+#pragma unroll 1
     for (int j = 0; j < NL; ++j) {
       uint64_t key[EPL];
       float val[EPL];
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         const int off = lb + j * STEP + e;
-        const float x = elem<T>(raw, j, e);
+        const float x = off < bn ? to_f32<T>(rowp[bstart + off]) : NINF;
         const bool pass = is_cand(x, off);
         key[e] = pass ? make_key(x, (uint32_t)(seg_start + bstart + off)) : 0ull;
         val[e] = pass ? x : NINF;  // the non-candidates are already in the tail
@@ -480,16 +578,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     after_merge();
   };
 
+  // the next batch is always in flight while one is processed; VEC loads past
+  // the segment's end return zeros and cost no memory traffic
   for (int b = 0; b < nbat; b += 2) {
-    if (b + 1 < nbat)
-      load_batch<T, VEC>(rb, rowp + (size_t)(b + 1) * kScanChunk, min(kScanChunk, seg_n - (b + 1) * kScanChunk));
+    if (VEC || b + 1 < nbat) load(rb, b + 1);
     process(ra, b);
-    if (b + 1 < nbat) {
-      if (b + 2 < nbat)
-        load_batch<T, VEC>(ra, rowp + (size_t)(b + 2) * kScanChunk,
-                           min(kScanChunk, seg_n - (b + 2) * kScanChunk));
-      process(rb, b + 1);
-    }
+    if (VEC || b + 2 < nbat) load(ra, b + 2);
+    if (b + 1 < nbat) process(rb, b + 1);
   }
 
   // a NaN makes a tail sum NaN (it never passes a comparison); +inf heads the list
