@@ -8,8 +8,9 @@ B=16, T=1, d_e=4096, d_h=512).  Logit buffers rotate through >= 512 MB so the
 256 MB Infinity Cache cannot serve the scan.
 
 Prints ONE JSON line: trees/s for the whole job, the per-kernel roofline of the
-dominant kernel (durations from HIP events recorded between the library's
-kernels on the launch stream) and the CPU oracle timed on a bounded sample.
+dominant kernel (mean durations over the timed calls, from HIP events the
+library records between its kernels on the launch stream) and the CPU oracle
+timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -26,6 +27,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILES = os.path.join(ROOT, "profiles")
+PROFILE_EVERY = 8   # stage events on every 8th timed call (each event costs a few us)
 
 
 def parse():
@@ -37,8 +39,6 @@ def parse():
                     choices=["tiny", "qwen3_4b", "qwen3_8b", "budget64", "concurrent"])
     ap.add_argument("--rotate-mb", type=float, default=512.0,
                     help="logit bytes cycled through in the timed loop")
-    ap.add_argument("--profile-steps", type=int, default=50,
-                    help="calls with stage events (per-kernel durations)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -57,21 +57,26 @@ def algorithmic(plan_cfg, stage):
     return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["M"] * c["d_h"]), "flops", "mfma"
 
 
+def source_digest(files):
+    """sha256 over the kernel sources a counter record was taken with."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        h.update(open(os.path.join(ROOT, "paper_2607_08642_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def traffic_from_profiles(workload, stage):
-    """HBM bytes per launch from committed PMC summaries, if they match the current kernel."""
+    """HBM bytes per launch from the committed PMC record, if it matches the current kernel."""
     path = os.path.join(PROFILES, "pmc_traffic.json")
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path)).get(workload, {}).get(stage)
-        if not rec:
-            return None
-        import hashlib
-        src = os.path.join(ROOT, "paper_2607_08642_amd", "csrc", rec["source"])
-        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["sha256"]:
-            return None          # the kernel changed since the counters were taken
+        rec = json.load(open(path))["records"].get(workload, {}).get(stage)
+        if not rec or source_digest(rec["sources"]) != rec["sha256"]:
+            return None          # no record, or the kernel changed since the counters were taken
         return rec["bytes_per_launch"]
-    except Exception:
+    except (OSError, KeyError, ValueError):
         return None
 
 
@@ -105,8 +110,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(trees shard across GPUs with no exchange; see the design notes).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(independent trees would shard across GPUs with no exchange).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -147,8 +152,10 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` calls, synchronised on both sides
+    # timed region: exactly `steps` calls, synchronised on both sides; the
+    # library records its stage events on the launch stream during these calls
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    plan.set_profiling(PROFILE_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -158,17 +165,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per_call = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]) * 1e3  # us
-
-    # per-kernel durations with stage events (same kernels, separate pass)
-    plan.set_profiling(True)
-    stages = {k: [] for k in binding.STAGES}
-    n_exp = []
-    for i in range(args.profile_steps):
-        step(i)
-        for k, v in plan.stage_ms().items():
-            stages[k].append(v * 1e3)
-    plan.set_profiling(False)
-    stage_us = {k: float(np.mean(v)) for k, v in stages.items()}
+    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled timed calls
+    plan.set_profiling(0)
 
     # expansions Alg. 1 performs: the root plus every popped node above depth L
     # (the kernel's extra speculative expansions are not counted as useful work)
@@ -215,6 +213,10 @@ def main():
         "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
                      "unit": runit, "frac": achieved / peak,
                      "traffic": traffic_from_profiles(wl.name, dom)},
+        "scan_roofline": {"kernel": "scan", "bound": "hbm",
+                          "achieved": scan_bytes / (scan_us * 1e-6) / 1e9, "peak": HBM_PEAK_GBS,
+                          "unit": "GB/s", "frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                          "traffic": traffic_from_profiles(wl.name, "scan")},
     }
 
     if args.copy_calibration:

@@ -171,13 +171,15 @@ dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, c
 /* Release the plan's device memory (NULL is ignored). */
 void dt_plan_destroy(dt_plan *plan);
 
-/* Stage timing (measurement aid).  When enabled, dt_build_tree records a HIP
- * event on its stream before its first kernel and after each kernel:
- * stage 0 = top-M scan of the logit chunks, 1 = per-row merge, expansion and
- * emission.  dt_plan_stage_ms waits for the last call's final event and writes
- * the 2 stage durations in milliseconds to ms[0..1].
- * Returns DT_ERR_SHAPE if no profiled call has been made yet. */
-dt_status dt_plan_set_profiling(dt_plan *plan, int enable);
+/* Stage timing (measurement aid).  With every = n > 0, every n-th dt_build_tree
+ * call (the first one included) records a HIP event on its stream before its
+ * first kernel and after each kernel: stage 0 = top-M scan of the logits
+ * (kernel 1), 1 = per-row merge, expansion and emission (kernel 2).  every = 0
+ * turns it off; enabling (again) starts a new count.
+ * dt_plan_stage_ms waits for the last profiled call and writes the mean stage
+ * durations in milliseconds over the profiled calls (the most recent 1024) to
+ * ms[0..1].  Returns DT_ERR_SHAPE if no profiled call has been made yet. */
+dt_status dt_plan_set_profiling(dt_plan *plan, int every);
 dt_status dt_plan_stage_ms(dt_plan *plan, float *ms);
 
 /* Workspace (bytes) for dt_scan_topm over `rows` rows. */

@@ -212,11 +212,12 @@ class Plan:
             _check(st)
         return out
 
-    def set_profiling(self, enable: bool) -> None:
-        _check(self._lib.dt_plan_set_profiling(self.handle, int(enable)))
+    def set_profiling(self, every: int) -> None:
+        """Record stage events on every `every`-th call (0 or False: off)."""
+        _check(self._lib.dt_plan_set_profiling(self.handle, int(every)))
 
     def stage_ms(self) -> dict:
-        """Durations (ms) of the last profiled call's kernels (waits for it)."""
+        """Mean kernel durations (ms) over the calls profiled since set_profiling(True)."""
         ms = (ctypes.c_float * 2)()
         _check(self._lib.dt_plan_stage_ms(self.handle, ms))
         return dict(zip(STAGES, list(ms)))

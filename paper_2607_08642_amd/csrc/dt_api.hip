@@ -181,31 +181,46 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
 
 dt_status dt_plan_set_profiling(dt_plan *p, int enable) {
   if (!p) return fail(DT_ERR_NULL, "plan is required");
-  if (enable && !p->ev[0]) {
-    for (int i = 0; i < 3; ++i) {
+  if (enable && !p->ev) {
+    p->ev = new (std::nothrow) hipEvent_t[3 * dt::kProfSlots]();
+    if (!p->ev) return fail(DT_ERR_HIP, "host allocation failed");
+    for (int i = 0; i < 3 * dt::kProfSlots; ++i) {
       hipError_t e = hipEventCreate(&p->ev[i]);
       if (e != hipSuccess) return hip_fail(e, "event create");
     }
   }
-  p->profiling = enable ? 1 : 0;
+  p->profiling = enable > 0 ? enable : 0;
   p->profiled_calls = 0;
+  p->calls_since = 0;
   return DT_OK;
 }
 
 dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
   if (!p || !ms) return fail(DT_ERR_NULL, "plan and ms are required");
-  if (!p->ev[0] || p->profiled_calls == 0)
+  if (!p->ev || p->profiled_calls == 0)
     return fail(DT_ERR_SHAPE, "no profiled dt_build_tree call yet");
-  hipError_t e = hipEventSynchronize(p->ev[2]);
-  for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipEventElapsedTime(&ms[i], p->ev[i], p->ev[i + 1]);
+  const int n = p->profiled_calls < dt::kProfSlots ? p->profiled_calls : dt::kProfSlots;
+  const int last = (p->profiled_calls - 1) % dt::kProfSlots;
+  hipError_t e = hipEventSynchronize(p->ev[3 * last + 2]);
+  double sum[2] = {0.0, 0.0};
+  for (int c = 0; c < n && e == hipSuccess; ++c)
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+      float t = 0.0f;
+      e = hipEventElapsedTime(&t, p->ev[3 * c + i], p->ev[3 * c + i + 1]);
+      sum[i] += t;
+    }
   if (e != hipSuccess) return hip_fail(e, "event timing");
+  for (int i = 0; i < 2; ++i) ms[i] = (float)(sum[i] / n);
   return DT_OK;
 }
 
 void dt_plan_destroy(dt_plan *p) {
   if (!p) return;
-  for (int i = 0; i < 3; ++i)
-    if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
+  if (p->ev) {
+    for (int i = 0; i < 3 * dt::kProfSlots; ++i)
+      if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
+    delete[] p->ev;
+  }
   if (p->wfold) (void)hipFree(p->wfold);
   if (p->b_ih) (void)hipFree(p->b_ih);
   if (p->b_hh) (void)hipFree(p->b_hh);
@@ -246,17 +261,19 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
   dt::Workspace ws = dt::carve(plan, batch, static_cast<char *>(workspace));
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
-  const bool prof = plan->profiling != 0;
-  hipError_t e = prof ? hipEventRecord(plan->ev[0], s) : hipSuccess;
+  // profiling every n-th call: the events' own cost (a few us each) stays small
+  const bool prof = plan->profiling > 0 && (plan->calls_since++ % plan->profiling) == 0;
+  hipEvent_t *ev = prof ? plan->ev + 3 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
+  hipError_t e = prof ? hipEventRecord(ev[0], s) : hipSuccess;
   // the scan kernel also clears the expansion kernel's barrier counters
   if (e == hipSuccess)
     e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, (batch + 2) * dt::kBarStride, s);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
-  if (prof) e = hipEventRecord(plan->ev[1], s);
+  if (prof) e = hipEventRecord(ev[1], s);
   if (e == hipSuccess) e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   if (prof) {
-    e = hipEventRecord(plan->ev[2], s);
+    e = hipEventRecord(ev[2], s);
     if (e != hipSuccess) return hip_fail(e, "event record");
     plan->profiled_calls++;
   }

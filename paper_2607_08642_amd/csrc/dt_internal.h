@@ -37,7 +37,8 @@ constexpr int kFoldBK = 64;
 constexpr int kExpThreads = 512;
 constexpr int kNodeCap = 1536;       // live nodes per tree kept in LDS
 constexpr int kChunkNodes = 16;      // nodes expanded together (shared weight pass)
-constexpr int kBarStride = 64;       // ints per tree of barrier counters (own cache lines)
+constexpr int kBarStride = 64;
+constexpr int kProfSlots = 1024;   // profiled calls kept for stage averages       // ints per tree of barrier counters (own cache lines)
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -93,9 +94,10 @@ struct dt_plan {
   int has_bc;
   void *whh_t;      // W_hh in MFMA A-fragment order (see pack_whh_*_kernel)
   int num_cus;
-  int profiling;            // record stage events in dt_build_tree
+  int profiling;            // > 0: record stage events on every profiling-th dt_build_tree call
+  int calls_since;          // dt_build_tree calls since profiling was enabled
   int profiled_calls;       // calls recorded since profiling was enabled
-  hipEvent_t ev[3];         // stage boundaries of the last profiled call
+  hipEvent_t *ev;           // [kProfSlots][3] stage boundaries, one slot per call (ring)
 };
 
 namespace dt {

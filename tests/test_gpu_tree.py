@@ -121,3 +121,24 @@ def test_qwen3_8b_paper_branching():
 
 def test_concurrent_workload_sampled():
     run_case(qwen("concurrent"), trees=[0, 1, 7, 19, 31], name="concurrent")
+
+
+def test_stage_timing_means():
+    # profiling records every call's stage events; stage_ms gives their means
+    wl = synth.random_small(31, batch=2, L=4, V=2000, M=16, B=8, T=0.5, d_e=32, d_h=64)
+    dw = DeviceWorkload(wl)
+    try:
+        with pytest.raises(binding.DTError):
+            dw.plan.stage_ms()                    # nothing profiled yet
+        dw.plan.set_profiling(1)
+        for _ in range(5):
+            dw.run()
+        ms = dw.plan.stage_ms()
+        assert set(ms) == set(binding.STAGES)
+        assert all(0.0 < v < 1000.0 for v in ms.values()), ms
+        dw.plan.set_profiling(1)                  # a new count
+        with pytest.raises(binding.DTError):
+            dw.plan.stage_ms()
+        dw.plan.set_profiling(0)
+    finally:
+        dw.close()
