@@ -124,7 +124,7 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   // the expansion's LDS for every group size a batch in [1, max_batch] can use
   size_t lds_need = 0;
   for (int G = dt::expand_group_size(d_h, ncu, max_batch);; G *= 2) {
-    const size_t b = dt::expand_lds_bytes(d_h, G, M, nchunks);
+    const size_t b = dt::expand_lds_bytes(d_h, G, M, nchunks, L);
     lds_need = b > lds_need ? b : lds_need;
     if (G == dt::expand_group_size(d_h, ncu, 1)) break;
   }

@@ -49,6 +49,7 @@ static_assert(CH == 2 * NW, "children step: two nodes per wave");
 
 struct ExpArgs {
   int L, M, B, k, dh, G, norm_mode, pos_offset, ecap, batch, nchunks, nxcd;
+  int use_us;  // U slices of the expanded depth staged into LDS (see us_fits)
   float inv_tau, c2;  // c2 = log2(e) / tau
   const uint64_t *ckeys;
   const float2 *ctail;
@@ -74,13 +75,21 @@ struct Lds {
   int ng, ntok, nparent, nstate, nslot, ndepth, nrank, nexp, newidx, elist;
   int ins, popd, ppi, order, anc;
   int rcand, rcandv;  // the merged row of the depth being expanded
+  int rowids, uslice;  // all rows' candidate ids; this member's U slice of one depth
   int gpart, Sp, Sn, ell, rnk, chunk, scal, total;
   int sortbuf;  // aliases gpart.. (prologue only)
 };
 
 __host__ __device__ inline int mp_of(int M) { return (M + 63) / 64 * 64; }
 
-__host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks) {
+// The U rows of a depth's candidates (this member's units) are staged into LDS
+// with the parent states when the slice and all rows' ids are small.
+__host__ __device__ inline bool us_fits(int dh, int G, int M, int L) {
+  const int MP = mp_of(M);
+  return MP * (dh / G) * 4 <= 16384 && L * MP * 4 <= 8192;
+}
+
+__host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int L) {
   Lds l;
   int o = 0;
   auto take = [&](int bytes) {
@@ -107,6 +116,9 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks) {
   l.anc = take(kMaxB * 8 * 4);
   l.rcand = take(MP * 4);
   l.rcandv = take(MP * 4);
+  const bool us = us_fits(dh, G, M, L);
+  l.rowids = take(us ? L * MP * 4 : 0);
+  l.uslice = take(us ? MP * UW * 4 : 0);
   l.chunk = take(CH * 2);
   l.scal = take(64 * 4);
   // region reused by the prologue's merge
@@ -335,7 +347,7 @@ struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per 
 template <typename TW>
 __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const Lds ly = lds_layout(a.dh, a.G, a.M, a.nchunks);
+  const Lds ly = lds_layout(a.dh, a.G, a.M, a.nchunks, a.L);
   float *ng = reinterpret_cast<float *>(smem + ly.ng);
   int32_t *ntok = reinterpret_cast<int32_t *>(smem + ly.ntok);
   int16_t *nparent = reinterpret_cast<int16_t *>(smem + ly.nparent);
@@ -358,6 +370,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int16_t *rnk = reinterpret_cast<int16_t *>(smem + ly.rnk);
   int32_t *rcand = reinterpret_cast<int32_t *>(smem + ly.rcand);
   float *rcandv = reinterpret_cast<float *>(smem + ly.rcandv);
+  int32_t *rowids = reinterpret_cast<int32_t *>(smem + ly.rowids);
+  float *Us = reinterpret_cast<float *>(smem + ly.uslice);
   int16_t *cl = reinterpret_cast<int16_t *>(smem + ly.chunk);
   int *scal = reinterpret_cast<int *>(smem + ly.scal);
   float *scalf = reinterpret_cast<float *>(smem + ly.scal);
@@ -429,6 +443,12 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   {
     const int f = tid < L ? ld_dev(a.rflag + (size_t)t * L + tid) : 0;
     if (f) atomicOr(&scal[S_STATUS], f);
+    if (a.use_us)
+      for (int i = tid; i < L * MP; i += NT) {
+        const int d = i / MP, m = i - d * MP;
+        const int id = m < M ? ld_dev(a.cand + ((size_t)t * L + d) * M + m) : 0;
+        rowids[i] = id > 0 ? id : 0;  // dead slots (-1) read row 0, unused
+      }
   }
   __syncthreads();
 
@@ -503,6 +523,18 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
               rs, (__attribute__((address_space(3))) void *)(Sp + i * 256), 16,
               (slot * dh + k) * 4, 0, 0, kSc1);
+        }
+      }
+      // this member's U slice of depth d's candidates, straight into LDS
+      if (a.use_us && d < L) {
+        const __amdgpu_buffer_rsrc_t ru =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.U_all), 0, 0x7FFFFFF0, 0x00020000);
+        for (int i = wave; i < MP * UW / 256; i += NW) {
+          const int e = i * 256 + 4 * lane;
+          const int m = e / UW, k = e - m * UW;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              ru, (__attribute__((address_space(3))) void *)(Us + i * 256), 16,
+              (rowids[d * MP + m] * dh + member * UW + k) * 4, 0, 0, 0);
         }
       }
       if (tid < MP) {
@@ -592,7 +624,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
       for (int q = 0; q < nq; ++q) {
         float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (m < M) av = *reinterpret_cast<const float4 *>(urow + q * 16 + kq);
+        if (a.use_us)
+          av = *reinterpret_cast<const float4 *>(Us + m * UW + q * 16 + kq);  // slots >= M: row 0, unused
+        else if (m < M)
+          av = *reinterpret_cast<const float4 *>(urow + q * 16 + kq);
         const float4 bv = *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
@@ -655,12 +690,21 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       if (tail) sum += expf(R - mx);
       const float logZ = mx + logf(sum);
       float lv[4];
+      bool any = false;  // a child that could enter (ranks are needed only then)
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         if (s >= MP / 64) break;
-        const int m = lane + 64 * s;
         lv[s] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
-        ell[c * MP + m] = lv[s];
+        any |= lv[s] > NEG_INF && gpar + lv[s] >= vB;
+      }
+      if (__ballot(any) == 0) {
+        if (lane == 0) wcnt[c] = 0;
+        return;
+      }
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s >= MP / 64) break;
+        ell[c * MP + lane + 64 * s] = lv[s];
       }
       wave_sync();
       int kc = 0;
@@ -706,6 +750,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     int tot = 0;
     for (int c = 0; c < nc; ++c) tot += wcnt[c];
     for (int c = wave; c < nc; c += NW) {
+      if (wcnt[c] == 0) continue;
       int off = base;
       for (int c2 = 0; c2 < c; ++c2) off += wcnt[c2];
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
@@ -1073,8 +1118,8 @@ int expand_group_size(int d_h, int num_cus, int batch) {
   return G;
 }
 
-size_t expand_lds_bytes(int dh, int G, int M, int nchunks) {
-  return (size_t)lds_layout(dh, G, M, nchunks).total;
+size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L) {
+  return (size_t)lds_layout(dh, G, M, nchunks, L).total;
 }
 
 size_t expand_part_bytes(const dt_plan *p, int batch) {
@@ -1098,6 +1143,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.batch = batch;
   a.nchunks = g.nchunks;
   a.nxcd = 8;
+  a.use_us = us_fits(p->d_h, a.G, p->M, p->L) && (size_t)p->V * p->d_h * 4 < (size_t)1 << 31;
   a.inv_tau = inv_tau;
   a.c2 = 1.4426950408889634f * inv_tau;
   a.ckeys = ws.chunk_keys;
@@ -1117,7 +1163,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.part = ws.part;
   a.bar = ws.bar;
   a.out = *out;
-  const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks);
+  const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks, p->L);
   const void *fn = p->wdt == DT_BF16 ? (const void *)expand_kernel<uint16_t>
                                      : (const void *)expand_kernel<float>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -134,7 +134,7 @@ hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s);
 int expand_group_size(int d_h, int num_cus, int batch);
-size_t expand_lds_bytes(int dh, int G, int M, int nchunks);
+size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L);
 size_t expand_part_bytes(const dt_plan *p, int batch);
 hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);
 

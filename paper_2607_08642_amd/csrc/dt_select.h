@@ -135,8 +135,9 @@ __device__ inline void put(T *p, T v) {
 }
 
 // LDS carve of merge_row for nlists lists of M keys (byte offsets)
+constexpr int kMergeAllPairs = 1024;  // survivors ranked among themselves up to this many
 struct MergeBuf {
-  int top, heads, scnt, sidx, total;
+  int top, heads, skeys, scnt, sidx, total;
 };
 __host__ __device__ inline int up16(int b) { return (b + 15) & ~15; }
 __host__ __device__ inline MergeBuf merge_buf(int nlists, int M) {
@@ -146,7 +147,9 @@ __host__ __device__ inline MergeBuf merge_buf(int nlists, int M) {
   MergeBuf b;
   b.top = up16(8 * n);                 // keys: n u64 at 0
   b.heads = up16(b.top + 8 * M);       // top: M u64
-  b.scnt = up16(b.heads + 8 * nhp);    // heads: nhp u64
+  b.skeys = up16(b.heads + 8 * nhp);   // heads: nhp u64
+  const int ns_cap = n < kMergeAllPairs ? n : kMergeAllPairs;
+  b.scnt = up16(b.skeys + 8 * (ns_cap + 2));  // skeys: survivors' keys (+ padding)
   b.sidx = up16(b.scnt + 4 * n);       // scnt: n i32
   b.total = up16(b.sidx + 2 * n);      // sidx: n i16
   return b;
@@ -161,11 +164,11 @@ __host__ __device__ inline int merge_buf_bytes(int nlists, int M) { return merge
 //  * thr = the M-th best of the first q = ceil(M / nlists) keys of every list.
 //    Those keys are all in the row, so at least M keys are >= thr and thr is
 //    <= the row's M-th best key: keys below thr go straight to the tail.
-//  * a surviving key's rank is its position in its own list plus, for every
-//    other list, the number of larger keys there (a binary search).  A key
-//    outside every list lies below the M keys of its chunk's list, so for a
-//    rank below M this count is exact, and a count of M or more means the key
-//    is not among the row's M best.
+//  * a surviving key's rank below M is the number of larger survivors: a key
+//    outside every list lies below the M keys of its chunk's list, and a list
+//    key above a survivor is a survivor itself.  (With very many survivors the
+//    rank is its position in its own list plus a binary search in every other
+//    list, exact in the same way.)
 // buf: merge_buf_bytes(nlists, M) bytes of LDS; red: NT/64 float2.
 // DEV_SCOPE selects device-scope stores (results read by other workgroups).
 // vadd (nullable): candv[m] = logit + vadd[cand[m]] instead of the logit.
@@ -183,6 +186,7 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
   uint64_t *keys = buf;                                           // [n]
   uint64_t *top = reinterpret_cast<uint64_t *>(base + mb.top);    // [M]
   uint64_t *heads = reinterpret_cast<uint64_t *>(base + mb.heads);  // [nhp]
+  uint64_t *skeys = reinterpret_cast<uint64_t *>(base + mb.skeys);  // survivors' keys
   int32_t *scnt = reinterpret_cast<int32_t *>(base + mb.scnt);    // [n] survivor ranks
   int16_t *sidx = reinterpret_cast<int16_t *>(base + mb.sidx);    // [n] survivor positions
   __shared__ uint64_t s_thr;
@@ -226,39 +230,63 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
       const int at = atomicAdd(&s_ns, 1);
       sidx[at] = (int16_t)i;
       scnt[at] = i % M;
+      if (at < kMergeAllPairs) skeys[at] = k;
     } else {
       tail_add1(t, key_value(k), c);
     }
   }
   __syncthreads();
-  // 3. + the larger keys of every other list: one binary search per (survivor, list)
   const int ns = s_ns;
-  for (int p = tid; p < ns * nlists; p += NT) {
-    const int sv = p / nlists, j = p % nlists;
-    const int i = sidx[sv];
-    if (j == i / M) continue;
-    const uint64_t k = keys[i];
-    const uint64_t *lj = keys + j * M;
-    int lo = 0, hi = M;  // count of lj[] > k (lj is descending)
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (lj[mid] > k)
-        lo = mid + 1;
+  if (ns <= kMergeAllPairs) {
+    // 3a. every key above a survivor is itself a survivor or lies below M keys
+    //     of its own list, so a survivor's rank among the survivors is its rank
+    //     in the row whenever that is below M
+    if (tid == 0 && (ns & 1)) skeys[ns] = 0ull;  // pad for paired reads
+    __syncthreads();
+    const ulonglong2 *s2 = reinterpret_cast<const ulonglong2 *>(skeys);
+    for (int sv = tid; sv < ns; sv += NT) {
+      const uint64_t k = skeys[sv];
+      int r = 0;
+#pragma unroll 4
+      for (int j = 0; j < (ns + 1) >> 1; ++j) {
+        const ulonglong2 kk = s2[j];
+        r += (kk.x > k) + (kk.y > k);
+      }
+      if (r < M)
+        top[r] = k;
       else
-        hi = mid;
+        tail_add1(t, key_value(k), c);
     }
-    if (lo) atomicAdd(&scnt[sv], lo);
+    __syncthreads();
+  } else {
+    // 3b. + the larger keys of every other list: one binary search per (survivor, list)
+    for (int p = tid; p < ns * nlists; p += NT) {
+      const int sv = p / nlists, j = p % nlists;
+      const int i = sidx[sv];
+      if (j == i / M) continue;
+      const uint64_t k = keys[i];
+      const uint64_t *lj = keys + j * M;
+      int lo = 0, hi = M;  // count of lj[] > k (lj is descending)
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (lj[mid] > k)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      if (lo) atomicAdd(&scnt[sv], lo);
+    }
+    __syncthreads();
+    for (int sv = tid; sv < ns; sv += NT) {
+      const int r = scnt[sv];
+      const uint64_t k = keys[sidx[sv]];
+      if (r < M)
+        top[r] = k;
+      else
+        tail_add1(t, key_value(k), c);
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  for (int sv = tid; sv < ns; sv += NT) {
-    const int r = scnt[sv];
-    const uint64_t k = keys[sidx[sv]];
-    if (r < M)
-      top[r] = k;
-    else
-      tail_add1(t, key_value(k), c);
-  }
-  __syncthreads();
   t = block_tail<NT>(t, c, red);
   for (int i = tid; i < M; i += NT) {
     const uint64_t k = top[i];
