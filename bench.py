@@ -7,10 +7,14 @@ default workload is the Qwen3-8B-shaped single stream (L=16, V=151936, M=64,
 B=16, T=1, d_e=4096, d_h=512).  Logit buffers rotate through >= 512 MB so the
 256 MB Infinity Cache cannot serve the scan.
 
+The K timed calls are captured into one HIP graph and timed as one replay
+(--eager: launched one by one); the same K calls also run eagerly first, which
+gives the per-call GPU times and the stage durations (HIP events the library
+records between its kernels on the launch stream, every 8th call), and the
+graph's output is checked against theirs.
+
 Prints ONE JSON line: trees/s for the whole job, the per-kernel roofline of the
-dominant kernel (mean durations over the timed calls, from HIP events the
-library records between its kernels on the launch stream) and the CPU oracle
-timed on a bounded sample.
+dominant kernel and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -41,6 +45,8 @@ def parse():
                     help="logit bytes cycled through in the timed loop")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the K calls launched one by one instead of one HIP-graph replay")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (scale for PMC byte counters)")
     return ap.parse_args()
@@ -145,15 +151,15 @@ def main():
     ws = plan.workspace(wl.batch)
     stream = torch.cuda.current_stream()
 
-    def step(i):
-        plan.build_tree(bufs[i % nbuf], wl.T, h0, out=out, workspace=ws)
+    def step(i, o=out):
+        plan.build_tree(bufs[i % nbuf], wl.T, h0, out=o, workspace=ws)
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` calls, synchronised on both sides; the
-    # library records its stage events on the launch stream during these calls
+    # eager pass over the same K calls: per-call GPU times and the stage
+    # events the library records on the launch stream (every PROFILE_EVERY-th call)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     plan.set_profiling(PROFILE_EVERY)
     torch.cuda.synchronize()
@@ -163,10 +169,32 @@ def main():
         step(args.warmup + i)
     evs[-1].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    eager_wall = time.perf_counter() - t0
     per_call = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]) * 1e3  # us
-    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled timed calls
+    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled calls
     plan.set_profiling(0)
+    eager_last = {k: getattr(out, k).cpu().clone() for k in ("tokens", "parents", "scores", "mask")}
+
+    if args.eager:
+        wall = eager_wall
+    else:
+        # the same K calls captured into one HIP graph (two kernel nodes per
+        # call, no copies or memsets), replayed once untimed, checked against
+        # the eager pass, then timed as one replay
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(args.steps):
+                step(args.warmup + i)
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in eager_last.items():
+            if not torch.equal(getattr(out, k).cpu(), v):
+                raise RuntimeError(f"graph replay differs from the eager calls in {k}")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        graph.replay()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
 
     # expansions Alg. 1 performs: the root plus every popped node above depth L
     # (the kernel's extra speculative expansions are not counted as useful work)
@@ -204,9 +232,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.batch, "L": wl.L, "V": w.V, "M": wl.M,
                    "B": wl.B, "T": wl.T, "d_e": w.d_e, "d_h": w.d_h, "logit_buffers": nbuf},
+        "timing": "eager" if args.eager else "hip_graph",
         "us_per_tree": wall / trees * 1e6,
-        "gpu_us_per_call_p50": float(np.percentile(per_call, 50)),
-        "gpu_us_per_call_p99": float(np.percentile(per_call, 99)),
+        "eager": {"us_per_tree": eager_wall / trees * 1e6,
+                  "gpu_us_per_call_p50": float(np.percentile(per_call, 50)),
+                  "gpu_us_per_call_p99": float(np.percentile(per_call, 99))},
         "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
         "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
         "stages_us": stage_us,

@@ -43,9 +43,9 @@
  *
  * Envelope: 1 <= M <= min(V, 256); 1 <= B <= 256; 1 <= L <= 64;
  * 32 <= d_h <= 1024 with d_h % 32 == 0; 1 <= d_e <= 8192; 1 <= V < 2^31;
- * 14 * ceil(V / 10240) * M + 8 * M <= 98304 (bytes of the per-row merge
- * buffer); the
- * expansion kernel's LDS must fit the device (checked by dt_plan_create).
+ * the per-row merge buffer, about 22 * ceil(V / 10240) * M + 20 * M bytes,
+ * must fit 96 KiB (DT_ERR_UNSUPPORTED otherwise); the expansion kernel's LDS
+ * must fit the device (both checked by dt_plan_create and dt_scan_topm).
  */
 #ifndef DOMINOTREE_H
 #define DOMINOTREE_H
@@ -159,7 +159,9 @@ dt_status dt_workspace_size(const dt_plan *plan, int batch, size_t *bytes);
  *   T:  temperature (T <= 0 scores with tau = 1);
  *   workspace: >= dt_workspace_size bytes, 256-byte aligned, caller-owned;
  *   out: output arrays as documented in dt_tree.
- * Launches on `stream` and returns without waiting.  For small batches several
+ * Launches on `stream` and returns without waiting; the call may be captured
+ * into a HIP graph (it records no memset or copy nodes, only its two kernels,
+ * whose arguments are fixed at capture).  For small batches several
  * workgroups (at most one per CU in total) build each tree together and wait
  * on one another; they rely on being resident at the same time, which holds on
  * a device that other work does not fill.  Each wait is bounded: a tree whose
@@ -175,7 +177,8 @@ void dt_plan_destroy(dt_plan *plan);
  * call (the first one included) records a HIP event on its stream before its
  * first kernel and after each kernel: stage 0 = top-M scan of the logits
  * (kernel 1), 1 = per-row merge, expansion and emission (kernel 2).  every = 0
- * turns it off; enabling (again) starts a new count.
+ * turns it off; enabling (again) starts a new count.  Calls made while the
+ * stream is being captured into a HIP graph record no events and do not count.
  * dt_plan_stage_ms waits for the last profiled call and writes the mean stage
  * durations in milliseconds over the profiled calls (the most recent 1024) to
  * ms[0..1].  Returns DT_ERR_SHAPE if no profiled call has been made yet. */

@@ -119,8 +119,8 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (e != hipSuccess) return hip_fail(e, "device query");
   const int nchunks = dt::scan_geom(1, V, M).nchunks;
   if (dt::merge_lds_bytes(dt::scan_geom(1, V, M)) > (size_t)dt::kMergeLdsMax)
-    return fail(DT_ERR_UNSUPPORTED, "14 * ceil(V/%d) * M + 8 * M must stay within %d bytes",
-                dt::kScanChunk, dt::kMergeLdsMax);
+    return fail(DT_ERR_UNSUPPORTED, "the row merge of V and M needs %zu bytes of LDS, more than %d",
+                dt::merge_lds_bytes(dt::scan_geom(1, V, M)), dt::kMergeLdsMax);
   // the expansion's LDS for every group size a batch in [1, max_batch] can use
   size_t lds_need = 0;
   for (int G = dt::expand_group_size(d_h, ncu, max_batch);; G *= 2) {
@@ -261,8 +261,15 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
   dt::Workspace ws = dt::carve(plan, batch, static_cast<char *>(workspace));
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
-  // profiling every n-th call: the events' own cost (a few us each) stays small
-  const bool prof = plan->profiling > 0 && (plan->calls_since++ % plan->profiling) == 0;
+  // profiling every n-th call: the events' own cost (a few us each) stays small.
+  // Calls captured into a graph are neither profiled nor counted.
+  bool prof = false;
+  if (plan->profiling > 0) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    const hipError_t ce = hipStreamIsCapturing(s, &cs);
+    if (ce != hipSuccess) return hip_fail(ce, "stream capture query");
+    if (cs == hipStreamCaptureStatusNone) prof = (plan->calls_since++ % plan->profiling) == 0;
+  }
   hipEvent_t *ev = prof ? plan->ev + 3 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
   hipError_t e = prof ? hipEventRecord(ev[0], s) : hipSuccess;
   // the scan kernel also clears the expansion kernel's barrier counters

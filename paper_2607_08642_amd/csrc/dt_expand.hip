@@ -76,6 +76,7 @@ struct Lds {
   int ins, popd, ppi, order, anc;
   int rcand, rcandv;  // the merged row of the depth being expanded
   int rowids, uslice;  // all rows' candidate ids; this member's U slice of one depth
+  int pin, bhn;        // GRU inputs P of the chunk's nodes (this member's units); b_hn
   int gpart, Sp, Sn, ell, rnk, chunk, scal, total;
   int sortbuf;  // aliases gpart.. (prologue only)
 };
@@ -84,6 +85,11 @@ __host__ __device__ inline int mp_of(int M) { return (M + 63) / 64 * 64; }
 
 // The U rows of a depth's candidates (this member's units) are staged into LDS
 // with the parent states when the slice and all rows' ids are small.
+// The GRU inputs (rows of P, gates r, z, n) of a chunk's nodes are staged into
+// LDS when this member's slice is small; W_hh fragments are then loaded ahead.
+// Each node's three UW-float rows take one 256-float slot (one wave instruction).
+constexpr int kPinSlot = 256;
+__host__ __device__ inline bool pin_fits(int dh, int G) { return 3 * (dh / G) <= kPinSlot; }
 __host__ __device__ inline bool us_fits(int dh, int G, int M, int L) {
   const int MP = mp_of(M);
   return MP * (dh / G) * 4 <= 16384 && L * MP * 4 <= 8192;
@@ -119,6 +125,9 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
   const bool us = us_fits(dh, G, M, L);
   l.rowids = take(us ? L * MP * 4 : 0);
   l.uslice = take(us ? MP * UW * 4 : 0);
+  const bool pin = pin_fits(dh, G);
+  l.pin = take(pin ? CH * kPinSlot * 4 : 0);
+  l.bhn = take(pin ? UW * 4 : 0);
   l.chunk = take(CH * 2);
   l.scal = take(64 * 4);
   // region reused by the prologue's merge
@@ -138,12 +147,6 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
 // scalar slots in LDS
 enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CNT0 };
 
-__device__ inline uint16_t f2bf(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-__device__ inline float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
 __device__ inline float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
 
@@ -274,6 +277,57 @@ struct Gates;
 
 template <>
 struct Gates<uint16_t> {  // bf16 W_hh: 16x16x32 bf16 MFMA, S split as hi + mid + lo
+  // a k range of up to kPre steps can have its weights loaded ahead of time
+  static constexpr int kPre = 4;
+  struct Pre {
+    uint4 w[kPre][3];
+  };
+  static __device__ inline void preload(const ExpArgs &a, int u, int ks0, int ks1, Pre &p) {
+    const int lane = threadIdx.x & 63;
+    const int nks = a.dh / 32;
+    const uint4 *W = static_cast<const uint4 *>(a.whh);
+#pragma unroll
+    for (int kk = 0; kk < kPre; ++kk)
+#pragma unroll
+      for (int g = 0; g < 3; ++g)
+        if (ks0 + kk < ks1) p.w[kk][g] = W[((size_t)(u * 3 + g) * nks + ks0 + kk) * 64 + lane];
+  }
+  static __device__ inline void step(const float *srow, int ks, const uint4 (&wv)[3],
+                                     f32x4 (&acc)[3]) {
+    const float4 s0 = *reinterpret_cast<const float4 *>(srow + ks * 32);
+    const float4 s1 = *reinterpret_cast<const float4 *>(srow + ks * 32 + 4);
+    const float x[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+    // S = hi + mid + lo, each rounded to nearest (v_cvt_pk_bf16_f32); the
+    // residuals are exact, so the three bf16 products carry S to fp32 accuracy
+    bf16x8 hi, mi, lo;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const __bf16 h = (__bf16)x[e];
+      const float r1 = x[e] - (float)h;
+      const __bf16 m = (__bf16)r1;
+      hi[e] = h;
+      mi[e] = m;
+      lo[e] = (__bf16)(r1 - (float)m);
+    }
+#pragma unroll
+    for (int g = 0; g < 3; ++g) {
+      const bf16x8 wa = __builtin_bit_cast(bf16x8, wv[g]);
+      acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, lo, acc[g], 0, 0, 0);
+      acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, mi, acc[g], 0, 0, 0);
+      acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, hi, acc[g], 0, 0, 0);
+    }
+  }
+  // k steps [ks0, ks1) from preload(a, u, ks0, ks1, p); ks1 - ks0 <= kPre
+  static __device__ inline void run_pre(const ExpArgs &a, const float *Sp, const Pre &p, int ks0,
+                                        int ks1, f32x4 (&acc)[3]) {
+    const int lane = threadIdx.x & 63;
+    const float *srow = Sp + (lane & 15) * a.dh + (lane >> 4) * 8;
+#pragma unroll
+    for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < kPre; ++kk)
+      if (ks0 + kk < ks1) step(srow, ks0 + kk, p.w[kk], acc);
+  }
   static __device__ inline void run(const ExpArgs &a, const float *Sp, int u, int ks0, int ks1,
                                     f32x4 (&acc)[3]) {
     const int lane = threadIdx.x & 63;
@@ -293,28 +347,7 @@ struct Gates<uint16_t> {  // bf16 W_hh: 16x16x32 bf16 MFMA, S split as hi + mid 
 #pragma unroll
       for (int kk = 0; kk < PF; ++kk) {
         if (k0 + kk >= ks1) break;
-        const int ks = k0 + kk;
-        const float4 s0 = *reinterpret_cast<const float4 *>(srow + ks * 32);
-        const float4 s1 = *reinterpret_cast<const float4 *>(srow + ks * 32 + 4);
-        const float x[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-        bf16x8 hi, mi, lo;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint16_t h = f2bf(x[e]);
-          const float r1 = x[e] - bf2f(h);
-          const uint16_t m = f2bf(r1);
-          const uint16_t l = f2bf(r1 - bf2f(m));
-          hi[e] = __builtin_bit_cast(__bf16, h);
-          mi[e] = __builtin_bit_cast(__bf16, m);
-          lo[e] = __builtin_bit_cast(__bf16, l);
-        }
-#pragma unroll
-        for (int g = 0; g < 3; ++g) {
-          const bf16x8 wa = __builtin_bit_cast(bf16x8, wv[kk][g]);
-          acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, lo, acc[g], 0, 0, 0);
-          acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, mi, acc[g], 0, 0, 0);
-          acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, hi, acc[g], 0, 0, 0);
-        }
+        step(srow, k0 + kk, wv[kk], acc);
       }
     }
   }
@@ -322,6 +355,14 @@ struct Gates<uint16_t> {  // bf16 W_hh: 16x16x32 bf16 MFMA, S split as hi + mid 
 
 template <>
 struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per ks
+  static constexpr int kPre = 0;  // no weights loaded ahead (too many registers)
+  struct Pre {};
+  static __device__ inline void preload(const ExpArgs &, int, int, int, Pre &) {}
+  static __device__ inline void run_pre(const ExpArgs &, const float *, const Pre &, int, int,
+                                        f32x4 (&acc)[3]) {
+#pragma unroll
+    for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};  // never called
+  }
   static __device__ inline void run(const ExpArgs &a, const float *Sp, int u, int ks0, int ks1,
                                     f32x4 (&acc)[3]) {
     const int lane = threadIdx.x & 63;
@@ -372,6 +413,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   float *rcandv = reinterpret_cast<float *>(smem + ly.rcandv);
   int32_t *rowids = reinterpret_cast<int32_t *>(smem + ly.rowids);
   float *Us = reinterpret_cast<float *>(smem + ly.uslice);
+  float *pin = reinterpret_cast<float *>(smem + ly.pin);
+  float *bhn = reinterpret_cast<float *>(smem + ly.bhn);
   int16_t *cl = reinterpret_cast<int16_t *>(smem + ly.chunk);
   int *scal = reinterpret_cast<int *>(smem + ly.scal);
   float *scalf = reinterpret_cast<float *>(smem + ly.scal);
@@ -384,6 +427,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   const int MP = mp_of(M);
   const int UW = dh / G;       // hidden units of this member
   const int NG = UW / 16;      // unit groups of this member
+  const bool use_pin = pin_fits(dh, G);
   const float NEG_INF = -__builtin_huge_valf();
 
   // ---- which tree, which member (members of a tree share an XCD) ------------
@@ -420,6 +464,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scal[S_NEXP] = 0;
     scal[S_STOP] = 0;
   }
+  if (use_pin)
+    for (int u = tid; u < UW; u += NT) bhn[u] = a.b_hh[2 * dh + member * UW + u];
   __syncthreads();
 
   // ---- prologue: merge this member's rows of the scan ------------------------
@@ -484,18 +530,25 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // candidates and tail) and the parent path states of the chunk's nodes
     const int32_t *ccand = rcand;
     const float *ccandv = rcandv;
+    // this wave's share of W_hh . S: unit group gu (-1: none) over k steps [gk0, gk1);
+    // weights that fit kPre steps are loaded now, in the staging round trip
+    const int nks = dh / 32;
+    int gu = -1, gk0 = 0, gk1 = nks;
+    if (NG >= NW) {
+      if (wave < NG) gu = wave;
+    } else if (wave < NG * (NW / NG)) {
+      const int WPG = NW / NG, f = wave / NG;
+      gu = wave % NG;
+      gk0 = (nks * f) / WPG;
+      gk1 = (nks * (f + 1)) / WPG;
+    }
+    typename Gates<TW>::Pre wpre;
+    const bool wearly =
+        Gates<TW>::kPre > 0 && use_pin && d > 0 && gu >= 0 && gk1 - gk0 <= Gates<TW>::kPre;
+    if (wearly) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);
     if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
-    // GRU inputs of the first unit group this wave finishes (unit group gi =
-    // wave): P of gates r, z, n and b_hn for units 4 (lane/16) .. +3 of node lane%16
-    GruIn pre;
-    pre.r = pre.z = pre.n = pre.b = make_float4(0.f, 0.f, 0.f, 0.f);
     {
       // all loads are issued before the first LDS write (one wait)
-      if (d > 0 && wave < NG && (lane & 15) < nc) {
-        const float *prow = a.P_all + (size_t)ntok[cn[lane & 15]] * (3 * dh);
-        const int j0 = member * UW + wave * 16 + (lane >> 4) * 4;
-        pre = load_gru_in(prow, a.b_hh, dh, j0);
-      }
       const size_t row = (size_t)t * L + (d < L ? d : 0);
       const __amdgpu_buffer_rsrc_t rc = dev_rsrc(a.cand + row * M);
       const __amdgpu_buffer_rsrc_t rv = dev_rsrc(a.candv + row * M);
@@ -537,6 +590,22 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
               (rowids[d * MP + m] * dh + member * UW + k) * 4, 0, 0, 0);
         }
       }
+      // GRU inputs of the chunk's nodes straight into LDS, one wave instruction
+      // per node: lane l < 3 UW/4 takes 4 floats of gate l / (UW/4); the other
+      // lanes re-read the first 16 bytes into the slot's unused tail
+      if (use_pin && d > 0) {
+        const int QW = UW / 4;
+        const int g = lane / QW, k = (lane - g * QW) * 4;
+        const int voff = lane < 3 * QW ? (g * dh + k) * 4 : 0;
+        for (int c = wave; c < nc; c += NW) {
+          const int tok = __builtin_amdgcn_readfirstlane(ntok[cn[c]]);
+          const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+              const_cast<float *>(a.P_all + (size_t)tok * (3 * dh) + member * UW), 0, 0x7FFFFFF0,
+              0x00020000);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rp, (__attribute__((address_space(3))) void *)(pin + c * kPinSlot), 16, voff, 0, 0, 0);
+        }
+      }
       if (tid < MP) {
         rcand[tid] = rowld ? cid : 0;
         rcandv[tid] = rowld ? cval : NEG_INF;
@@ -557,10 +626,20 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       const float *prow = a.P_all + (size_t)(node >= 0 ? ntok[node] : 0) * (3 * dh);
       // r = sig(P_r + W_hr h), z = sig(P_z + W_hz h), n = tanh(P_n + r (W_hn h + b_hn)),
       // S = (1 - z) n + z h  (P_r, P_z carry b_hr, b_hz)
-      auto apply = [&](int gi, const f32x4 (&gh)[3], GruIn in) {
+      auto apply = [&](int gi, const f32x4 (&gh)[3]) {
         if (node < 0) return;
         const int u4 = gi * 16 + (lane >> 4) * 4;  // first of this lane's 4 units (in the member)
         const int j0 = member * UW + u4;
+        GruIn in;
+        if (use_pin) {
+          const float *pr = pin + c * kPinSlot + u4;
+          in.r = *reinterpret_cast<const float4 *>(pr);
+          in.z = *reinterpret_cast<const float4 *>(pr + UW);
+          in.n = *reinterpret_cast<const float4 *>(pr + 2 * UW);
+          in.b = *reinterpret_cast<const float4 *>(bhn + u4);
+        } else {
+          in = load_gru_in(prow, a.b_hh, dh, j0);
+        }
         const float xr[4] = {in.r.x, in.r.y, in.r.z, in.r.w}, xz[4] = {in.z.x, in.z.y, in.z.z, in.z.w};
         const float xn[4] = {in.n.x, in.n.y, in.n.z, in.n.w}, xb[4] = {in.b.x, in.b.y, in.b.z, in.b.w};
         float sv[4];
@@ -576,38 +655,69 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         const __amdgpu_buffer_rsrc_t rsw = dev_rsrc(a.states + (size_t)t * a.ecap * dh);
         st_dev16(rsw, (nstate[node] * dh + j0) * 4, make_float4(sv[0], sv[1], sv[2], sv[3]));
       };
-      const int nks = dh / 32;
       if (NG >= NW) {
         for (int gi = wave; gi < NG; gi += NW) {
           f32x4 gh[3];
-          Gates<TW>::run(a, Sp, u0 + gi, 0, nks, gh);
-          apply(gi, gh, gi == wave ? pre
-                                   : load_gru_in(prow, a.b_hh, dh, member * UW + gi * 16 + (lane >> 4) * 4));
+          if (wearly && gi == wave)
+            Gates<TW>::run_pre(a, Sp, wpre, 0, nks, gh);
+          else
+            Gates<TW>::run(a, Sp, u0 + gi, 0, nks, gh);
+          apply(gi, gh);
         }
       } else {
         // WPG waves split the k range of one unit group; partial sums meet in LDS
         const int WPG = NW / NG;
         if (wave < NG * WPG) {
-          const int gi = wave % NG, f = wave / NG;
           f32x4 gh[3];
-          Gates<TW>::run(a, Sp, u0 + gi, (nks * f) / WPG, (nks * (f + 1)) / WPG, gh);
+          if (wearly)
+            Gates<TW>::run_pre(a, Sp, wpre, gk0, gk1, gh);
+          else
+            Gates<TW>::run(a, Sp, u0 + gu, gk0, gk1, gh);
 #pragma unroll
           for (int g = 0; g < 3; ++g)
 #pragma unroll
             for (int i = 0; i < 4; ++i) gpart[((wave * 3 + g) * 64 + lane) * 4 + i] = gh[g][i];
         }
         __syncthreads();
-        if (wave < NG) {
-          f32x4 sum[3];
+        // gate sums and the update, one (unit, node) per thread: element e holds
+        // MFMA output lane l = (e / 4) % 64, row i = e % 4 of unit group e / 256,
+        // i.e. node l % 16 and unit 16 (e / 256) + 4 (l / 16) + i
+        const __amdgpu_buffer_rsrc_t rsw = dev_rsrc(a.states + (size_t)t * a.ecap * dh);
+        for (int e = tid; e < NG * 256; e += NT) {
+          const int gi = e >> 8, l = (e >> 2) & 63, i = e & 3;
+          const int cc = l & 15;
+          if (cc >= nc) continue;
+          const int nd = cn[cc];
+          float gs[3];
 #pragma unroll
-          for (int g = 0; g < 3; ++g)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              float s = 0.0f;
-              for (int ff = 0; ff < WPG; ++ff) s += gpart[(((ff * NG + wave) * 3 + g) * 64 + lane) * 4 + i];
-              sum[g][i] = s;
-            }
-          apply(wave, sum, pre);
+          for (int g = 0; g < 3; ++g) {
+            float sum = 0.0f;
+            for (int ff = 0; ff < WPG; ++ff) sum += gpart[(((ff * NG + gi) * 3 + g) * 64 + l) * 4 + i];
+            gs[g] = sum;
+          }
+          const int u = gi * 16 + (l >> 4) * 4 + i;
+          const int j = member * UW + u;
+          float xr, xz, xn, xb;
+          if (use_pin) {
+            const float *pr = pin + cc * kPinSlot + u;
+            xr = pr[0];
+            xz = pr[UW];
+            xn = pr[2 * UW];
+            xb = bhn[u];
+          } else {
+            const float *pr = a.P_all + (size_t)ntok[nd] * (3 * dh) + j;
+            xr = pr[0];
+            xz = pr[dh];
+            xn = pr[2 * dh];
+            xb = a.b_hh[2 * dh + j];
+          }
+          const float r = sigmoidf_(xr + gs[0]);
+          const float z = sigmoidf_(xz + gs[1]);
+          const float n = tanhf(xn + r * (gs[2] + xb));
+          const float sv = (1.0f - z) * n + z * Sp[cc * dh + j];
+          Sn[cc * UW + u] = sv;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rsw,
+                                                (nstate[nd] * dh + j) * 4, 0, kSc1);
         }
       }
     }

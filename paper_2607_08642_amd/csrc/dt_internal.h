@@ -26,7 +26,7 @@ constexpr int kScanSortCap = 4096;   // bitonic sort buffer (keys) per workgroup
 constexpr int kScanTargetGroups = 1024;  // scan workgroups worth launching (4 per CU)
 constexpr int kScanMaxBatches = 8;       // batches of kScanChunk per segment, at most
 constexpr int kScanFlushAt = 256;    // fallback: flush the candidate buffer beyond this
-constexpr int kMergeLdsMax = 96 * 1024;  // row merge buffer: 14 n + 8 M bytes, n = ceil(V/kScanChunk) M
+constexpr int kMergeLdsMax = 96 * 1024;  // row merge buffer (sel::merge_buf_bytes) at most
 
 // fold GEMM tile (bf16 MFMA path)
 constexpr int kFoldBM = 128;
@@ -37,8 +37,8 @@ constexpr int kFoldBK = 64;
 constexpr int kExpThreads = 512;
 constexpr int kNodeCap = 1536;       // live nodes per tree kept in LDS
 constexpr int kChunkNodes = 16;      // nodes expanded together (shared weight pass)
-constexpr int kBarStride = 64;
-constexpr int kProfSlots = 1024;   // profiled calls kept for stage averages       // ints per tree of barrier counters (own cache lines)
+constexpr int kBarStride = 64;       // ints per tree of barrier counters (own cache lines)
+constexpr int kProfSlots = 1024;     // profiled calls kept for stage averages
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

@@ -137,7 +137,7 @@ __device__ inline void put(T *p, T v) {
 // LDS carve of merge_row for nlists lists of M keys (byte offsets)
 constexpr int kMergeAllPairs = 1024;  // survivors ranked among themselves up to this many
 struct MergeBuf {
-  int top, heads, skeys, scnt, sidx, total;
+  int top, topv, heads, skeys, scnt, sidx, total;
 };
 __host__ __device__ inline int up16(int b) { return (b + 15) & ~15; }
 __host__ __device__ inline MergeBuf merge_buf(int nlists, int M) {
@@ -146,7 +146,8 @@ __host__ __device__ inline MergeBuf merge_buf(int nlists, int M) {
   const int nhp = (nlists * q + 1) & ~1;
   MergeBuf b;
   b.top = up16(8 * n);                 // keys: n u64 at 0
-  b.heads = up16(b.top + 8 * M);       // top: M u64
+  b.topv = up16(b.top + 8 * M);        // top: M u64
+  b.heads = up16(b.topv + 4 * M);      // topv: M f32
   b.skeys = up16(b.heads + 8 * nhp);   // heads: nhp u64
   const int ns_cap = n < kMergeAllPairs ? n : kMergeAllPairs;
   b.scnt = up16(b.skeys + 8 * (ns_cap + 2));  // skeys: survivors' keys (+ padding)
@@ -169,6 +170,8 @@ __host__ __device__ inline int merge_buf_bytes(int nlists, int M) { return merge
 //    key above a survivor is a survivor itself.  (With very many survivors the
 //    rank is its position in its own list plus a binary search in every other
 //    list, exact in the same way.)
+// Every key joins the tail through the thread that holds its list position,
+// so the result does not depend on the order the survivors were collected in.
 // buf: merge_buf_bytes(nlists, M) bytes of LDS; red: NT/64 float2.
 // DEV_SCOPE selects device-scope stores (results read by other workgroups).
 // vadd (nullable): candv[m] = logit + vadd[cand[m]] instead of the logit.
@@ -185,6 +188,7 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
   char *base = reinterpret_cast<char *>(buf);
   uint64_t *keys = buf;                                           // [n]
   uint64_t *top = reinterpret_cast<uint64_t *>(base + mb.top);    // [M]
+  float *topv = reinterpret_cast<float *>(base + mb.topv);        // [M]
   uint64_t *heads = reinterpret_cast<uint64_t *>(base + mb.heads);  // [nhp]
   uint64_t *skeys = reinterpret_cast<uint64_t *>(base + mb.skeys);  // survivors' keys
   int32_t *scnt = reinterpret_cast<int32_t *>(base + mb.scnt);    // [n] survivor ranks
@@ -195,16 +199,41 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
     *flag_lds = 0;
     s_ns = 0;
     s_thr = 1;  // stays 1 (keep every key) when the heads hold fewer than M keys
+    if (nh & 1) heads[nh] = 0ull;
   }
-  for (int i = tid; i < n; i += NT) keys[i] = lists[i];
-  for (int h = tid; h < nhp; h += NT) heads[h] = h < nh ? lists[(h / q) * M + (h % q)] : 0ull;
-  for (int i = tid; i < M; i += NT) top[i] = 0ull;
+  // 0. one round trip: the lists (heads copied on the way), chunk tails and flags
   Tail t = tail_empty();
   int bad = 0;
-  for (int i = tid; i < nlists; i += NT) {
-    t = tail_merge(t, Tail{tails[i].x, tails[i].y}, c);
-    bad |= flags[i];
+  {
+    float2 tl = make_float2(0.0f, 0.0f);
+    if (tid < nlists) {
+      tl = tails[tid];
+      bad = flags[tid];
+    }
+    for (int i0 = 0; i0 < n; i0 += 4 * NT) {
+      uint64_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * NT + tid;
+        v[u] = i < n ? lists[i] : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * NT + tid;
+        if (i < n) {
+          keys[i] = v[u];
+          const int l = i / M, p = i - l * M;
+          if (p < q) heads[l * q + p] = v[u];
+        }
+      }
+    }
+    if (tid < nlists) t = tail_merge(t, Tail{tl.x, tl.y}, c);
+    for (int i = tid + NT; i < nlists; i += NT) {
+      t = tail_merge(t, Tail{tails[i].x, tails[i].y}, c);
+      bad |= flags[i];
+    }
   }
+  for (int i = tid; i < M; i += NT) top[i] = 0ull;
   __syncthreads();
   if (bad) atomicOr(flag_lds, bad);
   // 1. thr: the M-th largest head (q heads per list)
@@ -237,29 +266,31 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
   }
   __syncthreads();
   const int ns = s_ns;
+  // 3. rank the survivors; the M best go to top[] and leave keys[] (zeroed)
   if (ns <= kMergeAllPairs) {
-    // 3a. every key above a survivor is itself a survivor or lies below M keys
-    //     of its own list, so a survivor's rank among the survivors is its rank
-    //     in the row whenever that is below M
+    // every key above a survivor is itself a survivor or lies below M keys of
+    // its own list, so a survivor's rank among the survivors is its rank in
+    // the row whenever that is below M
     if (tid == 0 && (ns & 1)) skeys[ns] = 0ull;  // pad for paired reads
     __syncthreads();
     const ulonglong2 *s2 = reinterpret_cast<const ulonglong2 *>(skeys);
     for (int sv = tid; sv < ns; sv += NT) {
       const uint64_t k = skeys[sv];
+      const float va = vadd ? vadd[key_index(k)] : 0.0f;  // in flight during the count
       int r = 0;
 #pragma unroll 4
       for (int j = 0; j < (ns + 1) >> 1; ++j) {
         const ulonglong2 kk = s2[j];
         r += (kk.x > k) + (kk.y > k);
       }
-      if (r < M)
+      if (r < M) {
         top[r] = k;
-      else
-        tail_add1(t, key_value(k), c);
+        topv[r] = key_value(k) + va;
+        keys[sidx[sv]] = 0ull;
+      }
     }
-    __syncthreads();
   } else {
-    // 3b. + the larger keys of every other list: one binary search per (survivor, list)
+    // + the larger keys of every other list: one binary search per (survivor, list)
     for (int p = tid; p < ns * nlists; p += NT) {
       const int sv = p / nlists, j = p % nlists;
       const int i = sidx[sv];
@@ -279,21 +310,27 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
     __syncthreads();
     for (int sv = tid; sv < ns; sv += NT) {
       const int r = scnt[sv];
-      const uint64_t k = keys[sidx[sv]];
-      if (r < M)
+      if (r < M) {
+        const uint64_t k = keys[sidx[sv]];
         top[r] = k;
-      else
-        tail_add1(t, key_value(k), c);
+        topv[r] = key_value(k) + (vadd ? vadd[key_index(k)] : 0.0f);
+      }
     }
     __syncthreads();
+    for (int sv = tid; sv < ns; sv += NT)
+      if (scnt[sv] < M) keys[sidx[sv]] = 0ull;
+  }
+  __syncthreads();
+  // 4. survivors outside the M best join the tail from their list position
+  for (int i = tid; i < n; i += NT) {
+    const uint64_t k = keys[i];
+    if (k >= thr) tail_add1(t, key_value(k), c);  // thr >= 1: empty slots stay out
   }
   t = block_tail<NT>(t, c, red);
   for (int i = tid; i < M; i += NT) {
     const uint64_t k = top[i];
-    float v = -__builtin_huge_valf();
-    if (k) v = vadd ? key_value(k) + vadd[key_index(k)] : key_value(k);
     put<DEV_SCOPE>(cand + i, k ? (int32_t)key_index(k) : (int32_t)-1);
-    put<DEV_SCOPE>(candv + i, v);
+    put<DEV_SCOPE>(candv + i, k ? topv[i] : -__builtin_huge_valf());
   }
   if (tid == 0) {
     put<DEV_SCOPE>(tailR, t.s > 0.0f ? t.m * inv_tau + logf(t.s) : -__builtin_huge_valf());
