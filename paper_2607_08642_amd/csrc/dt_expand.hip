@@ -148,7 +148,13 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
 enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CNT0 };
 
 
-__device__ inline float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
+// GRU activations on the hardware exp2 and reciprocal (about 1 ulp each):
+// sigmoid(x) = 1 / (1 + 2^(-x log2 e)), tanh(x) = 2 sigmoid(2x) - 1 (absolute
+// error ~1e-7, far below the path-state tolerance)
+__device__ inline float sigmoid_fast(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.44269504088896341f * x));
+}
+__device__ inline float tanh_fast(float x) { return 2.0f * sigmoid_fast(2.0f * x) - 1.0f; }
 
 __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -464,11 +470,16 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scal[S_NEXP] = 0;
     scal[S_STOP] = 0;
   }
-  if (use_pin)
-    for (int u = tid; u < UW; u += NT) bhn[u] = a.b_hh[2 * dh + member * UW + u];
   __syncthreads();
 
   // ---- prologue: merge this member's rows of the scan ------------------------
+  // (the root's path state, h0 or zeros, is loaded first and stored after)
+  static_assert(kMaxDh <= 2 * NT, "root state: two units per thread");
+  float h0v[2] = {0.0f, 0.0f};
+  const float bhv = (use_pin && tid < UW) ? a.b_hh[2 * dh + member * UW + tid] : 0.0f;  // b_hn
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+    if (a.h0 && tid + q * NT < UW) h0v[q] = a.h0[(size_t)t * dh + member * UW + tid + q * NT];
   for (int d = member; d < L; d += G) {
     const int row = t * L + d;
     sel::merge_row<NT, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
@@ -480,10 +491,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   {
     // the root's path state (h0 or zeros) in slot ecap-1: this member's units
     float *root = a.states + ((size_t)t * a.ecap + a.ecap - 1) * dh;
-    for (int u = tid; u < UW; u += NT) {
-      const int j = member * UW + u;
-      st_dev(root + j, a.h0 ? a.h0[(size_t)t * dh + j] : 0.0f);
-    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+      if (tid + q * NT < UW) st_dev(root + member * UW + tid + q * NT, h0v[q]);
+    if (use_pin && tid < UW) bhn[tid] = bhv;
   }
   group_barrier(ctr, G, nbar, &scal[S_STATUS]);
   {
@@ -645,9 +656,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         float sv[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float r = sigmoidf_(xr[i] + gh[0][i]);
-          const float z = sigmoidf_(xz[i] + gh[1][i]);
-          const float n = tanhf(xn[i] + r * (gh[2][i] + xb[i]));
+          const float r = sigmoid_fast(xr[i] + gh[0][i]);
+          const float z = sigmoid_fast(xz[i] + gh[1][i]);
+          const float n = tanh_fast(xn[i] + r * (gh[2][i] + xb[i]));
           const float hprev = Sp[c * dh + j0 + i];
           sv[i] = (1.0f - z) * n + z * hprev;
           Sn[c * UW + u4 + i] = sv[i];
@@ -711,9 +722,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
             xn = pr[2 * dh];
             xb = a.b_hh[2 * dh + j];
           }
-          const float r = sigmoidf_(xr + gs[0]);
-          const float z = sigmoidf_(xz + gs[1]);
-          const float n = tanhf(xn + r * (gs[2] + xb));
+          const float r = sigmoid_fast(xr + gs[0]);
+          const float z = sigmoid_fast(xz + gs[1]);
+          const float n = tanh_fast(xn + r * (gs[2] + xb));
           const float sv = (1.0f - z) * n + z * Sp[cc * dh + j];
           Sn[cc * UW + u] = sv;
           __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rsw,
@@ -892,11 +903,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         scal[S_STATUS] |= DT_TREE_TRUNCATED;  // table overflow (massive exact ties)
       }
       scal[S_NN] = nn;
-      if (d > 0) {
-        scal[S_NEXP] += nc;
-        for (int c = 0; c < nc; ++c) nexp[cn[c]] = 1;
-      }
+      if (d > 0) scal[S_NEXP] += nc;
     }
+    if (d > 0 && tid < nc) nexp[cn[tid]] = 1;
     __syncthreads();
   };
 

@@ -234,20 +234,30 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
     }
   }
   for (int i = tid; i < M; i += NT) top[i] = 0ull;
+  for (int i = tid; i < nh; i += NT) scnt[i] = 0;
   __syncthreads();
   if (bad) atomicOr(flag_lds, bad);
-  // 1. thr: the M-th largest head (q heads per list)
-  for (int h = tid; h < nh; h += NT) {
-    const uint64_t k = heads[h];
-    if (!k) continue;
-    int r = 0;
+  // 1. thr: the M-th largest head (q heads per list); each head's count of
+  //    larger heads is split over RS threads
+  {
+    const int np = nhp / 2;
+    const int RS = nh >= NT ? 1 : (NT / nh > 16 ? 16 : NT / nh);
+    const int per = (np + RS - 1) / RS;
     const ulonglong2 *h2 = reinterpret_cast<const ulonglong2 *>(heads);
-#pragma unroll 8
-    for (int j = 0; j < nhp / 2; ++j) {
-      const ulonglong2 v = h2[j];
-      r += (v.x > k) + (v.y > k);
+    for (int p = tid; p < nh * RS; p += NT) {
+      const int h = p / RS, j0 = (p - h * RS) * per;
+      const int j1 = j0 + per < np ? j0 + per : np;
+      const uint64_t k = heads[h];
+      int r = 0;
+      for (int j = j0; j < j1; ++j) {
+        const ulonglong2 v = h2[j];
+        r += (v.x > k) + (v.y > k);
+      }
+      if (r) atomicAdd(&scnt[h], r);
     }
-    if (r == M - 1) s_thr = k;
+    __syncthreads();
+    for (int h = tid; h < nh; h += NT)
+      if (heads[h] && scnt[h] == M - 1) s_thr = heads[h];
   }
   __syncthreads();
   const uint64_t thr = s_thr;
@@ -270,20 +280,33 @@ __device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2
   if (ns <= kMergeAllPairs) {
     // every key above a survivor is itself a survivor or lies below M keys of
     // its own list, so a survivor's rank among the survivors is its rank in
-    // the row whenever that is below M
+    // the row whenever that is below M.  Each count is split over RS threads.
     if (tid == 0 && (ns & 1)) skeys[ns] = 0ull;  // pad for paired reads
+    for (int sv = tid; sv < ns; sv += NT) scnt[sv] = 0;
+    // the first survivor this thread places: its vadd entry is in flight during the count
+    const float va0 = (vadd && tid < ns) ? vadd[key_index(skeys[tid])] : 0.0f;
     __syncthreads();
+    const int np = (ns + 1) >> 1;
+    const int RS = ns >= NT ? 1 : (NT / ns > 16 ? 16 : NT / ns);
+    const int per = (np + RS - 1) / RS;
     const ulonglong2 *s2 = reinterpret_cast<const ulonglong2 *>(skeys);
-    for (int sv = tid; sv < ns; sv += NT) {
+    for (int p = tid; p < ns * RS; p += NT) {
+      const int sv = p / RS, j0 = (p - sv * RS) * per;
+      const int j1 = j0 + per < np ? j0 + per : np;
       const uint64_t k = skeys[sv];
-      const float va = vadd ? vadd[key_index(k)] : 0.0f;  // in flight during the count
       int r = 0;
-#pragma unroll 4
-      for (int j = 0; j < (ns + 1) >> 1; ++j) {
+      for (int j = j0; j < j1; ++j) {
         const ulonglong2 kk = s2[j];
         r += (kk.x > k) + (kk.y > k);
       }
+      if (r) atomicAdd(&scnt[sv], r);
+    }
+    __syncthreads();
+    for (int sv = tid; sv < ns; sv += NT) {
+      const int r = scnt[sv];
       if (r < M) {
+        const uint64_t k = skeys[sv];
+        const float va = sv == tid ? va0 : (vadd ? vadd[key_index(k)] : 0.0f);
         top[r] = k;
         topv[r] = key_value(k) + va;
         keys[sidx[sv]] = 0ull;
