@@ -145,7 +145,7 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
 }
 
 // scalar slots in LDS
-enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CNT0 };
+enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR, S_CNT0 };
 
 
 // GRU activations on the hardware exp2 and reciprocal (about 1 ulp each):
@@ -469,6 +469,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scalf[S_VB] = NEG_INF;
     scal[S_NEXP] = 0;
     scal[S_STOP] = 0;
+    scal[S_CUR] = 0;
   }
   __syncthreads();
 
@@ -910,8 +911,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   };
 
   // ---- vB = B-th best known score; drop nodes below it when room is needed --
-  auto update_vb = [&](bool compact) {
+  // Returns vB to every thread (S_VB is written for readers past the next barrier).
+  auto update_vb = [&](bool compact) -> float {
     const int nn = scal[S_NN];
+    float vB = scalf[S_VB];
     if (nn >= B) {
       float best = __builtin_huge_valf();
       const float4 *g4 = reinterpret_cast<const float4 *>(ng);
@@ -930,15 +933,12 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       best = wave_min_f(best);
       if (lane == 0) scalf[S_CNT0 + wave] = best;
       __syncthreads();
-      if (tid == 0) {
-        float v = scalf[S_CNT0];
-        for (int w = 1; w < NW; ++w) v = fminf(v, scalf[S_CNT0 + w]);
-        scalf[S_VB] = v;
-      }
-      __syncthreads();
+      vB = scalf[S_CNT0];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) vB = fminf(vB, scalf[S_CNT0 + w]);
+      if (tid == 0) scalf[S_VB] = vB;
     }
-    if (!compact || nn < B) return;
-    const float vB = scalf[S_VB];
+    if (!compact || nn < B) return vB;
     // keep g >= vB (parents always score at least their children: links stay valid)
     for (int r0 = 0; r0 < nn; r0 += NT) {
       const int i = r0 + tid;
@@ -987,91 +987,87 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     __syncthreads();
     if (tid == 0) scal[S_NN] = kept;
     __syncthreads();
+    return vB;
   };
 
   // ---- phase A ---------------------------------------------------------------
+  // Nodes enter the table in depth order (a chunk's children are one level
+  // deeper than every node not yet reached), so one cursor walks it once: each
+  // chunk is the next up-to-chunk_cap unexpanded nodes above depth L scoring
+  // >= vB, all at the depth of the first of them.  A node the cursor passes
+  // without taking scores below vB, and vB only grows, so it can never be
+  // popped.
   expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
-  update_vb(false);
-  for (int iter = 0; iter < L; ++iter) {
-    // eligible: known, unexpanded, above depth L, score >= vB (index order)
-    const int nn = scal[S_NN];
-    const float vB = scalf[S_VB];
-    for (int r0 = 0; r0 < nn; r0 += NT) {
-      const int i = r0 + tid;
-      const bool e = i < nn && !nexp[i] && ndepth[i] < L && ng[i] >= vB;
-      const Compact cp = block_compact(e, wcnt);
-      const int off = r0 ? scal[S_NE] : 0;
-      if (e) elist[off + cp.pos] = (int16_t)i;
-      __syncthreads();
-      if (tid == 0) scal[S_NE] = off + cp.total;
-      __syncthreads();
-    }
-    const int ne = nn ? scal[S_NE] : 0;
-    if (ne == 0) break;
-    int pos = 0;
-    while (pos < ne) {
-      __syncthreads();  // everyone has read the previous chunk's scalars
-      if (wave == 0) {
-        // the next up-to-chunk_cap entries of elist that still score >= vB, in order
-        const float v = scalf[S_VB];
-        int c = 0, p = pos;
-        while (p < ne && c < chunk_cap) {
-          const int idx = p + lane;
-          const int i = idx < ne ? elist[idx] : -1;
-          const bool ok = i >= 0 && ng[i] >= v;
-          const uint64_t bal = __ballot(ok);
-          const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
-          const int need = chunk_cap - c, have = __popcll(bal);
-          if (ok && before < need) cl[c + before] = (int16_t)i;
-          if (have >= need) {
-            // stop right after the need-th qualifying entry
-            const uint64_t last = __ballot(ok && before == need - 1);
-            p += __builtin_ctzll(last) + 1;
-            c = chunk_cap;
+  for (;;) {
+    const float vB = update_vb(false);
+    if (wave == 0) {
+      const int nn = scal[S_NN];
+      int p = scal[S_CUR], c = 0, dsel = -1;
+      bool done = false;
+      while (!done && p < nn) {
+        const int i = p + lane;
+        const bool ok = i < nn && !nexp[i] && ndepth[i] < L && ng[i] >= vB;
+        const int di = ok ? (int)ndepth[i] : -1;
+        const uint64_t bal = __ballot(ok);
+        if (bal == 0) {
+          p += 64;
+          continue;
+        }
+        if (dsel < 0) dsel = __shfl(di, __builtin_ctzll(bal));
+        const uint64_t deeper = __ballot(ok && di != dsel);
+        uint64_t use = __ballot(ok && di == dsel);
+        if (deeper) use &= (1ull << __builtin_ctzll(deeper)) - 1;  // stop at the next depth
+        const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(use >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)use, 0));
+        const bool mine = (use >> lane) & 1ull;
+        const int have = __popcll(use), need = chunk_cap - c;
+        if (mine && before < need) cl[c + before] = (int16_t)i;
+        if (have >= need) {
+          // the cursor moves right past the need-th node taken
+          const uint64_t last = __ballot(mine && before == need - 1);
+          p += __builtin_ctzll(last) + 1;
+          c = chunk_cap;
+          done = true;
+        } else {
+          c += have;
+          if (deeper) {
+            p += __builtin_ctzll(deeper);
+            done = true;
           } else {
-            p = (p + 64 < ne) ? p + 64 : ne;
-            c += have;
+            p += 64;
           }
         }
-        if (lane == 0) {
-          scal[S_NC] = c;
-          scal[S_TOT] = p;
-          if (c && scal[S_NEXP] + c > a.ecap - 1) {
-            scal[S_STATUS] |= DT_TREE_TRUNCATED;
-            scal[S_STOP] = 1;
-          }
+      }
+      if (lane == 0) {
+        scal[S_NC] = c;
+        scal[S_CUR] = p < nn ? p : nn;
+        if (c && scal[S_NEXP] + c > a.ecap - 1) {
+          scal[S_STATUS] |= DT_TREE_TRUNCATED;
+          scal[S_STOP] = 1;
         }
+      }
+    }
+    __syncthreads();
+    const int nc = scal[S_NC];
+    if (scal[S_STOP] || nc == 0) break;
+    if (scal[S_NN] + nc * a.k > NC - CH) {
+      // make room for this chunk's children; the cursor restarts (nodes it
+      // passed are expanded or below vB, and are passed again)
+      update_vb(true);
+      if (tid == 0) {
+        int c2 = 0;
+        for (int c = 0; c < nc; ++c) {
+          const int i = newidx[cl[c]];
+          if (i >= 0) cl[c2++] = (int16_t)i;
+        }
+        scal[S_NC] = c2;
+        scal[S_CUR] = 0;
       }
       __syncthreads();
-      const int nc = scal[S_NC];
-      pos = scal[S_TOT];
-      if (scal[S_STOP]) break;
-      if (nc == 0) continue;
-      if (scal[S_NN] + nc * a.k > NC - CH) {
-        // make room for this chunk's children
-        update_vb(true);
-        for (int p = tid; p < ne; p += NT) {
-          const int i = elist[p];
-          elist[p] = (i >= 0) ? newidx[i] : (int16_t)-1;
-        }
-        __syncthreads();
-        if (tid == 0) {
-          int c2 = 0;
-          for (int c = 0; c < nc; ++c) {
-            const int i = newidx[cl[c]];
-            if (i >= 0) cl[c2++] = (int16_t)i;
-          }
-          scal[S_NC] = c2;
-        }
-        __syncthreads();
-      }
-      const int nc2 = scal[S_NC];
-      if (nc2 == 0) continue;
-      expand_chunk(cl, nc2, ndepth[cl[0]]);
-      update_vb(false);
     }
-    if (scal[S_STOP]) break;
+    const int nc2 = scal[S_NC];
+    if (nc2 == 0) continue;
+    expand_chunk(cl, nc2, ndepth[cl[0]]);
   }
   if (member != 0) return;
 
