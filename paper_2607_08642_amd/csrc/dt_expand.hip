@@ -179,8 +179,8 @@ constexpr int kSc1 = 16;  // cache-policy bit: device scope
 __device__ inline float4 ld_dev16(__amdgpu_buffer_rsrc_t r, int byte_off) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kSc1));
 }
-__device__ inline float ld_dev4(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, kSc1));
+__device__ inline float ld_dev4(__amdgpu_buffer_rsrc_t r, int byte_off, int sgpr_off = 0) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, sgpr_off, kSc1));
 }
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -693,43 +693,49 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         __syncthreads();
         // gate sums and the update, one (unit, node) per thread: element e holds
         // MFMA output lane l = (e / 4) % 64, row i = e % 4 of unit group e / 256,
-        // i.e. node l % 16 and unit 16 (e / 256) + 4 (l / 16) + i
+        // i.e. node l % 16 and unit 16 (e / 256) + 4 (l / 16) + i.  The four
+        // lanes of a quad hold four consecutive units of one node: the first
+        // stores them with one 16-byte store.
         const __amdgpu_buffer_rsrc_t rsw = dev_rsrc(a.states + (size_t)t * a.ecap * dh);
-        for (int e = tid; e < NG * 256; e += NT) {
+        for (int e0 = 0; e0 < NG * 256; e0 += NT) {
+          const int e = e0 + tid;
           const int gi = e >> 8, l = (e >> 2) & 63, i = e & 3;
           const int cc = l & 15;
-          if (cc >= nc) continue;
-          const int nd = cn[cc];
-          float gs[3];
-#pragma unroll
-          for (int g = 0; g < 3; ++g) {
-            float sum = 0.0f;
-            for (int ff = 0; ff < WPG; ++ff) sum += gpart[(((ff * NG + gi) * 3 + g) * 64 + l) * 4 + i];
-            gs[g] = sum;
-          }
+          const bool live = e < NG * 256 && cc < nc;  // uniform over a quad
+          const int nd = live ? cn[cc] : 0;
           const int u = gi * 16 + (l >> 4) * 4 + i;
           const int j = member * UW + u;
-          float xr, xz, xn, xb;
-          if (use_pin) {
-            const float *pr = pin + cc * kPinSlot + u;
-            xr = pr[0];
-            xz = pr[UW];
-            xn = pr[2 * UW];
-            xb = bhn[u];
-          } else {
-            const float *pr = a.P_all + (size_t)ntok[nd] * (3 * dh) + j;
-            xr = pr[0];
-            xz = pr[dh];
-            xn = pr[2 * dh];
-            xb = a.b_hh[2 * dh + j];
+          float sv = 0.0f;
+          if (live) {
+            float gs[3];
+#pragma unroll
+            for (int g = 0; g < 3; ++g) {
+              float sum = 0.0f;
+              for (int ff = 0; ff < WPG; ++ff) sum += gpart[(((ff * NG + gi) * 3 + g) * 64 + l) * 4 + i];
+              gs[g] = sum;
+            }
+            float xr, xz, xn, xb;
+            if (use_pin) {
+              const float *pr = pin + cc * kPinSlot + u;
+              xr = pr[0];
+              xz = pr[UW];
+              xn = pr[2 * UW];
+              xb = bhn[u];
+            } else {
+              const float *pr = a.P_all + (size_t)ntok[nd] * (3 * dh) + j;
+              xr = pr[0];
+              xz = pr[dh];
+              xn = pr[2 * dh];
+              xb = a.b_hh[2 * dh + j];
+            }
+            const float r = sigmoid_fast(xr + gs[0]);
+            const float z = sigmoid_fast(xz + gs[1]);
+            const float n = tanh_fast(xn + r * (gs[2] + xb));
+            sv = (1.0f - z) * n + z * Sp[cc * dh + j];
+            Sn[cc * UW + u] = sv;
           }
-          const float r = sigmoid_fast(xr + gs[0]);
-          const float z = sigmoid_fast(xz + gs[1]);
-          const float n = tanh_fast(xn + r * (gs[2] + xb));
-          const float sv = (1.0f - z) * n + z * Sp[cc * dh + j];
-          Sn[cc * UW + u] = sv;
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rsw,
-                                                (nstate[nd] * dh + j) * 4, 0, kSc1);
+          const float s1 = sel::dpp_f<0x55>(sv), s2 = sel::dpp_f<0xAA>(sv), s3 = sel::dpp_f<0xFF>(sv);
+          if (live && i == 0) st_dev16(rsw, (nstate[nd] * dh + j) * 4, make_float4(sv, s1, s2, s3));
         }
       }
     }
@@ -738,7 +744,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // 2. this member's part of delta[c][m] = U[cand[m]] . S_c over its units (fp32 MFMA)
     const int RT = (M + 15) / 16;
     const int nq = UW / 16;
-    float *mypart = a.part + (((size_t)t * 2 + pb) * CH) * MP * G + member;
+    // parts of member j: a [CH][MP] block of their own (no line is shared by two writers)
+    const __amdgpu_buffer_rsrc_t rmy =
+        dev_rsrc(a.part + (((size_t)t * 2 + pb) * G + member) * CH * MP);
     for (int rt = wave; rt < RT; rt += NW) {
       const int m = rt * 16 + (lane & 15);
       const int c = lane & 15, kq = (lane >> 4) * 4;
@@ -758,27 +766,28 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       // lane l, register i: slot rt*16 + (l/16)*4 + i, node l%16
       if (c < nc)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          st_dev(mypart + ((size_t)c * MP + rt * 16 + (lane >> 4) * 4 + i) * G, acc[i]);
+        st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
+                 make_float4(acc[0], acc[1], acc[2], acc[3]));
     }
     group_barrier(ctr, G, nbar, &scal[S_STATUS]);
     // 3. children of each node: normalise, rank, keep the top-k above vB
     const float vB = scalf[S_VB];
     const float R = scalf[S_R];
-    const __amdgpu_buffer_rsrc_t rp = dev_rsrc(a.part + ((size_t)t * 2 + pb) * CH * MP * G);
+    const __amdgpu_buffer_rsrc_t rp = dev_rsrc(a.part + ((size_t)t * 2 + pb) * G * CH * MP);
     pb ^= 1;
-    // the G parts of a slot are contiguous: all loads are issued, then summed in order
+    // the G parts of a slot, one from each member's block: all loads are
+    // issued, then summed in member order
     auto load_parts = [&](int c, int m) -> Parts {
       Parts p;
-      const int off = ((c * MP + m) * G) * 4;
-      if (G >= 4) {
+      const int off = (c * MP + m) * 4, stride = CH * MP * 4;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-          if (q4 * 4 < G) p.q[q4] = ld_dev16(rp, off + q4 * 16);
-      } else {
-        p.q[0].x = ld_dev4(rp, off);
-        if (G > 1) p.q[0].y = ld_dev4(rp, off + 4);
+      for (int q4 = 0; q4 < 4; ++q4) {
+        p.q[q4] = make_float4(0.f, 0.f, 0.f, 0.f);
+        // (the member stride goes in the scalar offset)
+        if (4 * q4 + 0 < G) p.q[q4].x = ld_dev4(rp, off, (4 * q4 + 0) * stride);
+        if (4 * q4 + 1 < G) p.q[q4].y = ld_dev4(rp, off, (4 * q4 + 1) * stride);
+        if (4 * q4 + 2 < G) p.q[q4].z = ld_dev4(rp, off, (4 * q4 + 2) * stride);
+        if (4 * q4 + 3 < G) p.q[q4].w = ld_dev4(rp, off, (4 * q4 + 3) * stride);
       }
       return p;
     };
