@@ -499,14 +499,25 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   }
   group_barrier(ctr, G, nbar, &scal[S_STATUS]);
   {
-    const int f = tid < L ? ld_dev(a.rflag + (size_t)t * L + tid) : 0;
+    // one round trip: the row flags and (U slices staged) every row's candidate ids
+    const __amdgpu_buffer_rsrc_t rfl = dev_rsrc(a.rflag + (size_t)t * L);
+    const __amdgpu_buffer_rsrc_t rid = dev_rsrc(a.cand + (size_t)t * L * M);
+    const int f = tid < L ? __builtin_bit_cast(int, ld_dev4(rfl, tid * 4)) : 0;
+    constexpr int kIdsPer = 4;  // L * MP * 4 <= 8192 bytes when U slices are staged
+    static_assert(8192 / 4 <= kIdsPer * NT, "row ids per thread");
+    int ids[kIdsPer];
+#pragma unroll
+    for (int q = 0; q < kIdsPer; ++q) {
+      const int i = tid + q * NT;
+      const int d = i / MP, m = i - d * MP;
+      ids[q] = (a.use_us && i < L * MP && m < M) ? __builtin_bit_cast(int, ld_dev4(rid, (d * M + m) * 4)) : 0;
+    }
     if (f) atomicOr(&scal[S_STATUS], f);
-    if (a.use_us)
-      for (int i = tid; i < L * MP; i += NT) {
-        const int d = i / MP, m = i - d * MP;
-        const int id = m < M ? ld_dev(a.cand + ((size_t)t * L + d) * M + m) : 0;
-        rowids[i] = id > 0 ? id : 0;  // dead slots (-1) read row 0, unused
-      }
+#pragma unroll
+    for (int q = 0; q < kIdsPer; ++q) {
+      const int i = tid + q * NT;
+      if (a.use_us && i < L * MP) rowids[i] = ids[q] > 0 ? ids[q] : 0;  // dead slots (-1) read row 0, unused
+    }
   }
   __syncthreads();
 
