@@ -832,44 +832,72 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       if (tail) sum += expf(R - mx);
       const float logZ = mx + logf(sum);
       float lv[4];
-      bool any = false;  // a child that could enter (ranks are needed only then)
+      // E: the slots whose child could enter (log-prob finite, g >= vB).  A slot
+      // ranked above a member of E is in E itself, so a member's rank among
+      // all slots is its rank within E.
+      uint64_t em[4];
+      int ne = 0;
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
+        em[s] = 0ull;
         if (s >= MP / 64) break;
         lv[s] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
-        any |= lv[s] > NEG_INF && gpar + lv[s] >= vB;
+        em[s] = __ballot(lv[s] > NEG_INF && gpar + lv[s] >= vB);
+        ne += __popcll(em[s]);
+        ell[c * MP + lane + 64 * s] = lv[s];
       }
-      if (__ballot(any) == 0) {
+      if (ne == 0) {
         if (lane == 0) wcnt[c] = 0;
         return;
       }
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s >= MP / 64) break;
-        ell[c * MP + lane + 64 * s] = lv[s];
-      }
-      wave_sync();
       int kc = 0;
-      const float4 *e4 = reinterpret_cast<const float4 *>(ell + c * MP);
+      if (ne <= 24) {
+        // few members: walk E's slots, (log-prob desc, slot asc)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s >= MP / 64) break;
-        const int m = lane + 64 * s;
-        const float lm = lv[s];
-        // rank = slots ahead of m by (log-prob desc, slot asc); slots >= M hold -inf
-        int rank = 0;
-#pragma unroll 4
-        for (int q = 0; q < MP / 4; ++q) {
-          const float4 v = e4[q];
-          const int m2 = 4 * q;
-          rank += (v.x > lm) | ((v.x == lm) & (m2 < m));
-          rank += (v.y > lm) | ((v.y == lm) & (m2 + 1 < m));
-          rank += (v.z > lm) | ((v.z == lm) & (m2 + 2 < m));
-          rank += (v.w > lm) | ((v.w == lm) & (m2 + 3 < m));
+        for (int s = 0; s < 4; ++s) {
+          if (s >= MP / 64) break;
+          const int m = lane + 64 * s;
+          const float lm = lv[s];
+          int rank = 0;
+#pragma unroll
+          for (int s2 = 0; s2 < 4; ++s2) {
+            if (s2 >= MP / 64) break;
+            uint64_t b = em[s2];
+            while (b) {
+              const int bl = __builtin_ctzll(b);
+              b &= b - 1;
+              const float l2 = __builtin_bit_cast(
+                  float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lv[s2]), bl));
+              rank += (l2 > lm) | ((l2 == lm) & (64 * s2 + bl < m));
+            }
+          }
+          const bool keep = ((em[s] >> lane) & 1ull) && rank < a.k;
+          kc += __popcll(__ballot(keep));
+          rnk[c * MP + m] = keep ? (int16_t)rank : (int16_t)-1;
         }
-        const bool keep = lm > NEG_INF && rank < a.k && gpar + lm >= vB;
-        kc += __popcll(__ballot(keep));
-        rnk[c * MP + m] = keep ? (int16_t)rank : (int16_t)-1;
+      } else {
+        wave_sync();
+        const float4 *e4 = reinterpret_cast<const float4 *>(ell + c * MP);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          if (s >= MP / 64) break;
+          const int m = lane + 64 * s;
+          const float lm = lv[s];
+          // rank = slots ahead of m by (log-prob desc, slot asc); slots >= M hold -inf
+          int rank = 0;
+#pragma unroll 4
+          for (int q = 0; q < MP / 4; ++q) {
+            const float4 v = e4[q];
+            const int m2 = 4 * q;
+            rank += (v.x > lm) | ((v.x == lm) & (m2 < m));
+            rank += (v.y > lm) | ((v.y == lm) & (m2 + 1 < m));
+            rank += (v.z > lm) | ((v.z == lm) & (m2 + 2 < m));
+            rank += (v.w > lm) | ((v.w == lm) & (m2 + 3 < m));
+          }
+          const bool keep = ((em[s] >> lane) & 1ull) && rank < a.k;
+          kc += __popcll(__ballot(keep));
+          rnk[c * MP + m] = keep ? (int16_t)rank : (int16_t)-1;
+        }
       }
       if (lane == 0) wcnt[c] = kc;
     };
