@@ -176,7 +176,7 @@ __host__ __device__ inline int merge_buf_bytes(int nlists, int M) { return merge
 // DEV_SCOPE selects device-scope stores (results read by other workgroups).
 // vadd (nullable): candv[m] = logit + vadd[cand[m]] instead of the logit.
 template <int NT, bool DEV_SCOPE>
-__device__ void merge_row(const uint64_t *lists, int nlists, int M, const float2 *tails,
+__device__ __attribute__((always_inline)) void merge_row(const uint64_t *lists, int nlists, int M, const float2 *tails,
                           const int32_t *flags, float c, float inv_tau, uint64_t *buf,
                           float2 *red, int *flag_lds, int32_t *cand, float *candv, float *tailR,
                           int32_t *rflag, const float *vadd) {
