@@ -733,11 +733,16 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
               xn = pr[2 * UW];
               xb = bhn[u];
             } else {
-              const float *pr = a.P_all + (size_t)ntok[nd] * (3 * dh) + j;
-              xr = pr[0];
-              xz = pr[dh];
-              xn = pr[2 * dh];
-              xb = a.b_hh[2 * dh + j];
+              // buffer loads: a pointer shared with the LDS branch would make
+              // both flat accesses
+              const __amdgpu_buffer_rsrc_t rpr = __builtin_amdgcn_make_buffer_rsrc(
+                  const_cast<float *>(a.P_all + (size_t)ntok[nd] * (3 * dh)), 0, 0x7FFFFFF0, 0x00020000);
+              const __amdgpu_buffer_rsrc_t rbh =
+                  __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.b_hh), 0, 0x7FFFFFF0, 0x00020000);
+              xr = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rpr, j * 4, 0, 0));
+              xz = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rpr, (dh + j) * 4, 0, 0));
+              xn = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rpr, (2 * dh + j) * 4, 0, 0));
+              xb = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rbh, (2 * dh + j) * 4, 0, 0));
             }
             const float r = sigmoid_fast(xr + gs[0]);
             const float z = sigmoid_fast(xz + gs[1]);

@@ -63,24 +63,27 @@ __device__ inline float wave_reduce(float v, Op op) {
   v = op(v, dpp_f<0x140>(v));  // row_mirror
   return op(op(readlane_f(v, 0), readlane_f(v, 16)), op(readlane_f(v, 32), readlane_f(v, 48)));
 }
-// block-wide tail reduction in a fixed order (deterministic); red: NT/64 float2
+// block-wide tail reduction in a fixed order (deterministic); red: NT/64 float2.
+// The block max first, then every sum rescaled to it once and added up.
 template <int NT>
 __device__ inline Tail block_tail(Tail t, float c, float2 *red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  t = tail_merge(t, Tail{dpp_f<0xB1>(t.m), dpp_f<0xB1>(t.s)}, c);
-  t = tail_merge(t, Tail{dpp_f<0x4E>(t.m), dpp_f<0x4E>(t.s)}, c);
-  t = tail_merge(t, Tail{dpp_f<0x141>(t.m), dpp_f<0x141>(t.s)}, c);
-  t = tail_merge(t, Tail{dpp_f<0x140>(t.m), dpp_f<0x140>(t.s)}, c);
-  Tail r{readlane_f(t.m, 0), readlane_f(t.s, 0)};
-  r = tail_merge(r, Tail{readlane_f(t.m, 16), readlane_f(t.s, 16)}, c);
-  r = tail_merge(r, Tail{readlane_f(t.m, 32), readlane_f(t.s, 32)}, c);
-  r = tail_merge(r, Tail{readlane_f(t.m, 48), readlane_f(t.s, 48)}, c);
-  if (lane == 0) red[w] = make_float2(r.m, r.s);
+  (void)lane;
+  const float wm = wave_reduce(t.m, [](float x, float y) { return fmaxf(x, y); });
+  if ((threadIdx.x & 63) == 0) red[w].x = wm;
   __syncthreads();
-  Tail b{red[0].x, red[0].y};
-  for (int i = 1; i < NT / 64; ++i) b = tail_merge(b, Tail{red[i].x, red[i].y}, c);
+  float m = red[0].x;
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) m = fmaxf(m, red[i].x);
+  const float s = wave_reduce(t.s > 0.0f ? t.s * fast_exp2((t.m - m) * c) : 0.0f,
+                              [](float x, float y) { return x + y; });
+  if ((threadIdx.x & 63) == 0) red[w].y = s;
   __syncthreads();
-  return b;
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) sum += red[i].y;
+  __syncthreads();
+  return Tail{m, sum};
 }
 
 // descending bitonic sort of a wave's 64 values (one per lane)
@@ -249,6 +252,7 @@ __device__ __attribute__((always_inline)) void merge_row(const uint64_t *lists, 
       const int j1 = j0 + per < np ? j0 + per : np;
       const uint64_t k = heads[h];
       int r = 0;
+#pragma unroll 4
       for (int j = j0; j < j1; ++j) {
         const ulonglong2 v = h2[j];
         r += (v.x > k) + (v.y > k);
@@ -295,6 +299,7 @@ __device__ __attribute__((always_inline)) void merge_row(const uint64_t *lists, 
       const int j1 = j0 + per < np ? j0 + per : np;
       const uint64_t k = skeys[sv];
       int r = 0;
+#pragma unroll 4
       for (int j = j0; j < j1; ++j) {
         const ulonglong2 kk = s2[j];
         r += (kk.x > k) + (kk.y > k);
