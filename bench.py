@@ -9,9 +9,9 @@ B=16, T=1, d_e=4096, d_h=512).  Logit buffers rotate through >= 512 MB so the
 
 The K timed calls are captured into one HIP graph and timed as one replay
 (--eager: launched one by one); the same K calls also run eagerly first, which
-gives the per-call GPU times and the stage durations (HIP events the library
-records between its kernels on the launch stream, every 8th call), and the
-graph's output is checked against theirs.
+gives the per-call GPU times and the stage durations (every 8th call launches
+its two kernels with start and end events, so a stage is one kernel's execution
+time), and the graph's output is checked against theirs.
 
 Prints ONE JSON line: trees/s for the whole job, the per-kernel roofline of the
 dominant kernel and the CPU oracle timed on a bounded sample.
@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILES = os.path.join(ROOT, "profiles")
-PROFILE_EVERY = 8   # stage events on every 8th timed call (each event costs a few us)
+PROFILE_EVERY = 8   # kernel start/end events on every 8th eager call
 
 
 def parse():

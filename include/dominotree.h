@@ -174,9 +174,10 @@ dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, c
 void dt_plan_destroy(dt_plan *plan);
 
 /* Stage timing (measurement aid).  With every = n > 0, every n-th dt_build_tree
- * call (the first one included) records a HIP event on its stream before its
- * first kernel and after each kernel: stage 0 = top-M scan of the logits
- * (kernel 1), 1 = per-row merge, expansion and emission (kernel 2).  every = 0
+ * call (the first one included) launches its two kernels with HIP events taken
+ * at each kernel's start and end (hipExtLaunchKernel), so a stage is one
+ * kernel's execution time: stage 0 = top-M scan of the logits (kernel 1),
+ * 1 = per-row merge, expansion and emission (kernel 2).  every = 0
  * turns it off; enabling (again) starts a new count.  Calls made while the
  * stream is being captured into a HIP graph record no events and do not count.
  * dt_plan_stage_ms waits for the last profiled call and writes the mean stage

@@ -182,9 +182,9 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
 dt_status dt_plan_set_profiling(dt_plan *p, int enable) {
   if (!p) return fail(DT_ERR_NULL, "plan is required");
   if (enable && !p->ev) {
-    p->ev = new (std::nothrow) hipEvent_t[3 * dt::kProfSlots]();
+    p->ev = new (std::nothrow) hipEvent_t[4 * dt::kProfSlots]();
     if (!p->ev) return fail(DT_ERR_HIP, "host allocation failed");
-    for (int i = 0; i < 3 * dt::kProfSlots; ++i) {
+    for (int i = 0; i < 4 * dt::kProfSlots; ++i) {
       hipError_t e = hipEventCreate(&p->ev[i]);
       if (e != hipSuccess) return hip_fail(e, "event create");
     }
@@ -201,12 +201,12 @@ dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
     return fail(DT_ERR_SHAPE, "no profiled dt_build_tree call yet");
   const int n = p->profiled_calls < dt::kProfSlots ? p->profiled_calls : dt::kProfSlots;
   const int last = (p->profiled_calls - 1) % dt::kProfSlots;
-  hipError_t e = hipEventSynchronize(p->ev[3 * last + 2]);
+  hipError_t e = hipEventSynchronize(p->ev[4 * last + 3]);
   double sum[2] = {0.0, 0.0};
   for (int c = 0; c < n && e == hipSuccess; ++c)
     for (int i = 0; i < 2 && e == hipSuccess; ++i) {
       float t = 0.0f;
-      e = hipEventElapsedTime(&t, p->ev[3 * c + i], p->ev[3 * c + i + 1]);
+      e = hipEventElapsedTime(&t, p->ev[4 * c + 2 * i], p->ev[4 * c + 2 * i + 1]);
       sum[i] += t;
     }
   if (e != hipSuccess) return hip_fail(e, "event timing");
@@ -217,7 +217,7 @@ dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
 void dt_plan_destroy(dt_plan *p) {
   if (!p) return;
   if (p->ev) {
-    for (int i = 0; i < 3 * dt::kProfSlots; ++i)
+    for (int i = 0; i < 4 * dt::kProfSlots; ++i)
       if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
     delete[] p->ev;
   }
@@ -270,20 +270,17 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
     if (ce != hipSuccess) return hip_fail(ce, "stream capture query");
     if (cs == hipStreamCaptureStatusNone) prof = (plan->calls_since++ % plan->profiling) == 0;
   }
-  hipEvent_t *ev = prof ? plan->ev + 3 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
-  hipError_t e = prof ? hipEventRecord(ev[0], s) : hipSuccess;
+  // profiled calls time each kernel from its start to its end
+  hipEvent_t *ev = prof ? plan->ev + 4 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
   // the scan kernel also clears the expansion kernel's barrier counters
-  if (e == hipSuccess)
-    e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, (batch + 2) * dt::kBarStride, s);
+  hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar,
+                                        (batch + 2) * dt::kBarStride, s, prof ? ev[0] : nullptr,
+                                        prof ? ev[1] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
-  if (prof) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s);
+  e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s, prof ? ev[2] : nullptr,
+                        prof ? ev[3] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
-  if (prof) {
-    e = hipEventRecord(ev[2], s);
-    if (e != hipSuccess) return hip_fail(e, "event record");
-    plan->profiled_calls++;
-  }
+  if (prof) plan->profiled_calls++;
   return DT_OK;
 }
 

@@ -31,6 +31,7 @@
 // of a group are placed on one XCD (blocks are dealt to XCDs round-robin).
 // Member 0 replays the heap and emits the tree.
 #include "dt_select.h"
+#include <hip/hip_ext.h>
 
 namespace dt {
 
@@ -1296,7 +1297,8 @@ size_t expand_part_bytes(const dt_plan *p, int batch) {
 }
 
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
-                         const Workspace &ws, const dt_tree *out, hipStream_t s) {
+                         const Workspace &ws, const dt_tree *out, hipStream_t s, hipEvent_t t0,
+                         hipEvent_t t1) {
   ExpArgs a;
   const ScanGeom g = scan_geom(batch * p->L, p->V, p->M);
   a.L = p->L;
@@ -1340,10 +1342,16 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   // every member is resident on an otherwise idle device; members take their
   // slots in start order and every wait is bounded (DT_TREE_TIMEOUT).
   const int grid = a.G > 1 ? 8 * a.G * ((batch + 7) / 8) : batch;
-  if (p->wdt == DT_BF16)
+  if (t0) {
+    if (p->wdt == DT_BF16)
+      hipExtLaunchKernelGGL(expand_kernel<uint16_t>, dim3(grid), dim3(NT), lds, s, t0, t1, 0, a);
+    else
+      hipExtLaunchKernelGGL(expand_kernel<float>, dim3(grid), dim3(NT), lds, s, t0, t1, 0, a);
+  } else if (p->wdt == DT_BF16) {
     hipLaunchKernelGGL(expand_kernel<uint16_t>, dim3(grid), dim3(NT), lds, s, a);
-  else
+  } else {
     hipLaunchKernelGGL(expand_kernel<float>, dim3(grid), dim3(NT), lds, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -97,7 +97,7 @@ struct dt_plan {
   int profiling;            // > 0: record stage events on every profiling-th dt_build_tree call
   int calls_since;          // dt_build_tree calls since profiling was enabled
   int profiled_calls;       // calls recorded since profiling was enabled
-  hipEvent_t *ev;           // [kProfSlots][3] stage boundaries, one slot per call (ring)
+  hipEvent_t *ev;           // [kProfSlots][4] start and end of both kernels, one slot per call (ring)
 };
 
 namespace dt {
@@ -127,12 +127,16 @@ size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws);
 Workspace carve(const dt_plan *p, int batch, char *base);
 
 // kernel launchers (return hipError_t of the launch)
+// kernel launchers; with t0/t1 the launch records HIP events at the kernel's
+// start and end (hipExtLaunchKernel), used for stage timing
 hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
-                              const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s);
+                              const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s,
+                              hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s);
 hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
-                         const Workspace &ws, const dt_tree *out, hipStream_t s);
+                         const Workspace &ws, const dt_tree *out, hipStream_t s,
+                         hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 int expand_group_size(int d_h, int num_cus, int batch);
 size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L);
 size_t expand_part_bytes(const dt_plan *p, int batch);

@@ -22,6 +22,7 @@
 // it runs inside the expansion kernel, or in a small kernel of its own for
 // dt_scan_topm.
 #include "dt_select.h"
+#include <hip/hip_ext.h>
 
 namespace dt {
 
@@ -670,26 +671,37 @@ size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws) {
   return o;
 }
 
+// hipLaunchKernelGGL, or hipExtLaunchKernelGGL with start and end events
+template <typename F, typename... Args>
+static void launch_maybe_timed(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t s,
+                               hipEvent_t t0, hipEvent_t t1, Args... args) {
+  if (t0)
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, s, t0, t1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+}
+
 hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
-                              const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s) {
+                              const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s,
+                              hipEvent_t t0, hipEvent_t t1) {
   const float c = 1.4426950408889634f * inv_tau;  // exp(x / tau) = exp2(x * c)
   dim3 grid(g.nchunks, g.rows);
   const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16) == 0;
   if (ldt == DT_BF16) {
     const uint16_t *p = static_cast<const uint16_t *>(logits);
     if (aligned && g.V % 8 == 0)
-      hipLaunchKernelGGL((scan_chunk_kernel<uint16_t, true>), grid, dim3(kScanThreads), 0, s, p, g,
+      launch_maybe_timed(scan_chunk_kernel<uint16_t, true>, grid, dim3(kScanThreads), 0, s, t0, t1, p, g,
                          c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
     else
-      hipLaunchKernelGGL((scan_chunk_kernel<uint16_t, false>), grid, dim3(kScanThreads), 0, s, p,
+      launch_maybe_timed(scan_chunk_kernel<uint16_t, false>, grid, dim3(kScanThreads), 0, s, t0, t1, p,
                          g, c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
   } else {
     const float *p = static_cast<const float *>(logits);
     if (aligned && g.V % 4 == 0)
-      hipLaunchKernelGGL((scan_chunk_kernel<float, true>), grid, dim3(kScanThreads), 0, s, p, g, c,
+      launch_maybe_timed(scan_chunk_kernel<float, true>, grid, dim3(kScanThreads), 0, s, t0, t1, p, g, c,
                          ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
     else
-      hipLaunchKernelGGL((scan_chunk_kernel<float, false>), grid, dim3(kScanThreads), 0, s, p, g,
+      launch_maybe_timed(scan_chunk_kernel<float, false>, grid, dim3(kScanThreads), 0, s, t0, t1, p, g,
                          c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
   }
   return hipGetLastError();
