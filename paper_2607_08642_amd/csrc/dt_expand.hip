@@ -177,26 +177,37 @@ __device__ inline __amdgpu_buffer_rsrc_t dev_rsrc(const void *base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7FFFFFF0, 0x00020000);
 }
 constexpr int kSc1 = 16;  // cache-policy bit: device scope
-__device__ inline float4 ld_dev16(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kSc1));
+__device__ inline float4 ld_dev16(__amdgpu_buffer_rsrc_t r, int byte_off, int sgpr_off = 0) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, sgpr_off, kSc1));
 }
 __device__ inline float ld_dev4(__amdgpu_buffer_rsrc_t r, int byte_off, int sgpr_off = 0) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, sgpr_off, kSc1));
 }
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// the G (<= 16) partial corrections of one slot
+// Partial corrections of 64 slots from up to 16 members, four 16-byte loads
+// per lane: lane (q = lane % 16, r = lane / 16) holds slots 4q .. 4q+3 of
+// members r, r+4, r+8, r+12 (zeros for members >= G).
 struct Parts {
-  float4 q[4];
+  float4 v[4];
 };
-__device__ inline float part_at(const Parts &p, int j) {
-  const float4 v = p.q[j >> 2];
-  switch (j & 3) {
-    case 0: return v.x;
-    case 1: return v.y;
-    case 2: return v.z;
-    default: return v.w;
-  }
+__device__ inline float lane_pull(float v, int src_lane) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_ds_bpermute(src_lane * 4, __builtin_bit_cast(int, v)));
+}
+// The sum of the G parts of slot `lane`, bit-identical in every member: each
+// lane adds its members in the order r, r+4, r+8, r+12; lane groups {r, r^2}
+// then {r, r^1} combine (each slot's sum is formed in one lane, slot 4q + r
+// in lane (q, r)), and lane l finally takes slot l.
+__device__ inline float sum_parts(const Parts &p, int lane) {
+  const float4 t = ((p.v[0] + p.v[1]) + p.v[2]) + p.v[3];
+  const bool hi = lane >= 32, odd = (lane >> 4) & 1;
+  // r, r^2: the low pair keeps slots 4q, 4q+1, the high pair 4q+2, 4q+3
+  const float h0 = (hi ? t.z : t.x) + lane_pull(hi ? t.x : t.z, lane ^ 32);
+  const float h1 = (hi ? t.w : t.y) + lane_pull(hi ? t.y : t.w, lane ^ 32);
+  // r, r^1: lane r keeps slot 4q + r
+  const float tot = (odd ? h1 : h0) + lane_pull(odd ? h0 : h1, lane ^ 16);
+  return lane_pull(tot, (lane >> 2) + 16 * (lane & 3));
 }
 
 // GRU inputs of 4 consecutive hidden units j0..j0+3 of one node: P of gates
@@ -392,8 +403,14 @@ struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per 
   }
 };
 
-template <typename TW>
+// SDH, SG, SM, SL > 0 fix d_h, G, M and L at compile time (the LDS layout and
+// every loop bound over them become constants); 0 takes them from the arguments.
+template <typename TW, int SDH, int SG, int SM, int SL>
 __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
+  if constexpr (SDH > 0) a.dh = SDH;
+  if constexpr (SG > 0) a.G = SG;
+  if constexpr (SM > 0) a.M = SM;
+  if constexpr (SL > 0) a.L = SL;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const Lds ly = lds_layout(a.dh, a.G, a.M, a.nchunks, a.L);
   float *ng = reinterpret_cast<float *>(smem + ly.ng);
@@ -794,17 +811,15 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     pb ^= 1;
     // the G parts of a slot, one from each member's block: all loads are
     // issued, then summed in member order
-    auto load_parts = [&](int c, int m) -> Parts {
+    auto load_parts = [&](int c, int s) -> Parts {
       Parts p;
-      const int off = (c * MP + m) * 4, stride = CH * MP * 4;
+      const int r = lane >> 4, stride = CH * MP * 4;
+      const int off = (c * MP + 64 * s + 4 * (lane & 15)) * 4 + r * stride;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        p.q[q4] = make_float4(0.f, 0.f, 0.f, 0.f);
-        // (the member stride goes in the scalar offset)
-        if (4 * q4 + 0 < G) p.q[q4].x = ld_dev4(rp, off, (4 * q4 + 0) * stride);
-        if (4 * q4 + 1 < G) p.q[q4].y = ld_dev4(rp, off, (4 * q4 + 1) * stride);
-        if (4 * q4 + 2 < G) p.q[q4].z = ld_dev4(rp, off, (4 * q4 + 2) * stride);
-        if (4 * q4 + 3 < G) p.q[q4].w = ld_dev4(rp, off, (4 * q4 + 3) * stride);
+      for (int i = 0; i < 4; ++i) {
+        p.v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        // (the stride of four members goes in the scalar offset)
+        if (4 * i + r < G) p.v[i] = ld_dev16(rp, off, 4 * i * stride);
       }
       return p;
     };
@@ -816,13 +831,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       for (int s = 0; s < 4; ++s) {
         if (s >= MP / 64) break;
         const int m = lane + 64 * s;
-        const Parts p = s == 0 ? p0 : load_parts(c, m);
+        const Parts p = s == 0 ? p0 : load_parts(c, s);
         // x already holds logit + E[v] . b_c (added by the row merge)
         const float x = ccandv[m];
-        float dl = x;
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (j < G) dl += part_at(p, j);
+        const float dl = x + sum_parts(p, lane);
         const float z = x > NEG_INF ? dl * a.inv_tau : NEG_INF;  // slots >= M hold -inf
         zv[s] = z;
         mx = fmaxf(mx, z);
@@ -910,8 +922,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // two nodes per wave: the second node's loads are in flight during the first
     const int c0 = wave, c1 = wave + NW;
     Parts p0, p1;
-    if (c0 < nc) p0 = load_parts(c0, lane);
-    if (c1 < nc) p1 = load_parts(c1, lane);
+    if (c0 < nc) p0 = load_parts(c0, 0);
+    if (c1 < nc) p1 = load_parts(c1, 0);
     if (c0 < nc)
       node_children(c0, p0);
     else if (lane == 0)
@@ -1334,24 +1346,29 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.bar = ws.bar;
   a.out = *out;
   const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks, p->L);
-  const void *fn = p->wdt == DT_BF16 ? (const void *)expand_kernel<uint16_t>
-                                     : (const void *)expand_kernel<float>;
+  // shapes with a compiled specialisation: Qwen3 drafters (d_h = 512, M = 64,
+  // L = 16) with bf16 weights at G = 16 (one to eight trees) and G = 8
+  const void *fn;
+  if (p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16 && a.G == 16)
+    fn = (const void *)expand_kernel<uint16_t, 512, 16, 64, 16>;
+  else if (p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16 && a.G == 8)
+    fn = (const void *)expand_kernel<uint16_t, 512, 8, 64, 16>;
+  else if (p->wdt == DT_BF16)
+    fn = (const void *)expand_kernel<uint16_t, 0, 0, 0, 0>;
+  else
+    fn = (const void *)expand_kernel<float, 0, 0, 0, 0>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   // G > 1: the grid is at most one workgroup per CU (expand_group_size), so
   // every member is resident on an otherwise idle device; members take their
   // slots in start order and every wait is bounded (DT_TREE_TIMEOUT).
   const int grid = a.G > 1 ? 8 * a.G * ((batch + 7) / 8) : batch;
-  if (t0) {
-    if (p->wdt == DT_BF16)
-      hipExtLaunchKernelGGL(expand_kernel<uint16_t>, dim3(grid), dim3(NT), lds, s, t0, t1, 0, a);
-    else
-      hipExtLaunchKernelGGL(expand_kernel<float>, dim3(grid), dim3(NT), lds, s, t0, t1, 0, a);
-  } else if (p->wdt == DT_BF16) {
-    hipLaunchKernelGGL(expand_kernel<uint16_t>, dim3(grid), dim3(NT), lds, s, a);
-  } else {
-    hipLaunchKernelGGL(expand_kernel<float>, dim3(grid), dim3(NT), lds, s, a);
-  }
+  void *args[] = {&a};
+  if (t0)
+    e = hipExtLaunchKernel(fn, dim3(grid), dim3(NT), args, lds, s, t0, t1, 0);
+  else
+    e = hipLaunchKernel(fn, dim3(grid), dim3(NT), args, lds, s);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 
