@@ -138,7 +138,8 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
   l.Sn = take(CH * UW * 4);
   l.ell = take(CH * MP * 4);
   l.rnk = take(CH * MP * 2);
-  const int sortb = sel::merge_buf_bytes(nchunks, M);  // merge_row's buffer
+  // merge_row's buffer, or merge_row_tree's (NT keys)
+  const int sortb = sel::merge_buf_bytes(nchunks, M) > NT * 8 ? sel::merge_buf_bytes(nchunks, M) : NT * 8;
   l.sortbuf = reuse;
   if (reuse + sortb > o) o = reuse + sortb;
   l.total = o;
@@ -499,13 +500,33 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 #pragma unroll
   for (int q = 0; q < 2; ++q)
     if (a.h0 && tid + q * NT < UW) h0v[q] = a.h0[(size_t)t * dh + member * UW + tid + q * NT];
-  for (int d = member; d < L; d += G) {
-    const int row = t * L + d;
-    sel::merge_row<NT, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
-                             a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
-                             a.c2, a.inv_tau, sortbuf, red, &scal[S_MERGEFLAG],
-                             a.cand + (size_t)row * M, a.candv + (size_t)row * M, a.tailR + row,
-                             a.rflag + row, a.c_all);
+  if (sel::wave_merge_fits(a.nchunks, M) && a.nchunks > 2) {
+    // all waves on each of this member's rows
+    for (int d = member; d < L; d += G) {
+      const int row = t * L + d;
+      sel::merge_row_tree<true, NT>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+                                    a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
+                                    a.c2, a.inv_tau, sortbuf, red, a.cand + (size_t)row * M,
+                                    a.candv + (size_t)row * M, a.tailR + row, a.rflag + row, a.c_all);
+    }
+  } else if (sel::wave_merge_fits(a.nchunks, M)) {
+    // one wave per row (a single merge): rows member + G * (wave + NW * i)
+    for (int d = member + G * wave; d < L; d += G * NW) {
+      const int row = t * L + d;
+      sel::merge_row_wave<true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+                                a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
+                                a.c2, a.inv_tau, a.cand + (size_t)row * M, a.candv + (size_t)row * M,
+                                a.tailR + row, a.rflag + row, a.c_all);
+    }
+  } else {
+    for (int d = member; d < L; d += G) {
+      const int row = t * L + d;
+      sel::merge_row<NT, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+                               a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
+                               a.c2, a.inv_tau, sortbuf, red, &scal[S_MERGEFLAG],
+                               a.cand + (size_t)row * M, a.candv + (size_t)row * M, a.tailR + row,
+                               a.rflag + row, a.c_all);
+    }
   }
   {
     // the root's path state (h0 or zeros) in slot ecap-1: this member's units

@@ -367,5 +367,195 @@ __device__ __attribute__((always_inline)) void merge_row(const uint64_t *lists, 
   __syncthreads();
 }
 
+// ---------------------------------------------------------------------------
+// One wave merges a row's segment lists when M <= 64 and there are at most 16
+// lists: lane p holds position p of every list, and pairs of lists combine in
+// a tree.  Of a descending list A and an ascending list B, max(A[i], B[i]) is
+// the better half of A and B as a bitonic sequence (six compare-exchange
+// stages sort it) and min(A[i], B[i]) the worse half, which joins the lane's
+// tail right away: every key not among the row's M best is added to exactly
+// one lane's tail, in an order fixed by the tree.  No LDS and no barrier.
+
+// a 64-bit value from lane ^ J (DPP inside rows of 16 lanes, swizzle across
+// rows, permute across halves); the whole wave must be active
+template <int J>
+__device__ inline uint64_t lane_xor64(uint64_t v) {
+  const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+  int plo, phi;
+  if constexpr (J == 1 || J == 2 || J == 8) {
+    // quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_ror:8
+    constexpr int ctrl = J == 1 ? 0xB1 : (J == 2 ? 0x4E : 0x128);
+    plo = __builtin_amdgcn_update_dpp(0, lo, ctrl, 0xF, 0xF, false);
+    phi = __builtin_amdgcn_update_dpp(0, hi, ctrl, 0xF, 0xF, false);
+  } else if constexpr (J == 4) {
+    // row_shl:4 (from lane + 4) where bit 2 is clear, row_shr:4 (lane - 4) where set
+    const bool up = (threadIdx.x & 4) != 0;
+    const int lo_a = __builtin_amdgcn_update_dpp(0, lo, 0x104, 0xF, 0xF, false);
+    const int lo_b = __builtin_amdgcn_update_dpp(0, lo, 0x114, 0xF, 0xF, false);
+    const int hi_a = __builtin_amdgcn_update_dpp(0, hi, 0x104, 0xF, 0xF, false);
+    const int hi_b = __builtin_amdgcn_update_dpp(0, hi, 0x114, 0xF, 0xF, false);
+    plo = up ? lo_b : lo_a;
+    phi = up ? hi_b : hi_a;
+  } else if constexpr (J == 16) {
+    // swizzle bit mode inside 32 lanes: and 0x1F, or 0, xor 0x10
+    plo = __builtin_amdgcn_ds_swizzle(lo, 0x401F);
+    phi = __builtin_amdgcn_ds_swizzle(hi, 0x401F);
+  } else {
+    static_assert(J == 32, "lane distance");
+    const int a = (int)((threadIdx.x & 63) ^ 32) * 4;
+    plo = __builtin_amdgcn_ds_bpermute(a, lo);
+    phi = __builtin_amdgcn_ds_bpermute(a, hi);
+  }
+  return ((uint64_t)(uint32_t)phi << 32) | (uint32_t)plo;
+}
+
+template <int J>
+__device__ inline uint64_t cx_stage(uint64_t v, bool desc) {
+  const uint64_t p = lane_xor64<J>(v);
+  const bool keep_max = ((threadIdx.x & J) == 0) == desc;
+  return ((p > v) == keep_max) ? p : v;  // (equal keys are both empty)
+}
+
+// sorts a bitonic sequence of 64 keys (one per lane), descending or ascending
+__device__ inline uint64_t bitonic_clean64(uint64_t v, bool desc) {
+  v = cx_stage<32>(v, desc);
+  v = cx_stage<16>(v, desc);
+  v = cx_stage<8>(v, desc);
+  v = cx_stage<4>(v, desc);
+  v = cx_stage<2>(v, desc);
+  return cx_stage<1>(v, desc);
+}
+
+// the better half of a descending list a and an ascending list b, sorted in
+// direction desc; the worse half joins the lane's tail (empty slots add nothing)
+__device__ inline uint64_t merge_halves(uint64_t a, uint64_t b, bool desc, Tail &t, float c) {
+  const bool ga = a > b;
+  const uint64_t hi = ga ? a : b, lo = ga ? b : a;
+  tail_add1(t, lo ? key_value(lo) : -3.402823466e38f, c);
+  return bitonic_clean64(hi, desc);
+}
+
+constexpr int kWaveMergeLists = 16;
+
+__host__ __device__ inline bool wave_merge_fits(int nlists, int M) {
+  return M <= 64 && nlists <= kWaveMergeLists;
+}
+
+// The same results as merge_row (the row's M best keys, R over the rest, the
+// row flag), computed by the calling wave alone; wave_merge_fits must hold.
+template <bool DEV_SCOPE>
+__device__ __attribute__((always_inline)) void merge_row_wave(
+    const uint64_t *lists, int nlists, int M, const float2 *tails, const int32_t *flags, float c,
+    float inv_tau, int32_t *cand, float *candv, float *tailR, int32_t *rflag, const float *vadd) {
+  constexpr int NL = kWaveMergeLists;
+  const int lane = threadIdx.x & 63;
+  // lists at even positions of the tree descending, odd ones reversed (ascending)
+  uint64_t k[NL];
+#pragma unroll
+  for (int j = 0; j < NL; ++j) {
+    const int pos = (j & 1) ? 63 - lane : lane;
+    k[j] = (j < nlists && pos < M) ? lists[j * M + pos] : 0ull;
+  }
+  Tail t = tail_empty();
+  int bad = 0;
+  if (lane < nlists) {
+    const float2 tl = tails[lane];
+    t = Tail{tl.x, tl.y};
+    bad = flags[lane];
+  }
+  // level s: k[j] (j a multiple of 2s) takes the best 64 of lists j .. j+2s-1,
+  // descending when it is the left operand of the next level, else ascending
+#pragma unroll
+  for (int s = 1; s < NL; s <<= 1) {
+#pragma unroll
+    for (int j = 0; j < NL; j += 2 * s) {
+      if (j >= nlists) break;
+      const bool desc = ((j / (2 * s)) & 1) == 0;
+      if (j + s < nlists) {
+        k[j] = merge_halves(k[j], k[j + s], desc, t, c);
+      } else if (!desc) {
+        k[j] = bitonic_clean64(k[j], false);  // a lone list, now the right operand
+      }
+    }
+  }
+  const uint64_t top = k[0];
+  const bool keep = lane < M && top != 0ull;
+  if (lane >= M && top) tail_add1(t, key_value(top), c);
+  const float va = (keep && vadd) ? vadd[key_index(top)] : 0.0f;
+  // the tail: the wave's max, then every lane's sum rescaled to it once
+  const float m = wave_reduce(t.m, [](float x, float y) { return fmaxf(x, y); });
+  const float sum = wave_reduce(t.s > 0.0f ? t.s * fast_exp2((t.m - m) * c) : 0.0f,
+                                [](float x, float y) { return x + y; });
+  const bool any_bad = __ballot(bad != 0) != 0ull;
+  if (lane < M) {
+    put<DEV_SCOPE>(cand + lane, keep ? (int32_t)key_index(top) : (int32_t)-1);
+    put<DEV_SCOPE>(candv + lane, keep ? key_value(top) + va : -__builtin_huge_valf());
+  }
+  if (lane == 0) {
+    put<DEV_SCOPE>(tailR, sum > 0.0f ? m * inv_tau + logf(sum) : -__builtin_huge_valf());
+    put<DEV_SCOPE>(rflag, (int32_t)(any_bad ? DT_TREE_NONFINITE : 0));
+  }
+}
+
+// The same merge spread over the NT / 64 waves of a workgroup (every thread
+// calls it): wave w merges lists 2w and 2w + 1, then the tree's levels meet in
+// LDS (xbuf: NT keys), one barrier each; the tails combine as in block_tail.
+template <bool DEV_SCOPE, int NT>
+__device__ __attribute__((always_inline)) void merge_row_tree(
+    const uint64_t *lists, int nlists, int M, const float2 *tails, const int32_t *flags, float c,
+    float inv_tau, uint64_t *xbuf, float2 *red, int32_t *cand, float *candv, float *tailR,
+    int32_t *rflag, const float *vadd) {
+  constexpr int W = NT / 64;
+  static_assert(2 * W >= kWaveMergeLists, "two lists per wave");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = 2 * wave;  // this wave's first list; the tree as in merge_row_wave
+  Tail t = tail_empty();
+  int bad = 0;
+  if (wave == 0 && lane < nlists) {
+    const float2 tl = tails[lane];
+    t = Tail{tl.x, tl.y};
+    bad = flags[lane];
+  }
+  uint64_t v = 0ull;
+  if (j < nlists) {
+    const uint64_t a = lane < M ? lists[j * M + lane] : 0ull;
+    const bool desc = (wave & 1) == 0;
+    if (j + 1 < nlists) {
+      const uint64_t b = 63 - lane < M ? lists[(j + 1) * M + 63 - lane] : 0ull;
+      v = merge_halves(a, b, desc, t, c);
+    } else {
+      v = desc ? a : bitonic_clean64(a, false);
+    }
+  }
+#pragma unroll
+  for (int s = 2; s < 2 * W; s <<= 1) {
+    // right operands publish; a slot read at this level is never written at the next
+    if (j < nlists && (j % (2 * s)) == s) xbuf[wave * 64 + lane] = v;
+    __syncthreads();
+    if (j < nlists && (j % (2 * s)) == 0) {
+      const bool desc = ((j / (2 * s)) & 1) == 0;
+      if (j + s < nlists)
+        v = merge_halves(v, xbuf[(wave + s / 2) * 64 + lane], desc, t, c);
+      else if (!desc)
+        v = bitonic_clean64(v, false);
+    }
+  }
+  const bool keep = wave == 0 && lane < M && v != 0ull;
+  if (wave == 0 && lane >= M && v) tail_add1(t, key_value(v), c);
+  const float va = (keep && vadd) ? vadd[key_index(v)] : 0.0f;
+  const bool any_bad = __ballot(bad != 0) != 0ull;  // (wave 0 holds the flags)
+  t = block_tail<NT>(t, c, red);
+  if (wave == 0) {
+    if (lane < M) {
+      put<DEV_SCOPE>(cand + lane, keep ? (int32_t)key_index(v) : (int32_t)-1);
+      put<DEV_SCOPE>(candv + lane, keep ? key_value(v) + va : -__builtin_huge_valf());
+    }
+    if (lane == 0) {
+      put<DEV_SCOPE>(tailR, t.s > 0.0f ? t.m * inv_tau + logf(t.s) : -__builtin_huge_valf());
+      put<DEV_SCOPE>(rflag, (int32_t)(any_bad ? DT_TREE_NONFINITE : 0));
+    }
+  }
+}
+
 }  // namespace sel
 }  // namespace dt
