@@ -128,20 +128,6 @@ __device__ inline float to_f32<float>(float x) {
   return x;
 }
 
-// inclusive prefix sum over a wave: shifted adds inside rows of 16 lanes (DPP
-// row_shr 1, 2, 4, 8), then the totals of the rows below
-__device__ inline int wave_incl_scan(int x) {
-  const int lane = threadIdx.x & 63;
-  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);
-  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);
-  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);
-  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);
-  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
-  const int r2 = __builtin_amdgcn_readlane(x, 47);
-  const int row = lane >> 4;
-  return x + (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
-}
-
 // Raw registers of one batch: kScanPerThread elements per thread as 16-byte loads
 template <typename T>
 struct Raw {
@@ -289,27 +275,41 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) nc += wc[i];
     if (nc == 0) return;
-    // the regions hold segment offsets: read the values back, form the keys
-    for (int it = tid; it < nc; it += kScanThreads) {
-      int r = 0, o = it;
-#pragma unroll
-      for (int i = 0; i < kWaves - 1; ++i)
-        if (r == i && o >= wc[i]) {
-          o -= wc[i];
-          r = i + 1;
-        }
-      const uint32_t off = (uint32_t)sh.buf[r * kRegion + o];
-      // (an offset is always inside the segment; the guard keeps a wrong one
-      // from reading outside it)
-      sh.buf[r * kRegion + o] =
-          off < (uint32_t)seg_n ? make_key(to_f32<T>(rowp[off]), (uint32_t)seg_start + off) : 0ull;
-    }
+    const uint64_t *L0 = list[cur];
+    uint64_t *L1 = list[cur ^ 1];
+    if (M <= 64) {
+      // In registers: every wave sorts its own region (chunks of 64, even waves
+      // descending, odd ones ascending), keeping its best 64; the four lists
+      // and then the running list meet in a tree (sel::merge_halves).  Every
+      // key that drops out joins this lane's tail.
+      static_assert(kWaves == 4, "merge tree of four waves");
+      const bool mydesc = (w & 1) == 0;
+      uint64_t *rg = sh.buf + w * kRegion;
+      const int n = wc[w];
+      uint64_t v = sel::wave_sort64(lane < n ? rg[lane] : 0ull, mydesc);
+      for (int c0 = 64; c0 < n; c0 += 64) {
+        const uint64_t ch = sel::wave_sort64(c0 + lane < n ? rg[c0 + lane] : 0ull, !mydesc);
+        v = mydesc ? sel::merge_halves(v, ch, true, tail, c) : sel::merge_halves(ch, v, false, tail, c);
+      }
+      if (w & 1) rg[lane] = v;  // (a wave only ever reads its own region before this)
+      __syncthreads();
+      if ((w & 1) == 0) {
+        v = sel::merge_halves(v, sh.buf[(w + 1) * kRegion + lane], w == 0, tail, c);
+        if (w == 2) rg[lane] = v;
+      }
+      __syncthreads();
+      if (w == 0) {
+        v = sel::merge_halves(v, sh.buf[2 * kRegion + lane], true, tail, c);
+        const int li = 63 - lane;  // the running list, reversed
+        v = sel::merge_halves(v, li < nl ? L0[li] : 0ull, true, tail, c);
+        if (lane >= M && v) sel::tail_add1(tail, key_value(v), c);
+        if (lane < M) L1[lane] = v;
+      }
+    } else {
 #pragma unroll
     for (int i = 0; i < kWaves; ++i)
       if (tid == i && (wc[i] & 1)) sh.buf[i * kRegion + wc[i]] = 0ull;  // pad for paired reads
     __syncthreads();
-    const uint64_t *L0 = list[cur];
-    uint64_t *L1 = list[cur ^ 1];
     if (nc + nl <= 4 * kScanThreads) {
       // a candidate's rank is the number of larger candidates (paired reads
       // over the regions) plus the number of larger list keys (binary search);
@@ -376,6 +376,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
       const int tot = nc + nl;
       for (int i = M + tid; i < tot; i += kScanThreads) sel::tail_add1(tail, key_value(sh.buf[i]), c);
       for (int i = tid; i < M; i += kScanThreads) L1[i] = i < tot ? sh.buf[i] : 0ull;
+    }
     }
     __syncthreads();
     cur ^= 1;
@@ -445,74 +446,60 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     // batch keeps everything in range.
     const float tb = thr;
     const bool all_in = first && !(tb > NINF);
-      // tail of the elements that cannot enter (against tail.m, which is >= all
-    // of them) and the count of the others, branch-free over the registers
+    // One pass over the registers: the tail of the elements that cannot enter
+    // (against tail.m, which is >= all of them) and, for the rare elements that
+    // can, their key appended to this wave's region (wave-uniform branch on the
+    // comparison's lane mask; order (element, lane)).
     fence_regs<T>(raw);
-    // candidate flags, shifted in element by element: element k = j*EPL + e
-    // sits at bit 31 - k of lo (k < 32) or bit NE - 1 - k of hi (k >= 32)
-    constexpr int NE = NL * EPL;
-    static_assert(NE > 32 && NE <= 64, "flag words");
-    uint32_t lo = 0, hi = 0;
-    auto tail_pass = [&](auto cand) {
+    // one comparison x > te: te = tb for later batches; for the first batch
+    // any value below tb does (a few extra candidates are ranked exactly)
+    const float te = first && tb > NINF ? tb - (fabsf(tb) * 0x1p-20f + 0x1p-126f) : tb;
+    uint64_t *region = sh.buf + w * kRegion;
+    int wpos = wbase;  // wave-uniform
+    auto append = [&](bool pass, float x, int off) {
+      const uint64_t bal = __ballot(pass);
+      if (bal) {
+        const int at = wpos + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+        if (pass && at < kRegionCap) region[at] = make_key(x, (uint32_t)(seg_start + bstart + off));
+        wpos += __popcll(bal);
+      }
+    };
+    // exp((x - m) / tau) = 2^((x - m) c), 0 for candidates and padding.  While
+    // |m c| <= 128 the exponent is one fma, x c - (m c), off by at most half an
+    // ulp of m c (2^-17, the same for every term); otherwise two operations.
+    auto tail_pass = [&](auto expo) {
       float s = 0.0f;
-      const float m = tail.m;
 #pragma unroll
       for (int j = 0; j < NL; ++j)
 #pragma unroll
         for (int e = 0; e < EPL; ++e) {
           const float x = elem<T>(raw, j, e);
-          const bool pass = cand(x);
-          s += sel::fast_exp2(pass ? NINF : (x - m) * c);  // 0 for candidates and padding
-          if (j * EPL + e < 32)
-            lo = (lo << 1) | (uint32_t)pass;
-          else
-            hi = (hi << 1) | (uint32_t)pass;
+          const bool pass = x > te;
+          s += sel::fast_exp2(pass ? NINF : expo(x));
+          append(pass, x, lb + j * STEP + e);
         }
       tail.s += s;
     };
-    // one comparison x > te: te = tb for later batches; for the first batch
-    // any value below tb does (a few extra candidates are ranked exactly)
-    const float te = first && tb > NINF ? tb - (fabsf(tb) * 0x1p-20f + 0x1p-126f) : tb;
-    tail_pass([=](float x) { return x > te; });
-    // the same candidate set, element by element (used by the fallback below)
-    auto is_cand = [&](float x, int off) { return x > te || (all_in && off < bn && x == NINF); };
+    {
+      const float m = tail.m, mc = m * c;
+      if (fabsf(mc) <= 128.0f)
+        tail_pass([=](float x) { return __builtin_fmaf(x, c, -mc); });
+      else
+        tail_pass([=](float x) { return (x - m) * c; });
+    }
     if (all_in) {
       // a lower bound of -inf: the -inf elements in range are candidates too
       // (read again from memory; the tail pass gave them nothing)
 #pragma unroll 1
-      for (int k = 0; k < NE; ++k) {
+      for (int k = 0; k < NL * EPL; ++k) {
         const int off = lb + (k / EPL) * STEP + k % EPL;
-        if (off < bn && to_f32<T>(rowp[bstart + off]) == NINF) {
-          if (k < 32)
-            lo |= 1u << (31 - k);
-          else
-            hi |= 1u << (NE - 1 - k);
-        }
+        append(off < bn && to_f32<T>(rowp[bstart + off]) == NINF, NINF, off);
       }
     }
-    // candidates appended to this wave's region in (lane, element) order, as
-    // segment offsets (their keys are formed at the next merge)
-    const int cnt = __popc(lo) + __popc(hi);
-    uint64_t *region = sh.buf + w * kRegion;
-    const int incl = wave_incl_scan(cnt);
-    const int wn = __builtin_amdgcn_readlane(incl, 63);
-    {
-      int pos = wbase + incl - cnt;
-      auto put = [&](int k) {
-        if (pos < kRegionCap) region[pos] = (uint64_t)(uint32_t)(bstart + lb + (k / EPL) * STEP + k % EPL);
-        ++pos;
-      };
-      while (lo) {
-        const int bpos = 31 - __builtin_clz(lo);  // highest set bit: the lowest element
-        lo &= ~(1u << bpos);
-        put(31 - bpos);
-      }
-      while (hi) {
-        const int bpos = 31 - __builtin_clz(hi);
-        hi &= ~(1u << bpos);
-        put(NE - 1 - bpos);
-      }
-    }
+    const int wn = wpos - wbase;
+    // the same candidate set, element by element (used by the fallback below)
+    auto is_cand = [&](float x, int off) { return x > te || (all_in && off < bn && x == NINF); };
     const int wprev = wbase;
     wbase += wn;
     const int par = b & 1;

@@ -435,6 +435,29 @@ __device__ inline uint64_t merge_halves(uint64_t a, uint64_t b, bool desc, Tail 
   return bitonic_clean64(hi, desc);
 }
 
+// full bitonic sort of 64 keys (one per lane), descending or ascending
+__device__ inline uint64_t wave_sort64(uint64_t v, bool desc) {
+  const int lane = threadIdx.x & 63;
+  // a stage of block size k orders each k-block the way the next block size needs
+  auto dir = [&](int k) { return ((lane & k) == 0) == desc; };
+  v = cx_stage<1>(v, dir(2));
+  v = cx_stage<2>(v, dir(4));
+  v = cx_stage<1>(v, dir(4));
+  v = cx_stage<4>(v, dir(8));
+  v = cx_stage<2>(v, dir(8));
+  v = cx_stage<1>(v, dir(8));
+  v = cx_stage<8>(v, dir(16));
+  v = cx_stage<4>(v, dir(16));
+  v = cx_stage<2>(v, dir(16));
+  v = cx_stage<1>(v, dir(16));
+  v = cx_stage<16>(v, dir(32));
+  v = cx_stage<8>(v, dir(32));
+  v = cx_stage<4>(v, dir(32));
+  v = cx_stage<2>(v, dir(32));
+  v = cx_stage<1>(v, dir(32));
+  return bitonic_clean64(v, desc);
+}
+
 constexpr int kWaveMergeLists = 16;
 
 __host__ __device__ inline bool wave_merge_fits(int nlists, int M) {
