@@ -34,6 +34,10 @@ constexpr int kWaves = kScanThreads / 64;
 
 constexpr int kRegion = kScanSortCap / kWaves;       // candidate keys per wave
 constexpr int kRegionCap = kRegion - kMaxM / kWaves;  // fill limit: the list fits beside them
+#ifndef DT_SCAN_MERGE_AT
+#define DT_SCAN_MERGE_AT 2
+#endif
+constexpr int kMergeAt = DT_SCAN_MERGE_AT;  // candidates gathered (times M) that trigger a merge
 
 struct ScanLDS {
   alignas(16) uint64_t buf[kScanSortCap];
@@ -522,7 +526,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     if (!overflow) {
       // a merge costs a fixed latency plus a term quadratic in the candidates:
       // merge once about 2M have gathered
-      if (first || crowded || ncand >= 2 * M || b == nbat - 1) {
+      if (first || crowded || ncand >= kMergeAt * M || b == nbat - 1) {
         merge_regions(wc);
         after_merge();
       }
