@@ -34,10 +34,9 @@ constexpr int kWaves = kScanThreads / 64;
 
 constexpr int kRegion = kScanSortCap / kWaves;       // candidate keys per wave
 constexpr int kRegionCap = kRegion - kMaxM / kWaves;  // fill limit: the list fits beside them
-#ifndef DT_SCAN_MERGE_AT
-#define DT_SCAN_MERGE_AT 2
-#endif
-constexpr int kMergeAt = DT_SCAN_MERGE_AT;  // candidates gathered (times M) that trigger a merge
+// a merge is due once this many times M candidates have gathered (measured best
+// at 2 for Qwen3 shapes: 1, 4 and 8 were slower)
+constexpr int kMergeAt = 2;
 
 struct ScanLDS {
   alignas(16) uint64_t buf[kScanSortCap];
@@ -524,8 +523,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
       ncand += wc[i];
     }
     if (!overflow) {
-      // a merge costs a fixed latency plus a term quadratic in the candidates:
-      // merge once about 2M have gathered
+      // a merge costs a fixed latency plus a term growing with the candidates
       if (first || crowded || ncand >= kMergeAt * M || b == nbat - 1) {
         merge_regions(wc);
         after_merge();
