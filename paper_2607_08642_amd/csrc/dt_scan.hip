@@ -1,26 +1,33 @@
 // S1: per-depth marginal top-M and the tail log-sum-exp (Alg. 1 step 1;
 // section 3.2, candidate restriction).
 //
-// Each logit row [V] is cut into chunks of 10240 elements.  One 256-thread
-// workgroup loads its whole chunk into registers (40 values per thread, all
-// loads in flight at once) and selects the chunk's M best elements exactly:
+// Each logit row [V] is cut into segments of one or more batches of 10240
+// elements; a 256-thread workgroup streams its segment's batches through
+// registers (40 values per thread, the next batch always in flight) against a
+// running exact top-M list:
 //   * keys are 64-bit (order-preserving value bits, ~index), so the order
 //     (value desc, id asc) is a plain integer order without ties;
-//   * every wave finds the ceil(M/4)-th largest of its 64 per-lane maxima (a
-//     bitwise search with one ballot per bit); the minimum over the 4 waves
-//     leaves at least M elements at or above it, so it is an exact lower bound
-//     on the chunk's M-th best element;
-//   * a pass over the registers sends elements below that bound into the
-//     running tail sum (max, sum exp((x - max)/tau)); the survivors (about 1%
-//     of the chunk on drafter-like rows) go to a per-wave region of LDS;
-//     each survivor is ranked by counting the larger ones, the best M are the
-//     chunk's list and the rest join the tail.
-// Many survivors are bitonic-sorted instead; if a wave's survivors overflow
-// its region (adversarial rows: long runs of equal or monotone values), they
-// are streamed through a bounded selector that keeps a sorted list of M.
-// The per-row merge (merge_row) combines the chunk lists and tails of a row;
-// it runs inside the expansion kernel, or in a small kernel of its own for
-// dt_scan_topm.
+//   * first batch: every wave finds the ceil(M/4)-th largest of its 64 per-lane
+//     maxima (a bitwise search with one ballot per bit); the minimum over the
+//     4 waves leaves at least M elements at or above it, so it is an exact
+//     lower bound on the batch's M-th best element;  later batches: the list's
+//     M-th value;
+//   * one pass over the registers sends every element below that threshold
+//     into the running tail sum (max, sum exp((x - max)/tau)); the few above
+//     it are appended, as keys, to a per-wave region of LDS through the
+//     comparison's lane mask;
+//   * the regions are merged into the list after the first batch, once about
+//     2M candidates have gathered, and at the end.  For M <= 64 each wave
+//     sorts its region in registers (bitonic, 64 keys per lane-set) and the
+//     wave lists and the list meet in a tree of bitonic merges; larger M ranks
+//     every candidate by counting the larger ones (or sorts when there are
+//     many).  Keys that drop out of the list join the tail.
+// If a wave's candidates overflow its region (adversarial rows: long runs of
+// equal or monotone values), the batch is streamed through a bounded selector
+// that keeps a sorted list of M.
+// The per-row merge of the segment lists (merge_row and its register
+// variants) runs inside the expansion kernel, or in a small kernel of its own
+// for dt_scan_topm.
 #include "dt_select.h"
 #include <hip/hip_ext.h>
 
