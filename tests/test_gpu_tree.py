@@ -54,6 +54,13 @@ SWEEP = [
     (10, 2, 4, 64, 64, 20, 1.0, 32, 32, synth.DT_F32, {}, {}),
     (11, 1, 5, 333, 20, 30, 0.6, 36, 32, synth.DT_BF16, dict(max_children=8), {}),
     (12, 6, 16, 1500, 64, 64, 0.0, 64, 96, synth.DT_BF16, {}, dict(h0=True)),
+    # several segment lists per row (10240 logits each): the register tree
+    # merge with M < 64 and a 5-element last list, the one-wave merge of two
+    # lists, more than 16 lists (block merge) and M > 64 (block merges)
+    (13, 1, 4, 30725, 48, 16, 0.8, 32, 32, synth.DT_F32, {}, {}),
+    (14, 2, 3, 15000, 40, 12, 0.0, 32, 32, synth.DT_BF16, {}, {}),
+    (15, 1, 4, 200000, 32, 16, 1.0, 32, 32, synth.DT_F32, {}, {}),
+    (16, 2, 4, 50000, 100, 24, 0.7, 32, 32, synth.DT_BF16, {}, dict(h0=True)),
 ]
 
 
