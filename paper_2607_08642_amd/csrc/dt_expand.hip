@@ -147,7 +147,11 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
 }
 
 // scalar slots in LDS
-enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NE, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR, S_CNT0 };
+enum { S_NN, S_VB, S_NEXP, S_STATUS, S_LIST, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR, S_CNT0 };
+// after the per-wave slots S_CNT0 ..: two counters of the nodes a vB count
+// lists (used alternately by consecutive counts)
+constexpr int S_NTOP = S_CNT0 + kExpThreads / 64;
+static_assert(S_NTOP + 2 <= 32, "scalar slots below the reduction area");
 
 
 // GRU activations on the hardware exp2 and reciprocal (about 1 ulp each):
@@ -157,6 +161,9 @@ __device__ inline float sigmoid_fast(float x) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.44269504088896341f * x));
 }
 __device__ inline float tanh_fast(float x) { return 2.0f * sigmoid_fast(2.0f * x) - 1.0f; }
+// e^x and ln x on the hardware exp2 / log2 (about 1 ulp; x <= 0 and x >= 1 here)
+__device__ inline float exp_hw(float x) { return __builtin_amdgcn_exp2f(1.44269504088896341f * x); }
+__device__ inline float log_hw(float x) { return 0.69314718055994531f * __builtin_amdgcn_logf(x); }
 
 __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -489,6 +496,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scal[S_NEXP] = 0;
     scal[S_STOP] = 0;
     scal[S_CUR] = 0;
+    scal[S_LIST] = -1;
+    scal[S_NTOP] = 0;
+    scal[S_NTOP + 1] = 0;
   }
   __syncthreads();
 
@@ -866,10 +876,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       float sum = 0.0f;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        if (s < MP / 64) sum += (zv[s] > NEG_INF) ? expf(zv[s] - mx) : 0.0f;
+        if (s < MP / 64) sum += (zv[s] > NEG_INF) ? exp_hw(zv[s] - mx) : 0.0f;
       sum = wave_sum_f(sum);
-      if (tail) sum += expf(R - mx);
-      const float logZ = mx + logf(sum);
+      if (tail) sum += exp_hw(R - mx);
+      const float logZ = mx + log_hw(sum);
       float lv[4];
       // E: the slots whose child could enter (log-prob finite, g >= vB).  A slot
       // ranked above a member of E is in E itself, so a member's rank among
@@ -999,10 +1009,14 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 
   // ---- vB = B-th best known score; drop nodes below it when room is needed --
   // Returns vB to every thread (S_VB is written for readers past the next barrier).
+  // A count also lists the nodes scoring >= vB in elist (S_LIST names the
+  // counter holding their number; -1 once the table has changed under it).
+  int vbcall = 0;
   auto update_vb = [&](bool compact) -> float {
     const int nn = scal[S_NN];
     float vB = scalf[S_VB];
     if (nn >= B) {
+      const int slot = S_NTOP + (vbcall & 1);
       float best = __builtin_huge_valf();
       const float4 *g4 = reinterpret_cast<const float4 *>(ng);
       const int n4 = nn >> 2;
@@ -1015,7 +1029,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
         }
         for (int j = n4 * 4; j < nn; ++j) cnt += ng[j] > gi;
-        if (cnt < B) best = fminf(best, gi);
+        if (cnt < B) {
+          best = fminf(best, gi);
+          elist[atomicAdd(&scal[slot], 1)] = (int16_t)i;
+        }
       }
       best = wave_min_f(best);
       if (lane == 0) scalf[S_CNT0 + wave] = best;
@@ -1023,7 +1040,14 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       vB = scalf[S_CNT0];
 #pragma unroll
       for (int w = 1; w < NW; ++w) vB = fminf(vB, scalf[S_CNT0 + w]);
-      if (tid == 0) scalf[S_VB] = vB;
+      if (tid == 0) {
+        scalf[S_VB] = vB;
+        scal[S_LIST] = compact ? -1 : slot;
+        scal[S_NTOP + ((vbcall & 1) ^ 1)] = 0;  // the next count's counter
+      }
+      ++vbcall;
+    } else if (tid == 0) {
+      scal[S_LIST] = -1;
     }
     if (!compact || nn < B) return vB;
     // keep g >= vB (parents always score at least their children: links stay valid)
@@ -1168,15 +1192,20 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   const int nn = scal[S_NN];
   if (wave == 0) {
     const float vB = scalf[S_VB];
+    const int listed = scal[S_LIST];
     int ncand = 0;
-    for (int r0 = 0; r0 < nn; r0 += 64) {
-      const int i = r0 + lane;
-      const bool in = i < nn && ng[i] >= vB;
-      const uint64_t bal = __ballot(in);
-      const int at = ncand + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
-      if (in && at < 64) elist[at] = (int16_t)i;
-      ncand += __popcll(bal);
+    if (listed >= 0) {
+      ncand = scal[listed];  // the last vB count listed them (in any order)
+    } else {
+      for (int r0 = 0; r0 < nn; r0 += 64) {
+        const int i = r0 + lane;
+        const bool in = i < nn && ng[i] >= vB;
+        const uint64_t bal = __ballot(in);
+        const int at = ncand + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+        if (in && at < 64) elist[at] = (int16_t)i;
+        ncand += __popcll(bal);
+      }
     }
     wave_sync();
     int npop = 0;
