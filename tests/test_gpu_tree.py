@@ -61,6 +61,8 @@ SWEEP = [
     (14, 2, 3, 15000, 40, 12, 0.0, 32, 32, synth.DT_BF16, {}, {}),
     (15, 1, 4, 200000, 32, 16, 1.0, 32, 32, synth.DT_F32, {}, {}),
     (16, 2, 4, 50000, 100, 24, 0.7, 32, 32, synth.DT_BF16, {}, dict(h0=True)),
+    # the envelope's maxima: L = 64, M = 256, B = 256
+    (17, 1, 64, 3000, 256, 256, 0.9, 32, 32, synth.DT_F32, {}, {}),
 ]
 
 
