@@ -8,6 +8,9 @@ from .dominotree_ref import (  # noqa: F401
     DT_F32,
     NORM_SLICE,
     NORM_TAIL,
+    SCORER_COND,
+    SCORER_MARG,
+    SCORER_STATIC,
     TREE_NONFINITE,
     build_tree,
     build_trees,

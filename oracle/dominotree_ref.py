@@ -20,6 +20,12 @@ own order:
   until the budget is spent (Alg. 1, steps 3-4; DDTree heap, section 2.4).
 * Emission orders nodes so parents precede children and builds the
   ancestor-only verification mask (section 3.5; Appendix B, frontier selection).
+* The ablation arms' children functions (Appendix D, the three arms; Marg
+  children, section 3.1): MARG scores a depth's slice from the marginal logits
+  alone (no correction; one menu per depth, shared by all its nodes);
+  STATIC applies the correction once per depth, from the state of the greedy
+  chain (Domino's own decoder: at each depth the best corrected child), and
+  shares that corrected menu with every node of the depth.
 
 Readings of the paper that this file fixes (the paper is silent on them):
 
@@ -53,6 +59,9 @@ import numpy as np
 
 NORM_TAIL = 0
 NORM_SLICE = 1
+SCORER_COND = 0    # DominoTree: the correction recomputed from each node's own path state
+SCORER_MARG = 1    # Marg: marginal logits only
+SCORER_STATIC = 2  # Cond-static: the correction along the greedy chain, one menu per depth
 TREE_NONFINITE = 0x1
 
 DT_F32 = 0
@@ -145,11 +154,13 @@ def gru_cell(h: np.ndarray, xs: np.ndarray, w_ih, w_hh, b_ih, b_hh) -> np.ndarra
 class _Model:
     """float64 copies of the weights plus the per-depth candidate tables."""
 
-    def __init__(self, X, emb, emb_dtype, w, M, tau, norm_mode):
+    def __init__(self, X, emb, emb_dtype, w, M, tau, norm_mode, scorer=SCORER_COND):
         self.L = X.shape[0]
         self.M = M
         self.tau = tau
         self.norm_mode = norm_mode
+        self.scorer = scorer
+        self.menus = None
         self.w_ih = widen(w["w_ih"], w["dtype"])
         self.w_hh = widen(w["w_hh"], w["dtype"])
         self.b_ih = widen(w.get("b_ih"), w["dtype"])
@@ -165,16 +176,20 @@ class _Model:
             self.R.append(R)
             self.Ec.append(widen(np.asarray(emb)[ids], emb_dtype))
 
-    def slot_logprobs(self, S: np.ndarray, d: int):
+    def slot_logprobs(self, S: Optional[np.ndarray], d: int):
         """Corrected, normalised log-probs of depth d's slice given path state S.
 
         delta_m = E[cand_d[m]] . (W_c S + b_c);  z = (x + delta) / tau;
-        ell = z - logZ.  Returns (ell[M] with -inf for dead slots, live mask).
+        ell = z - logZ.  S = None: no correction (delta = 0, the marginals).
+        Returns (ell[M] with -inf for dead slots, live mask).
         """
-        q = self.w_c @ S
-        if self.b_c is not None:
-            q = q + self.b_c
-        delta = self.Ec[d - 1] @ q
+        if S is None:
+            delta = np.zeros(self.M)
+        else:
+            q = self.w_c @ S
+            if self.b_c is not None:
+                q = q + self.b_c
+            delta = self.Ec[d - 1] @ q
         x = self.xc[d - 1]
         live = x > -math.inf
         z = np.full(self.M, -math.inf)
@@ -187,9 +202,36 @@ class _Model:
         ell[live] = z[live] - logZ
         return ell, live
 
-    def children(self, S: np.ndarray, d: int, k: int, gaps: list):
-        """Children(S_{d-1}, d) of Alg. 1 step 2: top-k (token, ell, slot, child state)."""
-        ell, live = self.slot_logprobs(S, d)
+    def static_menus(self, S0: np.ndarray):
+        """Cond-static menus: walk the greedy chain from S0 (at each depth the best
+        corrected slot, by (ell desc, slot asc)), keeping every depth's corrected,
+        normalised slice log-probs.  Depths past a dead end get no live slot."""
+        self.menus = []
+        S = S0
+        for d in range(1, self.L + 1):
+            if S is None:
+                self.menus.append((np.full(self.M, -math.inf), np.zeros(self.M, bool)))
+                continue
+            ell, live = self.slot_logprobs(S, d)
+            self.menus.append((ell, live))
+            slots = [m for m in range(self.M) if live[m]]
+            if not slots:
+                S = None
+                continue
+            best = min(slots, key=lambda m: (-ell[m], m))
+            S = gru_cell(S, self.Ec[d - 1][[best]], self.w_ih, self.w_hh, self.b_ih, self.b_hh)[0]
+
+    def children(self, S: Optional[np.ndarray], d: int, k: int, gaps: list):
+        """Children(S_{d-1}, d) of Alg. 1 step 2: top-k (token, ell, slot, child state).
+
+        MARG and STATIC ignore S (their menus are path-independent) and return
+        no child states."""
+        if self.scorer == SCORER_MARG:
+            ell, live = self.slot_logprobs(None, d)
+        elif self.scorer == SCORER_STATIC:
+            ell, live = self.menus[d - 1]
+        else:
+            ell, live = self.slot_logprobs(S, d)
         slots = [m for m in range(self.M) if live[m]]
         slots.sort(key=lambda m: (-ell[m], m))
         if len(slots) > k:
@@ -198,6 +240,8 @@ class _Model:
         if not kept:
             return []
         tokens = [int(self.cand[d - 1][m]) for m in kept]
+        if self.scorer != SCORER_COND:
+            return [(tokens[i], float(ell[m]), m, None) for i, m in enumerate(kept)]
         states = gru_cell(S, self.Ec[d - 1][kept], self.w_ih, self.w_hh, self.b_ih, self.b_hh)
         return [(tokens[i], float(ell[m]), m, states[i]) for i, m in enumerate(kept)]
 
@@ -220,7 +264,7 @@ def _empty_tree(B: int, pos_offset: int, status: int):
 def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                h0: Optional[np.ndarray], M: int, B: int, T: float,
                max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
-               logits_dtype: int = DT_F32):
+               logits_dtype: int = DT_F32, scorer: int = SCORER_COND):
     """Build one draft tree (Alg. 1) and emit it in pop order.
 
     X: [L, V] stored marginal logits of one tree; emb: [V, d_e]; weights: dict
@@ -232,10 +276,12 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
         return _empty_tree(B, pos_offset, TREE_NONFINITE)
     tau = effective_temperature(T)
     k = min(M, B) if max_children <= 0 else min(max_children, M)
-    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode)
+    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode, scorer)
     L = model.L
     d_h = model.w_hh.shape[1]
     S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
+    if scorer == SCORER_STATIC:
+        model.static_menus(S0)
 
     gaps: List[float] = []
     heap = []          # entries (-g, insertion id, payload)
@@ -284,11 +330,12 @@ def _emit(tree, B: int, pos_offset: int, min_gap: float):
 def build_trees(logits: np.ndarray, logits_dtype: int, emb: np.ndarray, emb_dtype: int,
                 weights: dict, h0: Optional[np.ndarray], M: int, B: int, T: float,
                 max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
-                trees: Optional[Sequence[int]] = None):
+                trees: Optional[Sequence[int]] = None, scorer: int = SCORER_COND):
     """build_tree over the batch (or the listed tree indices)."""
     idx = range(logits.shape[0]) if trees is None else trees
     return [build_tree(logits[t], emb, emb_dtype, weights, None if h0 is None else h0[t],
-                       M, B, T, max_children, norm_mode, pos_offset, logits_dtype) for t in idx]
+                       M, B, T, max_children, norm_mode, pos_offset, logits_dtype, scorer)
+            for t in idx]
 
 
 def scan(logits: np.ndarray, logits_dtype: int, M: int, T: float):
@@ -305,7 +352,8 @@ def scan(logits: np.ndarray, logits_dtype: int, M: int, T: float):
 
 def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                 h0: Optional[np.ndarray], M: int, B: int, T: float, tokens, parents, n_nodes: int,
-                max_children: int = 0, norm_mode: int = NORM_TAIL, logits_dtype: int = DT_F32):
+                max_children: int = 0, norm_mode: int = NORM_TAIL, logits_dtype: int = DT_F32,
+                scorer: int = SCORER_COND):
     """Re-score a given tree with the oracle's Children function.
 
     Returns (g[n], valid): valid is False when a node's token is not among the
@@ -314,9 +362,11 @@ def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     Xd = widen(X, logits_dtype)
     tau = effective_temperature(T)
     k = min(M, B) if max_children <= 0 else min(max_children, M)
-    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode)
+    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode, scorer)
     d_h = model.w_hh.shape[1]
     S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
+    if scorer == SCORER_STATIC:
+        model.static_menus(S0)
     g = np.zeros(n_nodes)
     state = [None] * n_nodes
     depth = [0] * n_nodes

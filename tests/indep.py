@@ -146,6 +146,35 @@ def factorized_tree(X, logits_dtype, M, B, T, k, norm_slice=False):
     return toks, pars, deps, gs
 
 
+def _menu_heap(menus, B: int, L: int):
+    """DDTree's heap over per-depth menus of (token, log-prob) in rank order."""
+    heap, cnt = [], itertools.count()
+    for t, l in menus[0]:
+        heapq.heappush(heap, (-l, next(cnt), t, l, 1, -1))
+    toks, pars, deps, gs = [], [], [], []
+    while len(toks) < B and heap:
+        _, _, t, g, d, p = heapq.heappop(heap)
+        i = len(toks)
+        toks.append(t), pars.append(p), deps.append(d), gs.append(g)
+        if d < L:
+            for ct, cl in menus[d]:
+                heapq.heappush(heap, (-(g + cl), next(cnt), ct, g + cl, d + 1, i))
+    return toks, pars, deps, gs
+
+
+def static_tree(sc: TorchScorer, B: int, k: int):
+    """Cond-static arm (Appendix D): the corrected menu of depth d is computed once,
+    from the state of Domino's greedy chain (the best corrected child at every
+    depth), and offered to every node of depth d.  Returns pop-order
+    (tokens, parents, depth, g)."""
+    S, menus = sc.h0, []
+    for d in range(1, sc.L + 1):
+        kids = sc.ranked_children(S, d, sc.M) if S is not None else []
+        menus.append(kids[:k])
+        S = sc.step(S, kids[0][0]) if kids else None
+    return _menu_heap(menus, B, sc.L)
+
+
 def greedy_chain(sc: TorchScorer, length: int):
     """Domino's chain decoder at T=0 (Fact A): argmax of the corrected logits."""
     S, toks = sc.h0, []
