@@ -85,6 +85,16 @@ typedef enum {
 #define DT_NORM_TAIL 0  /* logZ includes the uncorrected out-of-slice mass R_d */
 #define DT_NORM_SLICE 1 /* logZ over the top-M slice only */
 
+/* children function (dt_options.scorer); the three arms of the paper's
+ * ablation (Appendix D) */
+#define DT_SCORER_COND 0   /* DominoTree: the correction recomputed from each node's own
+                              path state (Alg. 1, section 3.1) */
+#define DT_SCORER_MARG 1   /* Marg: a depth's slice scored from the marginal logits alone
+                              (no correction; the menu is shared by the depth's nodes) */
+#define DT_SCORER_STATIC 2 /* Cond-static: the correction computed once per depth from
+                              the state of Domino's greedy chain (the best corrected child
+                              at every depth), its menu shared by the depth's nodes */
+
 /* GRU of Domino's causal encoder (section 2.3), PyTorch GRUCell layout.
  * w_ih: [3*d_h, d_in] with d_in = the embedding width d_e; w_hh: [3*d_h, d_h];
  * b_ih, b_hh: [3*d_h] or NULL (treated as zeros).  dtype = the plan's
@@ -105,7 +115,7 @@ typedef struct {
                        The paper's headline setting is 8 (section 4.1). */
   int norm_mode;    /* DT_NORM_TAIL (default) or DT_NORM_SLICE */
   int pos_offset;   /* position_ids = pos_offset + depth */
-  int reserved;     /* must be 0 */
+  int scorer;       /* DT_SCORER_COND (default, 0), DT_SCORER_MARG or DT_SCORER_STATIC */
 } dt_options;
 
 /* Output tree of every batch entry b (device pointers, caller-owned).

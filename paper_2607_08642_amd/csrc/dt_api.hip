@@ -54,7 +54,11 @@ Workspace carve(const dt_plan *p, int batch, char *base) {
   ws.states = at((size_t)batch * ws.ecap * p->d_h * sizeof(float));
   ws.part = at(expand_part_bytes(p, batch));
   // per tree: barrier counters; then the member-slot counters of the launch
-  ws.bar = reinterpret_cast<int32_t *>(at((size_t)(batch + 2) * kBarStride * sizeof(int32_t)));
+  // (two sets: a call makes up to two expansion launches)
+  ws.bar = reinterpret_cast<int32_t *>(at((size_t)2 * (batch + 2) * kBarStride * sizeof(int32_t)));
+  ws.menus = p->scorer == DT_SCORER_STATIC
+                 ? at((size_t)batch * p->L * ((p->M + 63) / 64 * 64) * sizeof(float))
+                 : nullptr;
   ws.bytes = o;
   return ws;
 }
@@ -105,7 +109,8 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (o.max_children < 0) return fail(DT_ERR_SHAPE, "max_children must be >= 0");
   if (o.norm_mode != DT_NORM_TAIL && o.norm_mode != DT_NORM_SLICE)
     return fail(DT_ERR_UNSUPPORTED, "norm_mode must be DT_NORM_TAIL or DT_NORM_SLICE");
-  if (o.reserved != 0) return fail(DT_ERR_UNSUPPORTED, "dt_options.reserved must be 0");
+  if (o.scorer != DT_SCORER_COND && o.scorer != DT_SCORER_MARG && o.scorer != DT_SCORER_STATIC)
+    return fail(DT_ERR_UNSUPPORTED, "scorer must be DT_SCORER_COND, DT_SCORER_MARG or DT_SCORER_STATIC");
   const size_t ws = dsize(weights_dtype);
   if (!aligned(emb, 16) || !aligned(gru->w_ih, ws) || !aligned(gru->w_hh, ws) ||
       !aligned(head->w, ws) || (gru->b_ih && !aligned(gru->b_ih, ws)) ||
@@ -146,6 +151,7 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (k > B) k = B;  // a child ranked B or lower among its siblings can never be popped
   p->k = k;
   p->norm_mode = o.norm_mode;
+  p->scorer = o.scorer;
   p->pos_offset = o.pos_offset;
   p->wdt = weights_dtype;
   p->ldt = logits_dtype;
@@ -272,13 +278,31 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   }
   // profiled calls time each kernel from its start to its end
   hipEvent_t *ev = prof ? plan->ev + 4 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
-  // the scan kernel also clears the expansion kernel's barrier counters
-  hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar,
-                                        (batch + 2) * dt::kBarStride, s, prof ? ev[0] : nullptr,
-                                        prof ? ev[1] : nullptr);
+  // the scan kernel also clears the expansion launches' barrier counters
+  const int nbar = (batch + 2) * dt::kBarStride;
+  hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, 2 * nbar, s,
+                                        prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
+  dt::ExpMode mode;
+  if (plan->scorer == DT_SCORER_MARG) {
+    mode.nocorr = 1;
+  } else if (plan->scorer == DT_SCORER_STATIC) {
+    // the greedy chain (k = 1, L pops) writes every depth's corrected menu;
+    // the tree is then built from those menus
+    dt::ExpMode chain;
+    chain.menu_out = ws.menus;
+    chain.emit = 0;
+    chain.k = 1;
+    chain.B = plan->L;
+    e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s, nullptr, nullptr, chain);
+    if (e != hipSuccess) return hip_fail(e, "expand launch (greedy chain)");
+    mode.nocorr = 1;
+    mode.menu_in = ws.menus;
+    mode.skip_merge = 1;
+    mode.bar = ws.bar + nbar;
+  }
   e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s, prof ? ev[2] : nullptr,
-                        prof ? ev[3] : nullptr);
+                        prof ? ev[3] : nullptr, mode);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   if (prof) plan->profiled_calls++;
   return DT_OK;

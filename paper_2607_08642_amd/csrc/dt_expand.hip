@@ -51,6 +51,12 @@ static_assert(CH == 2 * NW, "children step: two nodes per wave");
 struct ExpArgs {
   int L, M, B, k, dh, G, norm_mode, pos_offset, ecap, batch, nchunks, nxcd;
   int use_us;  // U slices of the expanded depth staged into LDS (see us_fits)
+  // ablation-arm modes (ExpMode): no correction (the marginals, or menu_in's
+  // per-depth menus); menu_out: every expanded node's slot log-probs; emit = 0:
+  // no replay or emission; skip_merge: the rows are already merged
+  int nocorr, emit, skip_merge;
+  const float *menu_in;  // [batch][L][MP]
+  float *menu_out;       // [batch][L][MP]
   float inv_tau, c2;  // c2 = log2(e) / tau
   const uint64_t *ckeys;
   const float2 *ctail;
@@ -413,8 +419,17 @@ struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per 
 
 // SDH, SG, SM, SL > 0 fix d_h, G, M and L at compile time (the LDS layout and
 // every loop bound over them become constants); 0 takes them from the arguments.
-template <typename TW, int SDH, int SG, int SM, int SL>
+// ARMS compiles the ablation-arm modes in (nocorr, menu_in, menu_out, emit,
+// skip_merge); without it they are fixed off and cost nothing.
+template <typename TW, int SDH, int SG, int SM, int SL, bool ARMS>
 __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
+  if constexpr (!ARMS) {
+    a.nocorr = 0;
+    a.emit = 1;
+    a.skip_merge = 0;
+    a.menu_in = nullptr;
+    a.menu_out = nullptr;
+  }
   if constexpr (SDH > 0) a.dh = SDH;
   if constexpr (SG > 0) a.G = SG;
   if constexpr (SM > 0) a.M = SM;
@@ -510,7 +525,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 #pragma unroll
   for (int q = 0; q < 2; ++q)
     if (a.h0 && tid + q * NT < UW) h0v[q] = a.h0[(size_t)t * dh + member * UW + tid + q * NT];
-  if (sel::wave_merge_fits(a.nchunks, M) && a.nchunks > 2) {
+  if (a.skip_merge) {
+    // (the rows were merged by the call's first expansion launch)
+  } else if (sel::wave_merge_fits(a.nchunks, M) && a.nchunks > 2) {
     // all waves on each of this member's rows
     for (int d = member; d < L; d += G) {
       const int row = t * L + d;
@@ -615,8 +632,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       gk1 = (nks * (f + 1)) / WPG;
     }
     typename Gates<TW>::Pre wpre;
-    const bool wearly =
-        Gates<TW>::kPre > 0 && use_pin && d > 0 && gu >= 0 && gk1 - gk0 <= Gates<TW>::kPre;
+    const bool wearly = !a.nocorr && Gates<TW>::kPre > 0 && use_pin && d > 0 && gu >= 0 &&
+                        gk1 - gk0 <= Gates<TW>::kPre;
     if (wearly) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);
     if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
     {
@@ -635,7 +652,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       if (d < L && tid == NT - 1) rt = ld_dev(a.tailR + row);
       // parent states straight into LDS (16 bytes per lane, 256 floats per
       // wave instruction); unused columns read the root slot
-      if (d > 0) {
+      if (d > 0 && !a.nocorr) {
         const int root_slot = a.ecap - 1;
         for (int i = wave; i < CH * dh / 256; i += NW) {
           const int e = i * 256 + 4 * lane;
@@ -651,7 +668,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         }
       }
       // this member's U slice of depth d's candidates, straight into LDS
-      if (a.use_us && d < L) {
+      if (a.use_us && d < L && !a.nocorr) {
         const __amdgpu_buffer_rsrc_t ru =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.U_all), 0, 0x7FFFFFF0, 0x00020000);
         for (int i = wave; i < MP * UW / 256; i += NW) {
@@ -665,7 +682,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       // GRU inputs of the chunk's nodes straight into LDS, one wave instruction
       // per node: lane l < 3 UW/4 takes 4 floats of gate l / (UW/4); the other
       // lanes re-read the first 16 bytes into the slot's unused tail
-      if (use_pin && d > 0) {
+      if (use_pin && d > 0 && !a.nocorr) {
         const int QW = UW / 4;
         const int g = lane / QW, k = (lane - g * QW) * 4;
         const int voff = lane < 3 * QW ? (g * dh + k) * 4 : 0;
@@ -687,7 +704,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     }
     __syncthreads();
     // 1. path states of this member's units: S = GRU(S_parent, E[token]) (section 2.3)
-    if (d == 0) {
+    if (a.nocorr) {
+      // (no path states without the correction)
+    } else if (d == 0) {
       for (int u = tid; u < UW; u += NT) {
         const int j = member * UW + u;
         for (int c = 0; c < CH; ++c) Sn[c * UW + u] = (c == 0 && a.h0) ? a.h0[(size_t)t * dh + j] : 0.0f;
@@ -812,7 +831,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // parts of member j: a [CH][MP] block of their own (no line is shared by two writers)
     const __amdgpu_buffer_rsrc_t rmy =
         dev_rsrc(a.part + (((size_t)t * 2 + pb) * G + member) * CH * MP);
-    for (int rt = wave; rt < RT; rt += NW) {
+    for (int rt = a.nocorr ? RT : wave; rt < RT; rt += NW) {
       const int m = rt * 16 + (lane & 15);
       const int c = lane & 15, kq = (lane >> 4) * 4;
       const float *urow = a.U_all + (size_t)(m < M ? ccand[m] : 0) * dh + member * UW;
@@ -834,7 +853,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
                  make_float4(acc[0], acc[1], acc[2], acc[3]));
     }
-    group_barrier(ctr, G, nbar, &scal[S_STATUS]);
+    if (!a.nocorr) group_barrier(ctr, G, nbar, &scal[S_STATUS]);
     // 3. children of each node: normalise, rank, keep the top-k above vB
     const float vB = scalf[S_VB];
     const float R = scalf[S_R];
@@ -856,31 +875,48 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     };
     auto node_children = [&](int c, const Parts &p0) {
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
-      float zv[4];
-      float mx = NEG_INF;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s >= MP / 64) break;
-        const int m = lane + 64 * s;
-        const Parts p = s == 0 ? p0 : load_parts(c, s);
-        // x already holds logit + E[v] . b_c (added by the row merge)
-        const float x = ccandv[m];
-        const float dl = x + sum_parts(p, lane);
-        const float z = x > NEG_INF ? dl * a.inv_tau : NEG_INF;  // slots >= M hold -inf
-        zv[s] = z;
-        mx = fmaxf(mx, z);
-      }
-      mx = wave_max_f(mx);
-      const bool tail = (a.norm_mode == DT_NORM_TAIL) && R > NEG_INF;
-      if (tail) mx = fmaxf(mx, R);
-      float sum = 0.0f;
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (s < MP / 64) sum += (zv[s] > NEG_INF) ? exp_hw(zv[s] - mx) : 0.0f;
-      sum = wave_sum_f(sum);
-      if (tail) sum += exp_hw(R - mx);
-      const float logZ = mx + log_hw(sum);
       float lv[4];
+      if (a.menu_in) {
+        // a shared menu: depth d's slot log-probs, already normalised
+        const float *mrow = a.menu_in + ((size_t)t * L + d) * MP;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (s < MP / 64) lv[s] = mrow[lane + 64 * s];
+      } else {
+        float zv[4];
+        float mx = NEG_INF;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          if (s >= MP / 64) break;
+          const int m = lane + 64 * s;
+          // x already holds logit + E[v] . b_c (added by the row merge; not for the marginals)
+          const float x = ccandv[m];
+          const float dl = a.nocorr ? x : x + sum_parts(s == 0 ? p0 : load_parts(c, s), lane);
+          const float z = x > NEG_INF ? dl * a.inv_tau : NEG_INF;  // slots >= M hold -inf
+          zv[s] = z;
+          mx = fmaxf(mx, z);
+        }
+        mx = wave_max_f(mx);
+        const bool tail = (a.norm_mode == DT_NORM_TAIL) && R > NEG_INF;
+        if (tail) mx = fmaxf(mx, R);
+        float sum = 0.0f;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (s < MP / 64) sum += (zv[s] > NEG_INF) ? exp_hw(zv[s] - mx) : 0.0f;
+        sum = wave_sum_f(sum);
+        if (tail) sum += exp_hw(R - mx);
+        const float logZ = mx + log_hw(sum);
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (s < MP / 64) lv[s] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
+      }
+      if (a.menu_out && member == 0) {
+        // this node's slot log-probs: depth d's menu (one node per depth in a chain)
+        float *mrow = a.menu_out + ((size_t)t * L + d) * MP;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (s < MP / 64) mrow[lane + 64 * s] = lv[s];
+      }
       // E: the slots whose child could enter (log-prob finite, g >= vB).  A slot
       // ranked above a member of E is in E itself, so a member's rank among
       // all slots is its rank within E.
@@ -890,7 +926,6 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       for (int s = 0; s < 4; ++s) {
         em[s] = 0ull;
         if (s >= MP / 64) break;
-        lv[s] = (zv[s] > NEG_INF) ? zv[s] - logZ : NEG_INF;
         em[s] = __ballot(lv[s] > NEG_INF && gpar + lv[s] >= vB);
         ne += __popcll(em[s]);
         ell[c * MP + lane + 64 * s] = lv[s];
@@ -953,8 +988,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // two nodes per wave: the second node's loads are in flight during the first
     const int c0 = wave, c1 = wave + NW;
     Parts p0, p1;
-    if (c0 < nc) p0 = load_parts(c0, 0);
-    if (c1 < nc) p1 = load_parts(c1, 0);
+    if (c0 < nc && !a.nocorr) p0 = load_parts(c0, 0);
+    if (c1 < nc && !a.nocorr) p1 = load_parts(c1, 0);
     if (c0 < nc)
       node_children(c0, p0);
     else if (lane == 0)
@@ -1180,7 +1215,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     if (nc2 == 0) continue;
     expand_chunk(cl, nc2, ndepth[cl[0]]);
   }
-  if (member != 0) return;
+  if (member != 0 || !a.emit) return;
 
   // ---- phase B: exact replay of the heap --------------------------------------
   // Only nodes scoring >= vB (the B-th best score in the table) can be among
@@ -1360,13 +1395,18 @@ size_t expand_part_bytes(const dt_plan *p, int batch) {
 
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s, hipEvent_t t0,
-                         hipEvent_t t1) {
+                         hipEvent_t t1, const ExpMode &mode) {
   ExpArgs a;
   const ScanGeom g = scan_geom(batch * p->L, p->V, p->M);
   a.L = p->L;
   a.M = p->M;
-  a.B = p->B;
-  a.k = p->k;
+  a.B = mode.B > 0 ? mode.B : p->B;
+  a.k = mode.k > 0 ? mode.k : p->k;
+  a.nocorr = mode.nocorr;
+  a.emit = mode.emit;
+  a.skip_merge = mode.skip_merge;
+  a.menu_in = mode.menu_in;
+  a.menu_out = mode.menu_out;
   a.dh = p->d_h;
   a.G = expand_group_size(p->d_h, p->num_cus, batch);
   a.norm_mode = p->norm_mode;
@@ -1387,26 +1427,31 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.rflag = ws.row_flag;
   a.P_all = p->P_all;
   a.U_all = p->U_all;
-  a.c_all = p->c_all;
+  // (the marginals carry no E[v] . b_c term)
+  a.c_all = (mode.nocorr && !mode.menu_in) ? nullptr : p->c_all;
   a.whh = p->whh_t;
   a.b_hh = p->b_hh;
   a.h0 = h0;
   a.states = ws.states;
   a.part = ws.part;
-  a.bar = ws.bar;
+  a.bar = mode.bar ? mode.bar : ws.bar;
   a.out = *out;
   const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks, p->L);
   // shapes with a compiled specialisation: Qwen3 drafters (d_h = 512, M = 64,
   // L = 16) with bf16 weights at G = 16 (one to eight trees) and G = 8
   const void *fn;
-  if (p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16 && a.G == 16)
-    fn = (const void *)expand_kernel<uint16_t, 512, 16, 64, 16>;
+  const bool arms = mode.nocorr || mode.menu_in || mode.menu_out || !mode.emit || mode.skip_merge;
+  if (arms)
+    fn = p->wdt == DT_BF16 ? (const void *)expand_kernel<uint16_t, 0, 0, 0, 0, true>
+                           : (const void *)expand_kernel<float, 0, 0, 0, 0, true>;
+  else if (p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16 && a.G == 16)
+    fn = (const void *)expand_kernel<uint16_t, 512, 16, 64, 16, false>;
   else if (p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16 && a.G == 8)
-    fn = (const void *)expand_kernel<uint16_t, 512, 8, 64, 16>;
+    fn = (const void *)expand_kernel<uint16_t, 512, 8, 64, 16, false>;
   else if (p->wdt == DT_BF16)
-    fn = (const void *)expand_kernel<uint16_t, 0, 0, 0, 0>;
+    fn = (const void *)expand_kernel<uint16_t, 0, 0, 0, 0, false>;
   else
-    fn = (const void *)expand_kernel<float, 0, 0, 0, 0>;
+    fn = (const void *)expand_kernel<float, 0, 0, 0, 0, false>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   // G > 1: the grid is at most one workgroup per CU (expand_group_size), so

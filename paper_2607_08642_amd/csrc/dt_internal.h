@@ -79,7 +79,7 @@ struct ScanGeom {
 }  // namespace dt
 
 struct dt_plan {
-  int V, d_e, d_h, L, M, B, k, norm_mode, pos_offset;
+  int V, d_e, d_h, L, M, B, k, norm_mode, pos_offset, scorer;
   int wdt, ldt, max_batch;
   const void *emb;
   void *wfold;      // [nf_pad, d_e] (weights dtype): rows [0,3dh) = W_ih, [3dh,4dh) = W_c^T;
@@ -114,7 +114,10 @@ struct Workspace {
   // expansion
   float *states;          // [batch][ecap][dh]
   float *part;            // [batch][2][G][16][MP] partial corrections
-  int32_t *bar;           // [batch][kBarStride] barrier counters
+  int32_t *bar;           // [2][batch + 2][kBarStride] barrier and slot counters (one set
+                          // per expansion launch of a call)
+  float *menus;           // [batch][L][MP] corrected menus of the greedy chain (scorer
+                          // DT_SCORER_STATIC)
   int ecap;
   size_t bytes;
 };
@@ -134,9 +137,22 @@ hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, fl
                               hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s);
 hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
+// One expansion launch: DominoTree (the default), or, for the ablation arms,
+// without the correction (nocorr: the marginals, or menu_in's per-depth menus)
+// and/or writing every expanded depth's menu (menu_out; the greedy chain).
+struct ExpMode {
+  int nocorr = 0;                 // no GRU, no correction, no exchange
+  const float *menu_in = nullptr;  // [batch][L][MP] normalised log-probs of each depth's slots
+  float *menu_out = nullptr;       // written from every expanded node (a chain: one per depth)
+  int emit = 1;                   // 0: no replay or emission (outputs untouched)
+  int skip_merge = 0;             // the rows were merged by an earlier launch of the call
+  int k = 0, B = 0;               // 0: the plan's
+  int32_t *bar = nullptr;         // this launch's counters (zeroed), nullptr: ws.bar
+};
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s,
-                         hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+                         hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
+                         const ExpMode &mode = ExpMode());
 int expand_group_size(int d_h, int num_cus, int batch);
 size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L);
 size_t expand_part_bytes(const dt_plan *p, int batch);

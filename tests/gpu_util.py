@@ -27,7 +27,7 @@ def to_dev(a: np.ndarray, dtype: int, device="cuda"):
 
 
 class DeviceWorkload:
-    def __init__(self, wl, max_children=0, norm_mode=0, pos_offset=0):
+    def __init__(self, wl, max_children=0, norm_mode=0, pos_offset=0, scorer=0):
         w = wl.weights
         self.wl = wl
         d = synth.DT_BF16 if w.dtype == synth.DT_BF16 else synth.DT_F32
@@ -43,8 +43,9 @@ class DeviceWorkload:
         self.plan = binding.Plan(self.emb, self.w_ih, self.w_hh, self.b_ih, self.b_hh, self.w_c,
                                  self.b_c, L=wl.L, M=wl.M, B=wl.B, logits_dtype=wl.logits_dtype,
                                  max_batch=wl.batch, max_children=max_children,
-                                 norm_mode=norm_mode, pos_offset=pos_offset)
-        self.kw = dict(max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset)
+                                 norm_mode=norm_mode, pos_offset=pos_offset, scorer=scorer)
+        self.kw = dict(max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset,
+                       scorer=scorer)
 
     def run(self):
         tree = self.plan.build_tree(self.logits, self.wl.T, self.h0)
@@ -81,7 +82,7 @@ def compare_tree(wl, t, got, kw, tol=None):
         return "exact", err
     # ambiguous seed: the GPU tree must be a valid best-first tree within tolerance
     g, valid = rescore(wl, t, tok, par, n, max_children=kw.get("max_children", 0),
-                       norm_mode=kw.get("norm_mode", 0))
+                       norm_mode=kw.get("norm_mode", 0), scorer=kw.get("scorer", 0))
     assert valid, f"tree {t}: a GPU node is not a top-k child of its parent"
     err = float(np.max(np.abs(sc[:n] - g)))
     assert err <= tol, f"tree {t}: rescored error {err}"

@@ -66,6 +66,30 @@ SWEEP = [
 ]
 
 
+# the ablation arms (Appendix D): Marg (scorer 1) and Cond-static (scorer 2)
+ARM_CASES = [c for c in SWEEP if c[0] in (2, 3, 5, 9, 12, 13, 14)]
+
+
+@pytest.mark.parametrize("scorer", [1, 2], ids=["marg", "static"])
+@pytest.mark.parametrize("case", ARM_CASES, ids=[f"s{c[0]}" for c in ARM_CASES])
+def test_ablation_arms(case, scorer):
+    seed, batch, L, V, M, B, T, d_e, d_h, dt, kw, extra = case
+    wl = synth.random_small(seed, batch=batch, L=L, V=V, M=M, B=B, T=T, d_e=d_e, d_h=d_h,
+                            dtype=dt, **extra)
+    # (path-independent menus over bf16 logits tie exactly more often: a tree
+    # with a tie is checked as a valid best-first tree within tolerance)
+    run_case(wl, name=f"arm{scorer}-s{seed}", scorer=scorer, **kw)
+
+
+@pytest.mark.parametrize("scorer", [1, 2], ids=["marg", "static"])
+def test_ablation_arms_qwen_shape(scorer):
+    wl = synth.WORKLOADS["qwen3_8b"]()
+    kinds, _ = run_case(wl, name=f"arm{scorer}-qwen3_8b", scorer=scorer)
+    # Marg's shared menus of bf16 logits hold exact ties here (checked as a valid
+    # best-first tree within tolerance); the corrected menus of Cond-static do not
+    assert kinds[0][0] == "exact" or scorer == 1
+
+
 @pytest.mark.parametrize("case", SWEEP, ids=[f"s{c[0]}" for c in SWEEP])
 def test_random_sweep(case):
     seed, batch, L, V, M, B, T, d_e, d_h, dt, kw, extra = case
