@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILES = os.path.join(ROOT, "profiles")
+SCORERS = {"cond": 0, "marg": 1, "static": 2}
 PROFILE_EVERY = 8   # kernel start/end events on every 8th eager call
 
 
@@ -45,6 +46,8 @@ def parse():
                     help="logit bytes cycled through in the timed loop")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--scorer", default="cond", choices=list(SCORERS),
+                    help="children function: cond (DominoTree), marg or static (the ablation arms)")
     ap.add_argument("--eager", action="store_true",
                     help="time the K calls launched one by one instead of one HIP-graph replay")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -86,7 +89,7 @@ def traffic_from_profiles(workload, stage):
         return None
 
 
-def cpu_baseline(wl_name, wl, bufs_host, seconds):
+def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0):
     """The oracle as it stands, one BLAS thread, on trees of the same workload."""
     import numpy as np
     from threadpoolctl import threadpool_limits
@@ -102,7 +105,7 @@ def cpu_baseline(wl_name, wl, bufs_host, seconds):
             buf = bufs_host[(n // wl.batch) % len(bufs_host)]
             t = n % wl.batch
             oracle.build_tree(buf[t], w.emb, w.dtype, wd, None if wl.h0 is None else wl.h0[t],
-                              wl.M, wl.B, wl.T, logits_dtype=wl.logits_dtype)
+                              wl.M, wl.B, wl.T, logits_dtype=wl.logits_dtype, scorer=scorer)
             n += 1
             el = time.perf_counter() - t0
             if el >= seconds and n >= 3:
@@ -141,7 +144,8 @@ def main():
     emb = up(w.emb, d)
     plan = binding.Plan(emb, up(w.w_ih, d), up(w.w_hh, d), up(w.b_ih, d), up(w.b_hh, d),
                         up(w.w_c, d), up(w.b_c, d), L=wl.L, M=wl.M, B=wl.B,
-                        logits_dtype=wl.logits_dtype, max_batch=wl.batch)
+                        logits_dtype=wl.logits_dtype, max_batch=wl.batch,
+                        scorer=SCORERS[args.scorer])
     per_buf = wl.logits.nbytes
     nbuf = max(1, math.ceil(args.rotate_mb * 2**20 / per_buf))
     bufs_host = [wl.logits] + [synth.logits_buffer(wl.name, i, wl.batch) for i in range(1, nbuf)]
@@ -230,7 +234,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if d == synth.DT_BF16 else "f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "batch": wl.batch, "L": wl.L, "V": w.V, "M": wl.M,
+        "config": {"workload": wl.name if args.scorer == "cond" else f"{wl.name}-{args.scorer}",
+                   "scorer": args.scorer, "batch": wl.batch, "L": wl.L, "V": w.V, "M": wl.M,
                    "B": wl.B, "T": wl.T, "d_e": w.d_e, "d_h": w.d_h, "logit_buffers": nbuf},
         "timing": "eager" if args.eager else "hip_graph",
         "us_per_tree": wall / trees * 1e6,
@@ -256,7 +261,8 @@ def main():
         torch.cuda.synchronize()
 
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds,
+                                           SCORERS[args.scorer])
     plan.close()
     print(json.dumps(res), flush=True)
 
