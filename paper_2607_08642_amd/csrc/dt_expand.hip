@@ -634,6 +634,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     typename Gates<TW>::Pre wpre;
     const bool wearly = !a.nocorr && Gates<TW>::kPre > 0 && use_pin && d > 0 && gu >= 0 &&
                         gk1 - gk0 <= Gates<TW>::kPre;
+    // the root with no h0: its state is zero, so U . S = 0 and the correction is
+    // the E[v] . b_c the row merge already added -- no exchange
+    const bool nocorr = a.nocorr || (d == 0 && a.h0 == nullptr);
     if (wearly) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);
     if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
     {
@@ -668,7 +671,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         }
       }
       // this member's U slice of depth d's candidates, straight into LDS
-      if (a.use_us && d < L && !a.nocorr) {
+      if (a.use_us && d < L && !nocorr) {
         const __amdgpu_buffer_rsrc_t ru =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.U_all), 0, 0x7FFFFFF0, 0x00020000);
         for (int i = wave; i < MP * UW / 256; i += NW) {
@@ -704,7 +707,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     }
     __syncthreads();
     // 1. path states of this member's units: S = GRU(S_parent, E[token]) (section 2.3)
-    if (a.nocorr) {
+    if (nocorr) {
       // (no path states without the correction)
     } else if (d == 0) {
       for (int u = tid; u < UW; u += NT) {
@@ -831,7 +834,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // parts of member j: a [CH][MP] block of their own (no line is shared by two writers)
     const __amdgpu_buffer_rsrc_t rmy =
         dev_rsrc(a.part + (((size_t)t * 2 + pb) * G + member) * CH * MP);
-    for (int rt = a.nocorr ? RT : wave; rt < RT; rt += NW) {
+    for (int rt = nocorr ? RT : wave; rt < RT; rt += NW) {
       const int m = rt * 16 + (lane & 15);
       const int c = lane & 15, kq = (lane >> 4) * 4;
       const float *urow = a.U_all + (size_t)(m < M ? ccand[m] : 0) * dh + member * UW;
@@ -853,7 +856,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
                  make_float4(acc[0], acc[1], acc[2], acc[3]));
     }
-    if (!a.nocorr) group_barrier(ctr, G, nbar, &scal[S_STATUS]);
+    if (!nocorr) group_barrier(ctr, G, nbar, &scal[S_STATUS]);
     // 3. children of each node: normalise, rank, keep the top-k above vB
     const float vB = scalf[S_VB];
     const float R = scalf[S_R];
@@ -891,7 +894,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           const int m = lane + 64 * s;
           // x already holds logit + E[v] . b_c (added by the row merge; not for the marginals)
           const float x = ccandv[m];
-          const float dl = a.nocorr ? x : x + sum_parts(s == 0 ? p0 : load_parts(c, s), lane);
+          const float dl = nocorr ? x : x + sum_parts(s == 0 ? p0 : load_parts(c, s), lane);
           const float z = x > NEG_INF ? dl * a.inv_tau : NEG_INF;  // slots >= M hold -inf
           zv[s] = z;
           mx = fmaxf(mx, z);
@@ -988,8 +991,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // two nodes per wave: the second node's loads are in flight during the first
     const int c0 = wave, c1 = wave + NW;
     Parts p0, p1;
-    if (c0 < nc && !a.nocorr) p0 = load_parts(c0, 0);
-    if (c1 < nc && !a.nocorr) p1 = load_parts(c1, 0);
+    if (c0 < nc && !nocorr) p0 = load_parts(c0, 0);
+    if (c1 < nc && !nocorr) p1 = load_parts(c1, 0);
     if (c0 < nc)
       node_children(c0, p0);
     else if (lane == 0)
