@@ -9,6 +9,7 @@ from .dominotree_ref import (  # noqa: F401
     NORM_SLICE,
     NORM_TAIL,
     SCORER_COND,
+    SCORER_HEAD,
     SCORER_MARG,
     SCORER_STATIC,
     TREE_NONFINITE,
@@ -19,6 +20,7 @@ from .dominotree_ref import (  # noqa: F401
     logsumexp,
     scan,
     scan_row,
+    silu,
     score_paths,
     widen,
 )

@@ -26,6 +26,10 @@ own order:
   STATIC applies the correction once per depth, from the state of the greedy
   chain (Domino's own decoder: at each depth the best corrected child), and
   shares that corrected menu with every node of the depth.
+* HEAD is Domino's own correction head (section 2.3): a rank-r bottleneck
+  over the concatenation of the drafter's hidden state at the position and
+  the path state, delta = W_2 SiLU(W_1 [H_d; S]), with W_2's rows gathered
+  for the depth's slice.  The paper prints no biases, so there are none.
 
 Readings of the paper that this file fixes (the paper is silent on them):
 
@@ -62,6 +66,7 @@ NORM_SLICE = 1
 SCORER_COND = 0    # DominoTree: the correction recomputed from each node's own path state
 SCORER_MARG = 1    # Marg: marginal logits only
 SCORER_STATIC = 2  # Cond-static: the correction along the greedy chain, one menu per depth
+SCORER_HEAD = 3    # Domino's rank-r SiLU head over [H_d; S], recomputed per node
 TREE_NONFINITE = 0x1
 
 DT_F32 = 0
@@ -124,6 +129,11 @@ def sigmoid(a: np.ndarray) -> np.ndarray:
     return 1.0 / (1.0 + np.exp(-a))
 
 
+def silu(a: np.ndarray) -> np.ndarray:
+    """SiLU(a) = a * sigmoid(a), the head's nonlinearity (section 2.3)."""
+    return a * sigmoid(a)
+
+
 def gru_cell(h: np.ndarray, xs: np.ndarray, w_ih, w_hh, b_ih, b_hh) -> np.ndarray:
     """Advance state h [d_h] by each input row of xs [k, d_in]; returns [k, d_h].
 
@@ -154,7 +164,7 @@ def gru_cell(h: np.ndarray, xs: np.ndarray, w_ih, w_hh, b_ih, b_hh) -> np.ndarra
 class _Model:
     """float64 copies of the weights plus the per-depth candidate tables."""
 
-    def __init__(self, X, emb, emb_dtype, w, M, tau, norm_mode, scorer=SCORER_COND):
+    def __init__(self, X, emb, emb_dtype, w, M, tau, norm_mode, scorer=SCORER_COND, H=None):
         self.L = X.shape[0]
         self.M = M
         self.tau = tau
@@ -175,16 +185,29 @@ class _Model:
             self.xc.append(xs)
             self.R.append(R)
             self.Ec.append(widen(np.asarray(emb)[ids], emb_dtype))
+        if scorer == SCORER_HEAD:
+            # section 2.3: W_1 acts on [H_d; S]; its H half is path-independent,
+            # so a_d = W_1^H H_d once per depth; W_2's rows for the slice
+            w1 = widen(w["w1"], w["dtype"])
+            d_H = w1.shape[1] - self.w_hh.shape[1]
+            Hd = widen(H, w["dtype"])
+            self.w1s = w1[:, d_H:]
+            self.a = [w1[:, :d_H] @ Hd[d] for d in range(self.L)]
+            self.W2c = [widen(np.asarray(w["w2"])[ids], w["dtype"]) for ids in self.cand]
 
     def slot_logprobs(self, S: Optional[np.ndarray], d: int):
         """Corrected, normalised log-probs of depth d's slice given path state S.
 
-        delta_m = E[cand_d[m]] . (W_c S + b_c);  z = (x + delta) / tau;
-        ell = z - logZ.  S = None: no correction (delta = 0, the marginals).
+        delta_m = E[cand_d[m]] . (W_c S + b_c) (HEAD: W_2[cand_d[m]] .
+        SiLU(a_d + W_1^S S));  z = (x + delta) / tau;  ell = z - logZ.
+        S = None: no correction (delta = 0, the marginals).
         Returns (ell[M] with -inf for dead slots, live mask).
         """
         if S is None:
             delta = np.zeros(self.M)
+        elif self.scorer == SCORER_HEAD:
+            y = silu(self.a[d - 1] + self.w1s @ S)
+            delta = self.W2c[d - 1] @ y
         else:
             q = self.w_c @ S
             if self.b_c is not None:
@@ -240,7 +263,7 @@ class _Model:
         if not kept:
             return []
         tokens = [int(self.cand[d - 1][m]) for m in kept]
-        if self.scorer != SCORER_COND:
+        if self.scorer not in (SCORER_COND, SCORER_HEAD):
             return [(tokens[i], float(ell[m]), m, None) for i, m in enumerate(kept)]
         states = gru_cell(S, self.Ec[d - 1][kept], self.w_ih, self.w_hh, self.b_ih, self.b_hh)
         return [(tokens[i], float(ell[m]), m, states[i]) for i, m in enumerate(kept)]
@@ -264,11 +287,12 @@ def _empty_tree(B: int, pos_offset: int, status: int):
 def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                h0: Optional[np.ndarray], M: int, B: int, T: float,
                max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
-               logits_dtype: int = DT_F32, scorer: int = SCORER_COND):
+               logits_dtype: int = DT_F32, scorer: int = SCORER_COND, H: Optional[np.ndarray] = None):
     """Build one draft tree (Alg. 1) and emit it in pop order.
 
     X: [L, V] stored marginal logits of one tree; emb: [V, d_e]; weights: dict
-    with w_ih, w_hh, b_ih, b_hh, w_c, b_c, dtype; h0: [d_h] or None (zeros).
+    with w_ih, w_hh, b_ih, b_hh, w_c, b_c, dtype (HEAD: also w1 [r, d_H + d_h]
+    and w2 [V, r]); h0: [d_h] or None (zeros); H: [L, d_H], HEAD only.
     Returns a dict of emitted arrays plus the smallest decisive score gap.
     """
     Xd = widen(X, logits_dtype)
@@ -276,7 +300,7 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
         return _empty_tree(B, pos_offset, TREE_NONFINITE)
     tau = effective_temperature(T)
     k = min(M, B) if max_children <= 0 else min(max_children, M)
-    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode, scorer)
+    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode, scorer, H)
     L = model.L
     d_h = model.w_hh.shape[1]
     S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
@@ -330,11 +354,13 @@ def _emit(tree, B: int, pos_offset: int, min_gap: float):
 def build_trees(logits: np.ndarray, logits_dtype: int, emb: np.ndarray, emb_dtype: int,
                 weights: dict, h0: Optional[np.ndarray], M: int, B: int, T: float,
                 max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
-                trees: Optional[Sequence[int]] = None, scorer: int = SCORER_COND):
-    """build_tree over the batch (or the listed tree indices)."""
+                trees: Optional[Sequence[int]] = None, scorer: int = SCORER_COND,
+                H: Optional[np.ndarray] = None):
+    """build_tree over the batch (or the listed tree indices); H: [b, L, d_H]."""
     idx = range(logits.shape[0]) if trees is None else trees
     return [build_tree(logits[t], emb, emb_dtype, weights, None if h0 is None else h0[t],
-                       M, B, T, max_children, norm_mode, pos_offset, logits_dtype, scorer)
+                       M, B, T, max_children, norm_mode, pos_offset, logits_dtype, scorer,
+                       None if H is None else H[t])
             for t in idx]
 
 
@@ -353,7 +379,7 @@ def scan(logits: np.ndarray, logits_dtype: int, M: int, T: float):
 def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                 h0: Optional[np.ndarray], M: int, B: int, T: float, tokens, parents, n_nodes: int,
                 max_children: int = 0, norm_mode: int = NORM_TAIL, logits_dtype: int = DT_F32,
-                scorer: int = SCORER_COND):
+                scorer: int = SCORER_COND, H: Optional[np.ndarray] = None):
     """Re-score a given tree with the oracle's Children function.
 
     Returns (g[n], valid): valid is False when a node's token is not among the
@@ -362,7 +388,7 @@ def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     Xd = widen(X, logits_dtype)
     tau = effective_temperature(T)
     k = min(M, B) if max_children <= 0 else min(max_children, M)
-    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode, scorer)
+    model = _Model(Xd, emb, emb_dtype, weights, M, tau, norm_mode, scorer, H)
     d_h = model.w_hh.shape[1]
     S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
     if scorer == SCORER_STATIC:

@@ -37,6 +37,7 @@ QWEN3_VOCAB = 151936
 
 # tensor tags for SeedSequence
 TAG_LOGITS, TAG_EMB, TAG_WIH, TAG_WHH, TAG_BIH, TAG_BHH, TAG_WC, TAG_BC, TAG_H0, TAG_SPIKE = range(10)
+TAG_W1, TAG_W2, TAG_HID = 10, 11, 12
 
 DT_F32 = 0
 DT_BF16 = 1
@@ -207,6 +208,33 @@ WORKLOADS = {
     "budget64": budget64,
     "concurrent": concurrent,
 }
+
+
+@dataclasses.dataclass
+class DominoHead:
+    """Domino's own correction head (section 2.3): rank-r bottleneck with SiLU."""
+    w1: np.ndarray   # [rank, d_H + d_h]  Linear(d_H + d_h -> rank).weight; columns [0, d_H) take H
+    w2: np.ndarray   # [V, rank]          Linear(rank -> V).weight
+    dtype: int
+    d_H: int
+    rank: int
+
+
+def domino_head(seed: int, V: int, d_H: int, d_h: int, rank: int, dtype: int,
+                w1_scale: Optional[float] = None, w2_scale: Optional[float] = None,
+                threads: int = 8) -> DominoHead:
+    """Uniform weights at PyTorch Linear's fan-in scale unless scales are given."""
+    s1 = 1.0 / np.sqrt(d_H + d_h) if w1_scale is None else w1_scale
+    s2 = 1.0 / np.sqrt(rank) if w2_scale is None else w2_scale
+    w1 = _table(seed, TAG_W1, rank, d_H + d_h, "uniform", s1, dtype, threads=threads)
+    w2 = _table(seed, TAG_W2, V, rank, "uniform", s2, dtype, threads=threads)
+    return DominoHead(w1, w2, dtype, d_H, rank)
+
+
+def hidden_states(seed: int, batch: int, L: int, d_H: int, dtype: int, std: float = 1.0) -> np.ndarray:
+    """[batch, L, d_H] drafter hidden states H_d, standard normal times std."""
+    h = _rng(seed, TAG_HID, 0).standard_normal((batch, L, d_H), dtype=np.float32) * np.float32(std)
+    return _as_dtype(h, dtype)
 
 
 def random_small(seed: int, *, batch: int, L: int, V: int, M: int, B: int, T: float,

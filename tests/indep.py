@@ -212,3 +212,36 @@ def frontier_tree(sc: TorchScorer, B: int, k: int, W: Optional[int] = None):
             break
     items = sorted(ledger.items(), key=lambda kv: -kv[1])[:B]
     return {p for p, _ in items}
+
+
+class HeadTorchScorer(TorchScorer):
+    """The same full-vocabulary scorer with Domino's own head (section 2.3):
+    delta = W_2 SiLU(W_1 [H_d; S]) over every token, torch.nn.functional.silu."""
+
+    def __init__(self, X, logits_dtype, w, head, H, h0, M, T, norm_slice=False):
+        super().__init__(X, logits_dtype, w, h0, M, T, norm_slice)
+        self.W1 = _f64(head.w1, head.dtype)
+        self.W2 = _f64(head.w2, head.dtype)
+        self.H = _f64(H, head.dtype)
+
+    def logprobs(self, S, d) -> Dict[int, float]:
+        with torch.no_grad():
+            hs = torch.cat([self.H[d - 1], S])
+            delta = self.W2 @ torch.nn.functional.silu(torch.nn.functional.linear(hs, self.W1))
+            sl = torch.tensor(self.slices[d - 1])
+            y = self.X[d - 1].clone()
+            y[sl] = y[sl] + delta[sl]
+            if self.norm_slice:
+                lp = torch.log_softmax(y[sl] / self.tau, dim=0)
+                out = {int(t): float(v) for t, v in zip(sl.tolist(), lp.tolist())}
+            else:
+                lp = torch.log_softmax(y / self.tau, dim=0)
+                out = {int(t): float(lp[t]) for t in sl.tolist()}
+        return {t: v for t, v in out.items() if self.X[d - 1, t] > -math.inf}
+
+
+def menu_tree(sc: TorchScorer, B: int, k: int, S):
+    """DDTree's heap when every node of depth d is offered the same menu, the
+    top-k children of state S at that depth (a path-independent scorer)."""
+    menus = [sc.ranked_children(S, d, k) for d in range(1, sc.L + 1)]
+    return _menu_heap(menus, B, sc.L)
