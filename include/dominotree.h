@@ -210,6 +210,41 @@ dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, in
                        int32_t *ids, float *vals, float *tail_lse, int32_t *row_flags,
                        void *workspace, size_t ws_bytes, void *stream);
 
+/* Domino's own correction head (section 2.3): a rank-r bottleneck with SiLU
+ * over the drafter's hidden state at the position and the path state,
+ *   delta_m = W_2[cand_d[m]] . SiLU(W_1 [H_d; S])      (no biases)
+ * which replaces the linear head's E[v] . (W_c S + b_c) in the scoring above.
+ *   w1: [rank, d_H + d_h] (a Linear(d_H + d_h -> rank) weight; columns
+ *       [0, d_H) act on H_d, the rest on S);
+ *   w2: [V, rank] (a Linear(rank -> V) weight; row v is gathered for token v);
+ * both device pointers in the plan's weights dtype, 16-byte aligned,
+ * caller-owned and read by every dt_build_tree_head call.
+ * 8 <= d_H <= 8192 and 8 <= rank <= 1024, both multiples of 8. */
+typedef struct {
+  const void *w1, *w2;
+  int d_H, rank;
+} dt_domino_head;
+
+/* Workspace (bytes) dt_build_tree_head needs for `batch` trees with this head. */
+dt_status dt_head_workspace_size(const dt_plan *plan, int batch, const dt_domino_head *head,
+                                 size_t *bytes);
+
+/* Build `batch` draft trees (Alg. 1) scored with Domino's own head.
+ *   H: [batch, L, d_H] drafter hidden states (the plan's weights dtype,
+ *      16-byte aligned); row d scores the children at depth d + 1, the same
+ *      depth as logits row d;
+ *   the other arguments are those of dt_build_tree; the plan's linear head
+ *   (dt_head) is not used, its GRU is.
+ * One workgroup builds each tree, popping the heap one node at a time.
+ * Envelope beyond dt_plan_create's: M <= 64; the scan's segments per row
+ * <= 16 (true for V <= 163840 at any batch); k * (B + 1) <= 4096; the plan
+ * created with DT_SCORER_COND; the kernel's LDS must fit the device.
+ * DT_ERR_UNSUPPORTED otherwise.  Stream-ordered and capturable like
+ * dt_build_tree (three kernels, no memset or copy). */
+dt_status dt_build_tree_head(dt_plan *plan, const void *marginal_logits, int batch, const void *H,
+                             const dt_domino_head *head, const float *h0, float T,
+                             void *workspace, size_t ws_bytes, dt_tree *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

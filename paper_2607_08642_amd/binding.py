@@ -33,7 +33,8 @@ STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
 # every symbol include/dominotree.h declares
 EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_create",
            "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
-           "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm")
+           "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm", "dt_head_workspace_size",
+           "dt_build_tree_head")
 STAGES = ("scan", "expand")
 
 
@@ -50,6 +51,11 @@ class dt_gru(ctypes.Structure):
 
 class dt_head(ctypes.Structure):
     _fields_ = [("w", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+class dt_domino_head(ctypes.Structure):
+    _fields_ = [("w1", ctypes.c_void_p), ("w2", ctypes.c_void_p), ("d_H", ctypes.c_int),
+                ("rank", ctypes.c_int)]
 
 
 class dt_options(ctypes.Structure):
@@ -97,6 +103,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dt_scan_workspace_size.restype = ci
     lib.dt_scan_workspace_size.argtypes = [ci, ci, ci, ctypes.POINTER(sz)]
     lib.dt_scan_topm.restype = ci
+    lib.dt_head_workspace_size.restype = ci
+    lib.dt_head_workspace_size.argtypes = [vp, ci, ctypes.POINTER(dt_domino_head), ctypes.POINTER(sz)]
+    lib.dt_build_tree_head.restype = ci
+    lib.dt_build_tree_head.argtypes = [vp, vp, ci, vp, ctypes.POINTER(dt_domino_head), vp, cf, vp,
+                                       sz, ctypes.POINTER(dt_tree), vp]
     lib.dt_scan_topm.argtypes = [vp, ci, ci, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
     if lib.dt_abi_version() != ABI_VERSION:
         raise RuntimeError(f"ABI mismatch: library {lib.dt_abi_version()} vs binding {ABI_VERSION}")
@@ -212,6 +223,39 @@ class Plan:
         st = self._lib.dt_build_tree(self.handle, logits.data_ptr(), batch,
                                      None if h0 is None else h0.data_ptr(), T, ws.data_ptr(),
                                      ws.numel(), ctypes.byref(out.as_c()), _stream(stream))
+        if st != 0:
+            _check(st)
+        return out
+
+    def _head(self, w1, w2) -> dt_domino_head:
+        rank, width = w1.shape
+        return dt_domino_head(_ptr(w1), _ptr(w2), width - self.d_h, rank)
+
+    def head_workspace_size(self, batch: int, w1, w2) -> int:
+        n = ctypes.c_size_t()
+        hd = self._head(w1, w2)
+        _check(self._lib.dt_head_workspace_size(self.handle, batch, ctypes.byref(hd), ctypes.byref(n)))
+        return n.value
+
+    def build_tree_head(self, logits, H, w1, w2, T: float, h0=None, out: Optional[Tree] = None,
+                        workspace=None, stream=None) -> Tree:
+        """dt_build_tree_head (Domino's own head: w1 [rank, d_H + d_h], w2 [V, rank],
+        H [b, L, d_H], all in the weights dtype) on torch's current stream."""
+        import torch
+        batch = logits.shape[0]
+        if out is None:
+            out = Tree.empty(batch, self.B, logits.device)
+        hd = self._head(w1, w2)
+        if workspace is None:
+            key = ("head", batch, hd.rank)
+            if key not in self._ws:
+                self._ws[key] = torch.empty(self.head_workspace_size(batch, w1, w2),
+                                            dtype=torch.uint8, device=logits.device)
+            workspace = self._ws[key]
+        st = self._lib.dt_build_tree_head(self.handle, logits.data_ptr(), batch, H.data_ptr(),
+                                          ctypes.byref(hd), None if h0 is None else h0.data_ptr(),
+                                          T, workspace.data_ptr(), workspace.numel(),
+                                          ctypes.byref(out.as_c()), _stream(stream))
         if st != 0:
             _check(st)
         return out

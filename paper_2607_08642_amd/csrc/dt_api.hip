@@ -8,6 +8,7 @@
 #include <string>
 
 #include "dt_internal.h"
+#include "dt_select.h"
 
 namespace {
 
@@ -166,6 +167,10 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (e == hipSuccess) e = hipMalloc(&p->b_hh, sizeof(float) * 3 * d_h);
   if (e == hipSuccess) e = hipMalloc(&p->b_c, sizeof(float) * d_e);
   if (e == hipSuccess) e = hipMalloc(&p->whh_t, (size_t)3 * d_h * d_h * ws);
+  if (e == hipSuccess) e = hipMalloc(&p->whh_rm, (size_t)3 * d_h * d_h * ws);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(p->whh_rm, gru->w_hh, (size_t)3 * d_h * d_h * ws, hipMemcpyDeviceToDevice,
+                       nullptr);
   if (e == hipSuccess) e = hipMalloc(&p->P_all, (size_t)V * 3 * d_h * sizeof(float));
   if (e == hipSuccess) e = hipMalloc(&p->U_all, (size_t)V * d_h * sizeof(float));
   if (e == hipSuccess) e = hipMalloc(&p->c_all, (size_t)V * sizeof(float));
@@ -232,6 +237,7 @@ void dt_plan_destroy(dt_plan *p) {
   if (p->b_hh) (void)hipFree(p->b_hh);
   if (p->b_c) (void)hipFree(p->b_c);
   if (p->whh_t) (void)hipFree(p->whh_t);
+  if (p->whh_rm) (void)hipFree(p->whh_rm);
   if (p->P_all) (void)hipFree(p->P_all);
   if (p->U_all) (void)hipFree(p->U_all);
   if (p->c_all) (void)hipFree(p->c_all);
@@ -348,6 +354,75 @@ dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, in
   hipError_t e = dt::launch_scan_chunks(logits, logits_dtype, g, inv_tau, ws, nullptr, 0, s);
   if (e == hipSuccess) e = dt::launch_scan_merge(g, inv_tau, ws, s);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
+  return DT_OK;
+}
+
+// checks shared by dt_head_workspace_size and dt_build_tree_head
+static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head *hd) {
+  if (!plan || !hd) return fail(DT_ERR_NULL, "plan and head are required");
+  if (!hd->w1 || !hd->w2) return fail(DT_ERR_NULL, "head.w1 and head.w2 are required");
+  if (batch < 1 || batch > plan->max_batch)
+    return fail(DT_ERR_SHAPE, "batch %d outside [1, max_batch=%d]", batch, plan->max_batch);
+  if (hd->d_H < 8 || hd->d_H > 8192 || hd->d_H % 8 != 0 || hd->rank < 8 || hd->rank > 1024 ||
+      hd->rank % 8 != 0)
+    return fail(DT_ERR_SHAPE, "need 8 <= d_H <= 8192 and 8 <= rank <= 1024, multiples of 8 (d_H=%d rank=%d)",
+                hd->d_H, hd->rank);
+  if (plan->scorer != DT_SCORER_COND)
+    return fail(DT_ERR_UNSUPPORTED, "the Domino head needs a plan created with DT_SCORER_COND");
+  const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
+  if (!dt::sel::wave_merge_fits(g.nchunks, plan->M))
+    return fail(DT_ERR_UNSUPPORTED, "the Domino head needs M <= 64 and <= 16 scan segments per row (M=%d, %d)",
+                plan->M, g.nchunks);
+  if ((size_t)plan->k * (plan->B + 1) > (size_t)dt::kHeadCap)
+    return fail(DT_ERR_UNSUPPORTED, "k * (B + 1) = %d exceeds the heap's %d entries",
+                plan->k * (plan->B + 1), dt::kHeadCap);
+  int dev = 0, maxlds = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  const size_t lds = dt::head_lds_bytes(plan->L, plan->B, plan->d_h, hd->rank);
+  if (lds > (size_t)maxlds || (size_t)4 * 4 * hd->d_H > (size_t)maxlds)
+    return fail(DT_ERR_UNSUPPORTED, "the Domino head needs %zu bytes of LDS, the device has %d", lds, maxlds);
+  return DT_OK;
+}
+
+dt_status dt_head_workspace_size(const dt_plan *plan, int batch, const dt_domino_head *head,
+                                 size_t *bytes) {
+  if (!bytes) return fail(DT_ERR_NULL, "bytes is required");
+  const dt_status st = head_check(plan, batch, head);
+  if (st != DT_OK) return st;
+  *bytes = dt::carve_head(plan, batch, head->rank, nullptr).bytes;
+  return DT_OK;
+}
+
+dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const void *H,
+                             const dt_domino_head *head, const float *h0, float T, void *workspace,
+                             size_t ws_bytes, dt_tree *out, void *stream) {
+  if (!plan || !logits || !H || !out) return fail(DT_ERR_NULL, "plan, logits, H and out are required");
+  if (!out->tokens || !out->parents || !out->depth || !out->position_ids || !out->mask ||
+      !out->scores || !out->n_nodes || !out->status)
+    return fail(DT_ERR_NULL, "every dt_tree output pointer is required");
+  const dt_status st = head_check(plan, batch, head);
+  if (st != DT_OK) return st;
+  if (!(T == T)) return fail(DT_ERR_SHAPE, "temperature is NaN");
+  const size_t need = dt::carve_head(plan, batch, head->rank, nullptr).bytes;
+  if (!workspace || ws_bytes < need)
+    return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
+  if (!aligned(workspace, 256)) return fail(DT_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (!aligned(head->w1, 16) || !aligned(head->w2, 16) || !aligned(H, 16))
+    return fail(DT_ERR_ALIGN, "head.w1, head.w2 and H must be 16-byte aligned");
+  if (!aligned(logits, dsize(plan->ldt)) || (h0 && !aligned(h0, 4)) || !aligned(out->tokens, 4) ||
+      !aligned(out->parents, 4) || !aligned(out->depth, 4) || !aligned(out->position_ids, 4) ||
+      !aligned(out->scores, 4) || !aligned(out->n_nodes, 4) || !aligned(out->status, 4))
+    return fail(DT_ERR_ALIGN, "logits and outputs must be naturally aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
+  const dt::HeadWorkspace hw = dt::carve_head(plan, batch, head->rank, static_cast<char *>(workspace));
+  const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
+  hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hw.scan, nullptr, 0, s);
+  if (e != hipSuccess) return hip_fail(e, "scan launch");
+  e = dt::launch_head(plan, batch, H, *head, h0, inv_tau, hw, out, s);
+  if (e != hipSuccess) return hip_fail(e, "head launch");
   return DT_OK;
 }
 

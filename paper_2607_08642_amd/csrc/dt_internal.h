@@ -93,6 +93,7 @@ struct dt_plan {
   float *b_c;       // [d_e] fp32 (zeros when absent)
   int has_bc;
   void *whh_t;      // W_hh in MFMA A-fragment order (see pack_whh_*_kernel)
+  void *whh_rm;     // [3dh][dh] W_hh as given (weights dtype), for the Domino-head path
   int num_cus;
   int profiling;            // > 0: record stage events on every profiling-th dt_build_tree call
   int calls_since;          // dt_build_tree calls since profiling was enabled
@@ -137,6 +138,20 @@ hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, fl
                               hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s);
 hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
+// Domino-head path (dt_build_tree_head): heap entries per tree, workspace, launch
+constexpr int kHeadCap = 4096;
+struct HeadWorkspace {
+  Workspace scan;  // scan segment lists (chunk_keys, chunk_tail, chunk_flag) and row arrays
+  float *a;        // [batch * L][rank] W_1^H H
+  float *states;   // [batch][B + 1][dh]
+  float *ghs;      // [batch][B + 1][3dh]
+  size_t bytes;
+};
+HeadWorkspace carve_head(const dt_plan *p, int batch, int rank, char *base);
+size_t head_lds_bytes(int L, int B, int dh, int rank);
+hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
+                       const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
+                       hipStream_t s);
 // One expansion launch: DominoTree (the default), or, for the ablation arms,
 // without the correction (nocorr: the marginals, or menu_in's per-depth menus)
 // and/or writing every expanded depth's menu (menu_out; the greedy chain).

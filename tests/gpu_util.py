@@ -40,15 +40,26 @@ class DeviceWorkload:
         self.b_c = to_dev(w.b_c, d)
         self.logits = to_dev(wl.logits, wl.logits_dtype)
         self.h0 = None if wl.h0 is None else torch.from_numpy(wl.h0.astype(np.float32)).cuda()
+        # (Domino's own head is a separate entry point of a DominoTree plan)
+        pscorer = 0 if scorer == oracle.SCORER_HEAD else scorer
         self.plan = binding.Plan(self.emb, self.w_ih, self.w_hh, self.b_ih, self.b_hh, self.w_c,
                                  self.b_c, L=wl.L, M=wl.M, B=wl.B, logits_dtype=wl.logits_dtype,
                                  max_batch=wl.batch, max_children=max_children,
-                                 norm_mode=norm_mode, pos_offset=pos_offset, scorer=scorer)
+                                 norm_mode=norm_mode, pos_offset=pos_offset, scorer=pscorer)
         self.kw = dict(max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset,
                        scorer=scorer)
 
     def run(self):
-        tree = self.plan.build_tree(self.logits, self.wl.T, self.h0)
+        if self.kw["scorer"] == oracle.SCORER_HEAD:
+            hd = self.wl.head
+            if not hasattr(self, "w1"):
+                self.w1 = to_dev(hd.w1, hd.dtype)
+                self.w2 = to_dev(hd.w2, hd.dtype)
+                self.H = to_dev(self.wl.H, hd.dtype)
+            tree = self.plan.build_tree_head(self.logits, self.H, self.w1, self.w2, self.wl.T,
+                                             self.h0)
+        else:
+            tree = self.plan.build_tree(self.logits, self.wl.T, self.h0)
         torch.cuda.synchronize()
         return {k: getattr(tree, k).cpu().numpy() for k in
                 ("tokens", "parents", "depth", "position_ids", "mask", "scores", "n_nodes",

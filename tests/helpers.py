@@ -13,16 +13,26 @@ def weight_dict(w):
                 dtype=w.dtype)
 
 
+def _oracle_inputs(wl, t, kw):
+    """Weights dict and keyword arguments; a workload carrying Domino's own head
+    (attributes head, H) adds w1, w2 and its tree's hidden states."""
+    w = weight_dict(wl.weights)
+    if kw.get("scorer") == oracle.SCORER_HEAD:
+        w.update(w1=wl.head.w1, w2=wl.head.w2)
+        kw = dict(kw, H=wl.H[t])
+    return w, kw
+
+
 def run_oracle(wl, t=0, **kw):
-    w = wl.weights
-    return oracle.build_tree(wl.logits[t], w.emb, w.dtype, weight_dict(w),
+    w, kw = _oracle_inputs(wl, t, kw)
+    return oracle.build_tree(wl.logits[t], wl.weights.emb, wl.weights.dtype, w,
                              None if wl.h0 is None else wl.h0[t], wl.M, wl.B, wl.T,
                              logits_dtype=wl.logits_dtype, **kw)
 
 
 def rescore(wl, t, tokens, parents, n, **kw):
-    w = wl.weights
-    return oracle.score_paths(wl.logits[t], w.emb, w.dtype, weight_dict(w),
+    w, kw = _oracle_inputs(wl, t, kw)
+    return oracle.score_paths(wl.logits[t], wl.weights.emb, wl.weights.dtype, w,
                               None if wl.h0 is None else wl.h0[t], wl.M, wl.B, wl.T,
                               tokens, parents, n, logits_dtype=wl.logits_dtype, **kw)
 
