@@ -15,6 +15,11 @@ time), and the graph's output is checked against theirs.
 
 Prints ONE JSON line: trees/s for the whole job, the per-kernel roofline of the
 dominant kernel and the CPU oracle timed on a bounded sample.
+
+--scorer marg|static times the ablation arms; --scorer head times
+dt_build_tree_head (Domino's own rank-256 SiLU head over [H_d; S], d_H = d_e,
+synthetic hidden states), whose line carries no stage events or roofline (its
+kernel durations come from a rocprofv3 kernel trace of the same command).
 """
 from __future__ import annotations
 
@@ -31,7 +36,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILES = os.path.join(ROOT, "profiles")
-SCORERS = {"cond": 0, "marg": 1, "static": 2}
+SCORERS = {"cond": 0, "marg": 1, "static": 2, "head": 3}
+HEAD_RANK = 256   # the paper's bottleneck rank for Domino's own head
 PROFILE_EVERY = 8   # kernel start/end events on every 8th eager call
 
 
@@ -89,7 +95,7 @@ def traffic_from_profiles(workload, stage):
         return None
 
 
-def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0):
+def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None):
     """The oracle as it stands, one BLAS thread, on trees of the same workload."""
     import numpy as np
     from threadpoolctl import threadpool_limits
@@ -98,6 +104,8 @@ def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0):
     w = wl.weights
     wd = dict(w_ih=w.w_ih, w_hh=w.w_hh, b_ih=w.b_ih, b_hh=w.b_hh, w_c=w.w_c, b_c=w.b_c,
               dtype=w.dtype)
+    if head is not None:
+        wd.update(w1=head[0].w1, w2=head[0].w2)
     n = 0
     t0 = time.perf_counter()
     with threadpool_limits(limits=1):
@@ -105,7 +113,8 @@ def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0):
             buf = bufs_host[(n // wl.batch) % len(bufs_host)]
             t = n % wl.batch
             oracle.build_tree(buf[t], w.emb, w.dtype, wd, None if wl.h0 is None else wl.h0[t],
-                              wl.M, wl.B, wl.T, logits_dtype=wl.logits_dtype, scorer=scorer)
+                              wl.M, wl.B, wl.T, logits_dtype=wl.logits_dtype, scorer=scorer,
+                              H=None if head is None else head[1][t])
             n += 1
             el = time.perf_counter() - t0
             if el >= seconds and n >= 3:
@@ -145,18 +154,32 @@ def main():
     plan = binding.Plan(emb, up(w.w_ih, d), up(w.w_hh, d), up(w.b_ih, d), up(w.b_hh, d),
                         up(w.w_c, d), up(w.b_c, d), L=wl.L, M=wl.M, B=wl.B,
                         logits_dtype=wl.logits_dtype, max_batch=wl.batch,
-                        scorer=SCORERS[args.scorer])
+                        scorer=0 if args.scorer == "head" else SCORERS[args.scorer])
+    head = None
+    if args.scorer == "head":
+        # Domino's own head (dt_build_tree_head): d_H = the drafter's width,
+        # rank 256, synthetic hidden states
+        hw = synth.domino_head(43, w.V, w.d_e, w.d_h, HEAD_RANK, d, w2_scale=0.5)
+        hH = synth.hidden_states(43, wl.batch, wl.L, w.d_e, d)
+        head = (hw, hH)
+        w1, w2, Hdev = up(hw.w1, d), up(hw.w2, d), up(hH, d)
     per_buf = wl.logits.nbytes
     nbuf = max(1, math.ceil(args.rotate_mb * 2**20 / per_buf))
     bufs_host = [wl.logits] + [synth.logits_buffer(wl.name, i, wl.batch) for i in range(1, nbuf)]
     bufs = [up(b, wl.logits_dtype) for b in bufs_host]
     h0 = None if wl.h0 is None else torch.from_numpy(wl.h0).to(dev)
     out = binding.Tree.empty(wl.batch, wl.B, dev)
-    ws = plan.workspace(wl.batch)
     stream = torch.cuda.current_stream()
+    if head is None:
+        ws = plan.workspace(wl.batch)
 
-    def step(i, o=out):
-        plan.build_tree(bufs[i % nbuf], wl.T, h0, out=o, workspace=ws)
+        def step(i, o=out):
+            plan.build_tree(bufs[i % nbuf], wl.T, h0, out=o, workspace=ws)
+    else:
+        ws = torch.empty(plan.head_workspace_size(wl.batch, w1, w2), dtype=torch.uint8, device=dev)
+
+        def step(i, o=out):
+            plan.build_tree_head(bufs[i % nbuf], Hdev, w1, w2, wl.T, h0, out=o, workspace=ws)
 
     for i in range(args.warmup):
         step(i)
@@ -165,7 +188,8 @@ def main():
     # eager pass over the same K calls: per-call GPU times and the stage
     # events the library records on the launch stream (every PROFILE_EVERY-th call)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    plan.set_profiling(PROFILE_EVERY)
+    if head is None:
+        plan.set_profiling(PROFILE_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -175,8 +199,10 @@ def main():
     torch.cuda.synchronize()
     eager_wall = time.perf_counter() - t0
     per_call = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]) * 1e3  # us
-    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled calls
-    plan.set_profiling(0)
+    stage_us = None
+    if head is None:
+        stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled calls
+        plan.set_profiling(0)
     eager_last = {k: getattr(out, k).cpu().clone() for k in ("tokens", "parents", "scores", "mask")}
 
     if args.eager:
@@ -209,17 +235,18 @@ def main():
     cfg = dict(batch=wl.batch, L=wl.L, V=w.V, M=wl.M, d_e=w.d_e, d_h=w.d_h,
                logit_bytes=2 if wl.logits_dtype == synth.DT_BF16 else 4,
                expanded_nodes_per_call=expanded)
-    dom = max(stage_us, key=stage_us.get)
-    work, unit, bound = algorithmic(cfg, dom)
-    dur_s = stage_us[dom] * 1e-6
-    if unit == "bytes":
-        achieved, peak, runit = work / dur_s / 1e9, HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved = work / dur_s / 1e12
-        peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
-        runit = "TFLOP/s"
     scan_bytes = rows * w.V * cfg["logit_bytes"]
-    scan_us = stage_us["scan"]
+    if head is None:
+        dom = max(stage_us, key=stage_us.get)
+        work, unit, bound = algorithmic(cfg, dom)
+        dur_s = stage_us[dom] * 1e-6
+        if unit == "bytes":
+            achieved, peak, runit = work / dur_s / 1e9, HBM_PEAK_GBS, "GB/s"
+        else:
+            achieved = work / dur_s / 1e12
+            peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
+            runit = "TFLOP/s"
+        scan_us = stage_us["scan"]
     trees = wl.batch * args.steps
     res = {
         "metric": "draft trees built/sec",
@@ -242,17 +269,26 @@ def main():
         "eager": {"us_per_tree": eager_wall / trees * 1e6,
                   "gpu_us_per_call_p50": float(np.percentile(per_call, 50)),
                   "gpu_us_per_call_p99": float(np.percentile(per_call, 99))},
-        "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
-        "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
         "stages_us": stage_us,
-        "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
-                     "unit": runit, "frac": achieved / peak,
-                     "traffic": traffic_from_profiles(wl.name, dom)},
-        "scan_roofline": {"kernel": "scan", "bound": "hbm",
-                          "achieved": scan_bytes / (scan_us * 1e-6) / 1e9, "peak": HBM_PEAK_GBS,
-                          "unit": "GB/s", "frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                          "traffic": traffic_from_profiles(wl.name, "scan")},
     }
+    if head is None:
+        res.update({
+            "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
+            "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
+                         "unit": runit, "frac": achieved / peak,
+                         "traffic": traffic_from_profiles(wl.name, dom)},
+            "scan_roofline": {"kernel": "scan", "bound": "hbm",
+                              "achieved": scan_bytes / (scan_us * 1e-6) / 1e9,
+                              "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                              "traffic": traffic_from_profiles(wl.name, "scan")},
+        })
+    else:
+        # the head path records no per-kernel events: its kernel durations come
+        # from a rocprofv3 kernel trace of this command
+        res["config"].update(d_H=w.d_e, rank=HEAD_RANK)
+        res["roofline"] = None
 
     if args.copy_calibration:
         x = torch.empty(256 * 2**20 // 4, dtype=torch.float32, device=dev).fill_(1.0)
@@ -262,7 +298,7 @@ def main():
 
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds,
-                                           SCORERS[args.scorer])
+                                           SCORERS[args.scorer], head)
     plan.close()
     print(json.dumps(res), flush=True)
 

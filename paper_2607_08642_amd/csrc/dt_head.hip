@@ -40,8 +40,6 @@ __device__ inline void load8(const uint16_t *p, float (&v)[8]) {
     v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
   }
 }
-__device__ inline float widen1(float v) { return v; }
-__device__ inline float widen1(uint16_t v) { return bf16_to_f32(v); }
 
 // w[0..7] . x[0..7] with x 16-byte aligned (LDS)
 __device__ inline float dot8(const float (&w)[8], const float *x) {
@@ -74,21 +72,43 @@ __device__ inline uint64_t wave_max_key(uint64_t v) {
 }
 
 // out[r] = sum_{c < n} W[r * ld + c] x[c] for r < nrows: eight lanes per row,
-// eight consecutive columns per lane and step (n % 8 == 0; W rows 16-byte
-// aligned); x in LDS.  Every thread of the block calls it.
+// eight consecutive columns per lane and chunk (n % 8 == 0; W rows 16-byte
+// aligned); x in LDS.  Each pass takes kRU rows and kCU chunks per lane with
+// every load issued before the first is used (out-of-range ones read a valid
+// address and count zero), so a pass costs one memory round trip.  Every
+// thread of the block calls it.
+constexpr int kRU = 2, kCU = 4;
 template <typename T>
 __device__ void rows_dot(const T *W, size_t ld, int nrows, int n, const float *x, float *out) {
   const int grp = threadIdx.x >> 3, sub = threadIdx.x & 7;
-  for (int r = grp; r < nrows; r += kHT / 8) {
-    const T *wr = W + (size_t)r * ld;
-    float acc = 0.0f;
-    for (int c = sub * 8; c < n; c += 64) {
-      float w[8];
-      load8(wr + c, w);
-      acc += dot8(w, x + c);
+  for (int r0 = grp * kRU; r0 < nrows; r0 += (kHT / 8) * kRU) {
+    float acc[kRU];
+#pragma unroll
+    for (int i = 0; i < kRU; ++i) acc[i] = 0.0f;
+    for (int c0 = sub * 8; c0 < n; c0 += 64 * kCU) {
+      float w[kRU][kCU][8];
+#pragma unroll
+      for (int i = 0; i < kRU; ++i)
+#pragma unroll
+        for (int j = 0; j < kCU; ++j) {
+          const int r = r0 + i < nrows ? r0 + i : nrows - 1;
+          const int c = c0 + 64 * j < n ? c0 + 64 * j : 0;
+          load8(W + (size_t)r * ld + c, w[i][j]);
+        }
+#pragma unroll
+      for (int i = 0; i < kRU; ++i)
+#pragma unroll
+        for (int j = 0; j < kCU; ++j) {
+          const int c = c0 + 64 * j;
+          const float v = dot8(w[i][j], x + (c < n ? c : 0));
+          acc[i] += c < n ? v : 0.0f;
+        }
     }
-    acc = sum8(acc);
-    if (sub == 0) out[r] = acc;
+#pragma unroll
+    for (int i = 0; i < kRU; ++i) {
+      const float v = sum8(acc[i]);
+      if (sub == 0 && r0 + i < nrows) out[r0 + i] = v;
+    }
   }
 }
 
@@ -101,9 +121,21 @@ __global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1
   extern __shared__ __attribute__((aligned(16))) float hs[];  // [kProjRows][d_H]
   const int row0 = blockIdx.x * kProjRows;
   const int nr = rows - row0 < kProjRows ? rows - row0 : kProjRows;
-  for (int i = threadIdx.x; i < kProjRows * d_H; i += kHT) {
-    const int q = i / d_H, j = i - q * d_H;
-    hs[i] = q < nr ? widen1(H[(size_t)(row0 + q) * d_H + j]) : 0.0f;
+  // the block's H rows, eight elements (16 or 32 bytes) per thread and step
+  // (d_H % 8 == 0: a group of eight never crosses a row)
+#pragma unroll 4
+  for (int i = threadIdx.x; i < kProjRows * d_H / 8; i += kHT) {
+    const int q = (8 * i) / d_H, j = 8 * i - q * d_H;
+    float v[8];
+    if (q < nr) {
+      load8(H + (size_t)(row0 + q) * d_H + j, v);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+    }
+    float4 *dst = reinterpret_cast<float4 *>(hs + 8 * i);
+    dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+    dst[1] = make_float4(v[4], v[5], v[6], v[7]);
   }
   __syncthreads();
   const int grp = threadIdx.x >> 3, sub = threadIdx.x & 7;
@@ -113,11 +145,22 @@ __global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1
   float acc[kProjRows];
 #pragma unroll
   for (int q = 0; q < kProjRows; ++q) acc[q] = 0.0f;
-  for (int c = sub * 8; c < d_H; c += 64) {
-    float w[8];
-    load8(wr + c, w);
+  // eight chunks per lane in flight per pass (out-of-range ones read column 0 and count zero)
+  constexpr int kPU = 8;
+  for (int c0 = sub * 8; c0 < d_H; c0 += 64 * kPU) {
+    float w[kPU][8];
 #pragma unroll
-    for (int q = 0; q < kProjRows; ++q) acc[q] += dot8(w, hs + q * d_H + c);
+    for (int j = 0; j < kPU; ++j) load8(wr + (c0 + 64 * j < d_H ? c0 + 64 * j : 0), w[j]);
+#pragma unroll
+    for (int j = 0; j < kPU; ++j) {
+      const int c = c0 + 64 * j < d_H ? c0 + 64 * j : 0;
+      const bool ok = c0 + 64 * j < d_H;
+#pragma unroll
+      for (int q = 0; q < kProjRows; ++q) {
+        const float v = dot8(w[j], hs + q * d_H + c);
+        acc[q] += ok ? v : 0.0f;
+      }
+    }
   }
 #pragma unroll
   for (int q = 0; q < kProjRows; ++q) {
@@ -271,14 +314,21 @@ __global__ __launch_bounds__(kHT) void head_tree_kernel(HeadArgs a) {
         const int m = tid >> 3, sub = tid & 7;
         if (m < M) {
           const int v = rc[64 * d + m];
+          const T *wr = w2 + (size_t)(v >= 0 ? v : 0) * R;
           float acc = 0.0f;
-          if (v >= 0)
-            for (int c = sub * 8; c < R; c += 64) {
-              float w[8];
-              load8(w2 + (size_t)v * R + c, w);
-              acc += dot8(w, yy + c);
+          for (int c0 = sub * 8; c0 < R; c0 += 64 * kCU) {
+            float w[kCU][8];
+#pragma unroll
+            for (int j = 0; j < kCU; ++j) load8(wr + (c0 + 64 * j < R ? c0 + 64 * j : 0), w[j]);
+#pragma unroll
+            for (int j = 0; j < kCU; ++j) {
+              const int c = c0 + 64 * j;
+              const float p = dot8(w[j], yy + (c < R ? c : 0));
+              acc += c < R ? p : 0.0f;
             }
+          }
           acc = sum8(acc);
+          if (v < 0) acc = 0.0f;
           if (sub == 0) dl[m] = acc;
         }
       }
