@@ -41,6 +41,8 @@ Readings of the paper that this file fixes (the paper is silent on them):
   log-softmax; the top-M selection uses the raw logits.
 * Ties: top-M by (logit desc, token id asc); children by (log-prob desc,
   slot asc); heap by (g desc, insertion id asc), children inserted in rank order.
+* HEAD: no biases in either layer; W_1's columns are [H_d; S] in that order;
+  H's row d-1 scores depth d, like the logits' row d-1.
 * k (children per expansion) = min(M, B) unless max_children > 0, then
   min(max_children, M).
 * Dead slots (logit == -inf) are never returned as children.  A tree whose
