@@ -962,6 +962,15 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           kc += __popcll(__ballot(keep));
           rnk[c * MP + m] = keep ? (int16_t)rank : (int16_t)-1;
         }
+      } else if (MP == 64) {
+        // many members (the root while vB is -inf): one bitonic sort of E's keys,
+        // (log-prob desc, slot asc); lane j of the sorted keys holds rank j
+        const uint64_t srt = sel::wave_sort64(
+            ((em[0] >> lane) & 1ull) ? make_key(lv[0], (uint32_t)lane) : 0ull, true);
+        const bool keep = srt != 0ull && lane < a.k;
+        rnk[c * MP + lane] = (int16_t)-1;
+        if (keep) rnk[c * MP + (int)key_index(srt)] = (int16_t)lane;
+        kc = __popcll(__ballot(keep));
       } else {
         wave_sync();
         const float4 *e4 = reinterpret_cast<const float4 *>(ell + c * MP);
