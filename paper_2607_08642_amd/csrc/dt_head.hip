@@ -23,7 +23,8 @@ namespace {
 
 constexpr int kHT = 512;        // threads of both kernels
 constexpr int kProjRows = 4;    // H rows per projection workgroup
-constexpr int kProjRanks = 64;  // ranks per projection workgroup (8 lanes each)
+// lanes per rank in the projection: 8, or 32 when the 8-lane grid would leave
+// most CUs idle (few tree-depth rows)
 
 __device__ inline void load8(const float *p, float (&v)[8]) {
   const float4 a = *reinterpret_cast<const float4 *>(p);
@@ -113,7 +114,7 @@ __device__ void rows_dot(const T *W, size_t ld, int nrows, int n, const float *x
 }
 
 // a[row][r] = sum_j W_1[r][j] H[row][j] over the H half (j < d_H)
-template <typename T>
+template <typename T, int kProjLanes>
 __global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1,
                                                         const T *__restrict__ H,
                                                         float *__restrict__ a, int rows, int d_H,
@@ -138,7 +139,8 @@ __global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1
     dst[1] = make_float4(v[4], v[5], v[6], v[7]);
   }
   __syncthreads();
-  const int grp = threadIdx.x >> 3, sub = threadIdx.x & 7;
+  constexpr int kProjRanks = kHT / kProjLanes;  // ranks per workgroup
+  const int grp = threadIdx.x / kProjLanes, sub = threadIdx.x % kProjLanes;
   const int r = blockIdx.y * kProjRanks + grp;
   if (r >= rank) return;  // (whole groups; no barrier follows)
   const T *wr = w1 + (size_t)r * ld1;
@@ -147,14 +149,15 @@ __global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1
   for (int q = 0; q < kProjRows; ++q) acc[q] = 0.0f;
   // eight chunks per lane in flight per pass (out-of-range ones read column 0 and count zero)
   constexpr int kPU = 8;
-  for (int c0 = sub * 8; c0 < d_H; c0 += 64 * kPU) {
+  constexpr int kStep = 8 * kProjLanes;  // columns per chunk step of the group
+  for (int c0 = sub * 8; c0 < d_H; c0 += kStep * kPU) {
     float w[kPU][8];
 #pragma unroll
-    for (int j = 0; j < kPU; ++j) load8(wr + (c0 + 64 * j < d_H ? c0 + 64 * j : 0), w[j]);
+    for (int j = 0; j < kPU; ++j) load8(wr + (c0 + kStep * j < d_H ? c0 + kStep * j : 0), w[j]);
 #pragma unroll
     for (int j = 0; j < kPU; ++j) {
-      const int c = c0 + 64 * j < d_H ? c0 + 64 * j : 0;
-      const bool ok = c0 + 64 * j < d_H;
+      const int c = c0 + kStep * j < d_H ? c0 + kStep * j : 0;
+      const bool ok = c0 + kStep * j < d_H;
 #pragma unroll
       for (int q = 0; q < kProjRows; ++q) {
         const float v = dot8(w[j], hs + q * d_H + c);
@@ -164,7 +167,9 @@ __global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1
   }
 #pragma unroll
   for (int q = 0; q < kProjRows; ++q) {
-    const float s = sum8(acc[q]);
+    float s = acc[q];
+#pragma unroll
+    for (int o = 1; o < kProjLanes; o <<= 1) s += __shfl_xor(s, o);  // within the aligned group
     if (sub == 0 && q < nr) a[(size_t)(row0 + q) * rank + r] = s;
   }
 }
@@ -470,13 +475,16 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
   const int rows = batch * p->L;
   const ScanGeom g = scan_geom(rows, p->V, p->M);
   const size_t plds = (size_t)kProjRows * hd.d_H * sizeof(float);
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&head_proj_kernel<T>),
+  const int rblocks = (rows + kProjRows - 1) / kProjRows;
+  const bool fine = (size_t)rblocks * ((hd.rank + kHT / 8 - 1) / (kHT / 8)) < (size_t)p->num_cus;
+  auto proj = fine ? &head_proj_kernel<T, 32> : &head_proj_kernel<T, 8>;
+  const int rpb = fine ? kHT / 32 : kHT / 8;  // ranks per workgroup
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(proj),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)plds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(head_proj_kernel<T>, dim3((rows + kProjRows - 1) / kProjRows,
-                                               (hd.rank + kProjRanks - 1) / kProjRanks),
-                     dim3(kHT), plds, s, static_cast<const T *>(hd.w1), static_cast<const T *>(H),
-                     hw.a, rows, hd.d_H, hd.d_H + p->d_h, hd.rank);
+  hipLaunchKernelGGL(proj, dim3(rblocks, (hd.rank + rpb - 1) / rpb), dim3(kHT), plds, s,
+                     static_cast<const T *>(hd.w1), static_cast<const T *>(H), hw.a, rows, hd.d_H,
+                     hd.d_H + p->d_h, hd.rank);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   HeadArgs a;

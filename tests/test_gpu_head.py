@@ -55,6 +55,8 @@ CASES = [
     (38, 2, 6, 300, 8, 6, 0.0, 64, 32, synth.DT_F32, 32, 16, dict(max_children=1), {}),
     (39, 2, 4, 30000, 64, 20, 0.9, 64, 96, synth.DT_F32, 200, 40, {}, dict(h0=True)),
     (40, 1, 3, 700, 5, 33, 1.2, 48, 32, synth.DT_F32, 8, 1024, dict(max_children=4), {}),
+    # 256 tree-depth rows at rank 256: the projection's 8-lane grid (enough workgroups)
+    (46, 16, 16, 2000, 16, 8, 0.7, 64, 32, synth.DT_BF16, 64, 256, {}, dict(h0=True)),
 ]
 
 
