@@ -18,8 +18,7 @@ dominant kernel and the CPU oracle timed on a bounded sample.
 
 --scorer marg|static times the ablation arms; --scorer head times
 dt_build_tree_head (Domino's own rank-256 SiLU head over [H_d; S], d_H = d_e,
-synthetic hidden states), whose line carries no stage events or roofline (its
-kernel durations come from a rocprofv3 kernel trace of the same command).
+synthetic hidden states); its stage "expand" is the head path's tree kernel.
 """
 from __future__ import annotations
 
@@ -67,8 +66,11 @@ def algorithmic(plan_cfg, stage):
     rows = c["batch"] * c["L"]
     if stage == "scan":
         return rows * c["V"] * c["logit_bytes"], "bytes", "hbm"
-    # expansion: MFMA work of Alg. 1's expansions (GRU hidden GEMV + slice correction)
+    # expansion: MFMA work of Alg. 1's expansions (GRU hidden GEMV + slice correction;
+    # Domino's own head: W_1^S S and W_2[cand] . y in place of the linear head)
     n = c["expanded_nodes_per_call"]
+    if c.get("rank"):
+        return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["rank"] * (c["d_h"] + c["M"])), "flops", "mfma"
     return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["M"] * c["d_h"]), "flops", "mfma"
 
 
@@ -188,8 +190,7 @@ def main():
     # eager pass over the same K calls: per-call GPU times and the stage
     # events the library records on the launch stream (every PROFILE_EVERY-th call)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    if head is None:
-        plan.set_profiling(PROFILE_EVERY)
+    plan.set_profiling(PROFILE_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -199,10 +200,8 @@ def main():
     torch.cuda.synchronize()
     eager_wall = time.perf_counter() - t0
     per_call = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]) * 1e3  # us
-    stage_us = None
-    if head is None:
-        stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled calls
-        plan.set_profiling(0)
+    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled calls
+    plan.set_profiling(0)
     eager_last = {k: getattr(out, k).cpu().clone() for k in ("tokens", "parents", "scores", "mask")}
 
     if args.eager:
@@ -234,19 +233,18 @@ def main():
     rows = wl.batch * wl.L
     cfg = dict(batch=wl.batch, L=wl.L, V=w.V, M=wl.M, d_e=w.d_e, d_h=w.d_h,
                logit_bytes=2 if wl.logits_dtype == synth.DT_BF16 else 4,
-               expanded_nodes_per_call=expanded)
+               expanded_nodes_per_call=expanded, rank=HEAD_RANK if head is not None else 0)
     scan_bytes = rows * w.V * cfg["logit_bytes"]
-    if head is None:
-        dom = max(stage_us, key=stage_us.get)
-        work, unit, bound = algorithmic(cfg, dom)
-        dur_s = stage_us[dom] * 1e-6
-        if unit == "bytes":
-            achieved, peak, runit = work / dur_s / 1e9, HBM_PEAK_GBS, "GB/s"
-        else:
-            achieved = work / dur_s / 1e12
-            peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
-            runit = "TFLOP/s"
-        scan_us = stage_us["scan"]
+    dom = max(stage_us, key=stage_us.get)
+    work, unit, bound = algorithmic(cfg, dom)
+    dur_s = stage_us[dom] * 1e-6
+    if unit == "bytes":
+        achieved, peak, runit = work / dur_s / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = work / dur_s / 1e12
+        peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
+        runit = "TFLOP/s"
+    scan_us = stage_us["scan"]
     trees = wl.batch * args.steps
     res = {
         "metric": "draft trees built/sec",
@@ -271,24 +269,23 @@ def main():
                   "gpu_us_per_call_p99": float(np.percentile(per_call, 99))},
         "stages_us": stage_us,
     }
-    if head is None:
-        res.update({
-            "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
-            "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-            "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
-                         "unit": runit, "frac": achieved / peak,
-                         "traffic": traffic_from_profiles(wl.name, dom)},
-            "scan_roofline": {"kernel": "scan", "bound": "hbm",
-                              "achieved": scan_bytes / (scan_us * 1e-6) / 1e9,
-                              "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                              "frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                              "traffic": traffic_from_profiles(wl.name, "scan")},
-        })
-    else:
-        # the head path records no per-kernel events: its kernel durations come
-        # from a rocprofv3 kernel trace of this command
+    res.update({
+        "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
+        "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
+                     "unit": runit, "frac": achieved / peak,
+                     "traffic": traffic_from_profiles(wl.name, dom)},
+        "scan_roofline": {"kernel": "scan", "bound": "hbm",
+                          "achieved": scan_bytes / (scan_us * 1e-6) / 1e9,
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                          "traffic": traffic_from_profiles(wl.name, "scan")},
+    })
+    if head is not None:
+        # stage "expand" is the head path's tree kernel; no counter record is kept for it
         res["config"].update(d_H=w.d_e, rank=HEAD_RANK)
-        res["roofline"] = None
+        res["roofline"]["kernel"] = "head_tree"
+        res["roofline"]["traffic"] = None
 
     if args.copy_calibration:
         x = torch.empty(256 * 2**20 // 4, dtype=torch.float32, device=dev).fill_(1.0)

@@ -240,7 +240,9 @@ dt_status dt_head_workspace_size(const dt_plan *plan, int batch, const dt_domino
  * <= 16 (true for V <= 163840 at any batch); k * (B + 1) <= 4096; the plan
  * created with DT_SCORER_COND; the kernel's LDS must fit the device.
  * DT_ERR_UNSUPPORTED otherwise.  Stream-ordered and capturable like
- * dt_build_tree (three kernels, no memset or copy). */
+ * dt_build_tree (three kernels, no memset or copy).  Stage timing
+ * (dt_plan_set_profiling) counts these calls too: stage 0 = the scan,
+ * stage 1 = the tree kernel (the projection between them is not timed). */
 dt_status dt_build_tree_head(dt_plan *plan, const void *marginal_logits, int batch, const void *H,
                              const dt_domino_head *head, const float *h0, float T,
                              void *workspace, size_t ws_bytes, dt_tree *out, void *stream);

@@ -419,10 +419,22 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
   const dt::HeadWorkspace hw = dt::carve_head(plan, batch, head->rank, static_cast<char *>(workspace));
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
-  hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hw.scan, nullptr, 0, s);
+  // stage timing as in dt_build_tree: stage 0 the scan, stage 1 the tree kernel
+  bool prof = false;
+  if (plan->profiling > 0) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    const hipError_t ce = hipStreamIsCapturing(s, &cs);
+    if (ce != hipSuccess) return hip_fail(ce, "stream capture query");
+    if (cs == hipStreamCaptureStatusNone) prof = (plan->calls_since++ % plan->profiling) == 0;
+  }
+  hipEvent_t *ev = prof ? plan->ev + 4 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
+  hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hw.scan, nullptr, 0, s,
+                                        prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
-  e = dt::launch_head(plan, batch, H, *head, h0, inv_tau, hw, out, s);
+  e = dt::launch_head(plan, batch, H, *head, h0, inv_tau, hw, out, s, prof ? ev[2] : nullptr,
+                      prof ? ev[3] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "head launch");
+  if (prof) plan->profiled_calls++;
   return DT_OK;
 }
 

@@ -17,6 +17,7 @@
 // (one wave's bitonic sort of the slice).
 #include "dt_internal.h"
 #include "dt_select.h"
+#include <hip/hip_ext.h>
 
 namespace dt {
 namespace {
@@ -471,7 +472,7 @@ HeadWorkspace carve_head(const dt_plan *p, int batch, int rank, char *base) {
 template <typename T>
 static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
                                 const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
-                                hipStream_t s) {
+                                hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
   const int rows = batch * p->L;
   const ScanGeom g = scan_geom(rows, p->V, p->M);
   const size_t plds = (size_t)kProjRows * hd.d_H * sizeof(float);
@@ -517,15 +518,18 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
   e = hipFuncSetAttribute(reinterpret_cast<const void *>(&head_tree_kernel<T>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(head_tree_kernel<T>, dim3(batch), dim3(kHT), lds, s, a);
+  if (t0)
+    hipExtLaunchKernelGGL(head_tree_kernel<T>, dim3(batch), dim3(kHT), lds, s, t0, t1, 0, a);
+  else
+    hipLaunchKernelGGL(head_tree_kernel<T>, dim3(batch), dim3(kHT), lds, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
                        const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
-                       hipStream_t s) {
-  return p->wdt == DT_BF16 ? launch_head_t<uint16_t>(p, batch, H, hd, h0, inv_tau, hw, out, s)
-                           : launch_head_t<float>(p, batch, H, hd, h0, inv_tau, hw, out, s);
+                       hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
+  return p->wdt == DT_BF16 ? launch_head_t<uint16_t>(p, batch, H, hd, h0, inv_tau, hw, out, s, t0, t1)
+                           : launch_head_t<float>(p, batch, H, hd, h0, inv_tau, hw, out, s, t0, t1);
 }
 
 }  // namespace dt

@@ -149,9 +149,10 @@ struct HeadWorkspace {
 };
 HeadWorkspace carve_head(const dt_plan *p, int batch, int rank, char *base);
 size_t head_lds_bytes(int L, int B, int dh, int rank);
+// (with t0/t1: events at the start and end of the tree kernel)
 hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
                        const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
-                       hipStream_t s);
+                       hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 // One expansion launch: DominoTree (the default), or, for the ablation arms,
 // without the correction (nocorr: the marginals, or menu_in's per-depth menus)
 // and/or writing every expanded depth's menu (menu_out; the greedy chain).
