@@ -246,29 +246,36 @@ class _Model:
             best = min(slots, key=lambda m: (-ell[m], m))
             S = gru_cell(S, self.Ec[d - 1][[best]], self.w_ih, self.w_hh, self.b_ih, self.b_hh)[0]
 
+    def menu(self, S: Optional[np.ndarray], d: int):
+        """The log-probs the children function ranks at depth d (all M slots)."""
+        if self.scorer == SCORER_MARG:
+            return self.slot_logprobs(None, d)
+        if self.scorer == SCORER_STATIC:
+            return self.menus[d - 1]
+        return self.slot_logprobs(S, d)
+
     def children(self, S: Optional[np.ndarray], d: int, k: int, gaps: list):
         """Children(S_{d-1}, d) of Alg. 1 step 2: top-k (token, ell, slot, child state).
 
-        MARG and STATIC ignore S (their menus are path-independent) and return
-        no child states."""
-        if self.scorer == SCORER_MARG:
-            ell, live = self.slot_logprobs(None, d)
-        elif self.scorer == SCORER_STATIC:
-            ell, live = self.menus[d - 1]
-        else:
-            ell, live = self.slot_logprobs(S, d)
+        Returns (children, ell_out) where ell_out is the log-prob of the best
+        slot left out by the top-k cut (-inf if none).  The gap between the k-th
+        and (k+1)-th log-prob is logged as a "children" gap.  MARG and STATIC
+        ignore S (their menus are path-independent) and return no child states."""
+        ell, live = self.menu(S, d)
         slots = [m for m in range(self.M) if live[m]]
         slots.sort(key=lambda m: (-ell[m], m))
+        ell_out = -math.inf
         if len(slots) > k:
-            gaps.append(ell[slots[k - 1]] - ell[slots[k]])
+            ell_out = float(ell[slots[k]])
+            gaps.append(("children", ell[slots[k - 1]] - ell[slots[k]]))
         kept = slots[:k]
         if not kept:
-            return []
+            return [], ell_out
         tokens = [int(self.cand[d - 1][m]) for m in kept]
         if self.scorer not in (SCORER_COND, SCORER_HEAD):
-            return [(tokens[i], float(ell[m]), m, None) for i, m in enumerate(kept)]
+            return [(tokens[i], float(ell[m]), m, None) for i, m in enumerate(kept)], ell_out
         states = gru_cell(S, self.Ec[d - 1][kept], self.w_ih, self.w_hh, self.b_ih, self.b_hh)
-        return [(tokens[i], float(ell[m]), m, states[i]) for i, m in enumerate(kept)]
+        return [(tokens[i], float(ell[m]), m, states[i]) for i, m in enumerate(kept)], ell_out
 
 
 def _empty_tree(B: int, pos_offset: int, status: int):
@@ -280,9 +287,14 @@ def _empty_tree(B: int, pos_offset: int, status: int):
         "mask": np.zeros((B, B), np.uint8),
         "scores": np.full(B, -np.inf, np.float64),
         "slots": np.full(B, -1, np.int32),
+        "ell": np.full(B, -np.inf, np.float64),
+        "ell_out": np.full(B, -np.inf, np.float64),
+        "rank": np.full(B, -1, np.int32),
         "n_nodes": 0,
         "status": status,
         "min_gap": math.inf,
+        "gaps": [],
+        "excluded": -math.inf,
     }
 
 
@@ -309,36 +321,48 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     if scorer == SCORER_STATIC:
         model.static_menus(S0)
 
-    gaps: List[float] = []
+    gaps: list = []    # (kind, value): the decisive score gaps
     heap = []          # entries (-g, insertion id, payload)
     next_id = 0
     # Alg. 1 step 3: the root's children
-    for tok, ell, m, S in model.children(S0, 1, k, gaps):
-        heapq.heappush(heap, (-ell, next_id, (tok, ell, m, S, 1, -1)))
+    kids, ell_out = model.children(S0, 1, k, gaps)
+    for r, (tok, ell, m, S) in enumerate(kids):
+        heapq.heappush(heap, (-ell, next_id, (tok, ell, m, S, 1, -1, ell, ell_out, r)))
         next_id += 1
     # Alg. 1 step 4: pop the best entry, add it to the tree, push its children
-    tree = []          # (token, g, slot, depth, parent pop index)
+    tree = []          # (token, g, slot, depth, parent pop index, ell, ell_out, rank)
     while len(tree) < B and heap:
-        neg_g, _, (tok, g, m, S, d, parent) = heapq.heappop(heap)
+        neg_g, _, (tok, g, m, S, d, parent, ell, eo, r) = heapq.heappop(heap)
         i = len(tree)
-        tree.append((tok, g, m, d, parent))
+        tree.append((tok, g, m, d, parent, ell, eo, r))
         if d < L:
-            for ctok, ell, cm, cS in model.children(S, d + 1, k, gaps):
-                heapq.heappush(heap, (-(g + ell), next_id, (ctok, g + ell, cm, cS, d + 1, i)))
+            kids, ell_out = model.children(S, d + 1, k, gaps)
+            for rr, (ctok, cell, cm, cS) in enumerate(kids):
+                heapq.heappush(heap, (-(g + cell), next_id,
+                                      (ctok, g + cell, cm, cS, d + 1, i, cell, ell_out, rr)))
                 next_id += 1
     # decisive gaps: consecutive pops and the last pop vs the best entry left out
     for i in range(len(tree) - 1):
-        gaps.append(tree[i][1] - tree[i + 1][1])
-    if len(tree) == B and heap:
-        gaps.append(tree[-1][1] - (-heap[0][0]))
-    return _emit(tree, B, pos_offset, min(gaps) if gaps else math.inf)
+        gaps.append(("pop", tree[i][1] - tree[i + 1][1]))
+    excluded = -math.inf
+    if heap:
+        excluded = -heap[0][0]
+        if len(tree) == B:
+            gaps.append(("boundary", tree[-1][1] - excluded))
+    out = _emit(tree, B, pos_offset, min(v for _, v in gaps) if gaps else math.inf)
+    out["gaps"] = gaps
+    out["excluded"] = excluded
+    return out
 
 
 def _emit(tree, B: int, pos_offset: int, min_gap: float):
     """Pop-order arrays and the ancestor-or-self mask (section 3.5)."""
     out = _empty_tree(B, pos_offset, 0)
     n = len(tree)
-    for i, (tok, g, m, d, parent) in enumerate(tree):
+    for i, (tok, g, m, d, parent, ell, ell_out, rank) in enumerate(tree):
+        out["ell"][i] = ell
+        out["ell_out"][i] = ell_out
+        out["rank"][i] = rank
         out["tokens"][i] = tok
         out["parents"][i] = parent
         out["depth"][i] = d
@@ -381,11 +405,16 @@ def scan(logits: np.ndarray, logits_dtype: int, M: int, T: float):
 def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                 h0: Optional[np.ndarray], M: int, B: int, T: float, tokens, parents, n_nodes: int,
                 max_children: int = 0, norm_mode: int = NORM_TAIL, logits_dtype: int = DT_F32,
-                scorer: int = SCORER_COND, H: Optional[np.ndarray] = None):
+                scorer: int = SCORER_COND, H: Optional[np.ndarray] = None, tie_tol: float = 0.0):
     """Re-score a given tree with the oracle's Children function.
 
-    Returns (g[n], valid): valid is False when a node's token is not among the
-    top-k children of its parent's path (or a parent index is not earlier).
+    Returns (g[n], valid): g[i] is the cumulative log-prob of node i along its
+    own path; valid is False when a parent index is not earlier, a node lies
+    below depth L, or a node is not among the top-k children of its parent's
+    path.  With tie_tol = 0 the top-k is the exact (log-prob desc, slot asc)
+    cut; with tie_tol > 0 a node also counts as a top-k child when fewer than k
+    live slots beat its log-prob by more than tie_tol (a child whose log-prob is
+    that close to the cut may take the k-th place).
     """
     Xd = widen(X, logits_dtype)
     tau = effective_temperature(T)
@@ -398,7 +427,6 @@ def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     g = np.zeros(n_nodes)
     state = [None] * n_nodes
     depth = [0] * n_nodes
-    valid = True
     for i in range(n_nodes):
         p = int(parents[i])
         if p >= i:
@@ -406,12 +434,20 @@ def score_paths(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
         S, gp, d = (S0, 0.0, 1) if p < 0 else (state[p], g[p], depth[p] + 1)
         if d > model.L:
             return g, False
-        kids = model.children(S, d, k, [])
-        match = [c for c in kids if c[0] == int(tokens[i])]
-        if not match:
+        ell, live = model.menu(S, d)
+        hit = np.flatnonzero(model.cand[d - 1] == int(tokens[i]))
+        if hit.size == 0 or not live[hit[0]]:
             return g, False
-        _, ell, _, cS = match[0]
-        g[i] = gp + ell
-        state[i] = cS
+        m = int(hit[0])
+        if tie_tol > 0:
+            above = int(np.sum(live & (ell > ell[m] + tie_tol)))
+        else:
+            above = int(np.sum(live & ((ell > ell[m]) | ((ell == ell[m]) & (np.arange(model.M) < m)))))
+        if above >= k:
+            return g, False
+        g[i] = gp + ell[m]
         depth[i] = d
-    return g, valid
+        if scorer in (SCORER_COND, SCORER_HEAD):
+            state[i] = gru_cell(S, model.Ec[d - 1][[m]], model.w_ih, model.w_hh, model.b_ih,
+                                model.b_hh)[0]
+    return g, True

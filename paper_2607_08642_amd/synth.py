@@ -13,6 +13,16 @@ Workloads (names follow the drafter each one is shaped like):
 * ``budget64``  -- Qwen3-8B shapes, B=64, T=0, flattened spikes (wide trees).
 * ``concurrent``-- 32 independent trees of the Qwen3-8B shape, T=0.7, per-tree
                    h0 ~ N(0, 0.1^2).
+* ``deep``      -- Qwen3-8B shapes, batch 1, T=1.0, with 2-4 strong spikes
+                   (+U(13,17)) per row: the top candidates dominate each row's
+                   mass, so the B=16 tree grows long paths (depth 9 here) and
+                   the expansion runs a long chain of dependent steps.
+* ``deep_concurrent`` -- 32 trees of that kind, T=0.7, per-tree h0.
+
+``twin_tokens(wl)`` turns a workload into one with exact structural ties:
+the top token of every row gets a twin (a low-logit token given the same
+embedding row and the same logit in every row), so twin paths score
+identically on any builder and only the tie rules order them.
 
 The vocabulary (151936) is Qwen3's; the block length 16 matches the b16
 drafters (paper, section 4.1).  Marginal logits are 2*N(0,1) with a few
@@ -201,13 +211,54 @@ def concurrent(batch: int = 32) -> Workload:
     return Workload("concurrent", x, DT_BF16, h0, w, 16, 64, 16, 0.7, batch)
 
 
+def deep() -> Workload:
+    w = qwen_weights(4096, 2)
+    x = peaked_logits(7, 0, 16, QWEN3_VOCAB, DT_BF16, 2, 4, 13.0, 17.0)[None]
+    return Workload("deep", x, DT_BF16, None, w, 16, 64, 16, 1.0, 1)
+
+
+def deep_concurrent(batch: int = 32) -> Workload:
+    w = qwen_weights(4096, 2)
+    x = np.stack([peaked_logits(8, t, 16, QWEN3_VOCAB, DT_BF16, 2, 4, 13.0, 17.0)
+                  for t in range(batch)])
+    h0 = np.stack([_rng(8, TAG_H0, 1000 + t).standard_normal(512, dtype=np.float32)
+                   * np.float32(0.1) for t in range(batch)])
+    return Workload("deep_concurrent", x, DT_BF16, h0, w, 16, 64, 16, 0.7, batch)
+
+
 WORKLOADS = {
     "tiny": tiny,
     "qwen3_4b": qwen3_4b,
     "qwen3_8b": qwen3_8b,
     "budget64": budget64,
     "concurrent": concurrent,
+    "deep": deep,
+    "deep_concurrent": deep_concurrent,
 }
+
+
+def twin_tokens(wl: Workload) -> Workload:
+    """A copy of `wl` whose rows' top tokens have twins.
+
+    For every distinct token a that tops some row of some tree, a twin b is
+    taken from the tokens that top no row and sit lowest in row 0 of tree 0;
+    E[b] is set to E[a] and, in every row of every tree, the logit of b to
+    that of a.  The embedding table is copied (the cached one is untouched).
+    """
+    x = wl.logits.copy()
+    flat = x.reshape(-1, x.shape[-1])
+    vals = bf16_bits_to_f32(flat) if wl.logits_dtype == DT_BF16 else flat
+    tops = sorted({int(np.argmax(r)) for r in vals})
+    row0 = vals[0]
+    spare = [int(v) for v in np.argsort(row0, kind="stable") if int(v) not in set(tops)]
+    w = wl.weights
+    emb = w.emb.copy()
+    for a, b in zip(tops, spare):
+        emb[b] = emb[a]
+        flat[:, b] = flat[:, a]
+    wt = dataclasses.replace(w, emb=emb)
+    return Workload(wl.name + "_twins", x, wl.logits_dtype, wl.h0, wt, wl.L, wl.M, wl.B, wl.T,
+                    wl.batch)
 
 
 @dataclasses.dataclass
@@ -268,6 +319,10 @@ LOGIT_RECIPES = {
                      fixed=None),
     "concurrent": dict(seed=4, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=1, n_hi=4, lo=6.0,
                        hi=12.0, fixed=None),
+    "deep": dict(seed=7, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=2, n_hi=4, lo=13.0, hi=17.0,
+                 fixed=None),
+    "deep_concurrent": dict(seed=8, dtype=DT_BF16, L=16, V=QWEN3_VOCAB, n_lo=2, n_hi=4, lo=13.0,
+                            hi=17.0, fixed=None),
 }
 
 
