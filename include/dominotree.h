@@ -180,6 +180,23 @@ dt_status dt_workspace_size(const dt_plan *plan, int batch, size_t *bytes);
 dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, const float *h0,
                         float T, void *workspace, size_t ws_bytes, dt_tree *out, void *stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): dt_build_tree without a workspace
+ * argument.  The workspace is a 32 MiB array of library-owned device memory per
+ * device (held until the process ends; enough for 32 trees per call at the
+ * Qwen3-8B shape, L = 16, M = 64, B = 16, d_h = 512).  The call itself allocates
+ * nothing; the array's address is resolved when a plan is created on the device.
+ *   arguments: as dt_build_tree (the plan's device must be current);
+ *   DT_ERR_WORKSPACE when dt_workspace_size(plan, batch) exceeds 32 MiB
+ *   (use dt_build_tree with a workspace then), DT_ERR_SHAPE when the current
+ *   device is not the plan's.
+ * Every call on a device shares that device's array, which keeps the last
+ * call's contents (the kernels clear what they need zeroed): calls that can
+ * overlap on one device -- on different streams, or from several host threads
+ * -- race and must not be made. */
+dt_status dt_build_tree_noalloc(dt_plan *plan, const void *marginal_logits, int batch,
+                                const float *h0, float T, dt_tree *out, void *stream);
+
 /* Release the plan's device memory (NULL is ignored). */
 void dt_plan_destroy(dt_plan *plan);
 

@@ -34,7 +34,7 @@ STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
 EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_create",
            "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
            "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm", "dt_head_workspace_size",
-           "dt_build_tree_head")
+           "dt_build_tree_head", "dt_build_tree_noalloc")
 STAGES = ("scan", "expand")
 
 
@@ -109,6 +109,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dt_build_tree_head.argtypes = [vp, vp, ci, vp, ctypes.POINTER(dt_domino_head), vp, cf, vp,
                                        sz, ctypes.POINTER(dt_tree), vp]
     lib.dt_scan_topm.argtypes = [vp, ci, ci, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
+    lib.dt_build_tree_noalloc.restype = ci
+    lib.dt_build_tree_noalloc.argtypes = [vp, vp, ci, vp, cf, ctypes.POINTER(dt_tree), vp]
     if lib.dt_abi_version() != ABI_VERSION:
         raise RuntimeError(f"ABI mismatch: library {lib.dt_abi_version()} vs binding {ABI_VERSION}")
     _lib = lib
@@ -223,6 +225,20 @@ class Plan:
         st = self._lib.dt_build_tree(self.handle, logits.data_ptr(), batch,
                                      None if h0 is None else h0.data_ptr(), T, ws.data_ptr(),
                                      ws.numel(), ctypes.byref(out.as_c()), _stream(stream))
+        if st != 0:
+            _check(st)
+        return out
+
+    def build_tree_noalloc(self, logits, T: float, h0=None, out: Optional[Tree] = None,
+                           stream=None) -> Tree:
+        """dt_build_tree_noalloc: no workspace argument (the library's per-device
+        scratch array); `out` must be given by callers that cannot allocate."""
+        batch = logits.shape[0]
+        if out is None:
+            out = Tree.empty(batch, self.B, logits.device)
+        st = self._lib.dt_build_tree_noalloc(self.handle, logits.data_ptr(), batch,
+                                             None if h0 is None else h0.data_ptr(), T,
+                                             ctypes.byref(out.as_c()), _stream(stream))
         if st != 0:
             _check(st)
         return out

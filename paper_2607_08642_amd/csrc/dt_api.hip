@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -35,6 +36,35 @@ bool valid_dtype(int d) { return d == DT_F32 || d == DT_BF16; }
 size_t dsize(int d) { return d == DT_BF16 ? 2 : 4; }
 
 int ecap_for(const dt_plan *p) { return p->L * p->B + dt::kChunkNodes; }
+
+// ---- scratch of the allocation-free entry point (dt_build_tree_noalloc) ----
+constexpr size_t kScratchBytes = (size_t)32 << 20;  // 32 MiB per device
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];  // the array's device address on each device (null: not yet)
+
+}  // namespace
+
+// The workspace of dt_build_tree_noalloc: one array per device, alive until the
+// process ends.  Its name is a host-side stand-in; kernels get the address that
+// hipGetSymbolAddress returns for the current device (scratch_address).
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// The scratch array's address on the current device, resolved once per device.
+hipError_t scratch_address(int dev, void **ptr) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *q = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = q;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 }  // namespace
 
@@ -162,6 +192,13 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   p->nf_pad = (p->nf + dt::kFoldBN - 1) / dt::kFoldBN * dt::kFoldBN;
   p->has_bc = head->b != nullptr;
   p->num_cus = ncu;
+  p->device = dev;
+  void *scratch_ptr = nullptr;
+  e = scratch_address(dev, &scratch_ptr);  // once per device: dt_build_tree_noalloc's workspace
+  if (e != hipSuccess) {
+    delete p;
+    return hip_fail(e, "scratch address");
+  }
   e = hipMalloc(&p->wfold, (size_t)p->nf_pad * d_e * ws);
   if (e == hipSuccess) e = hipMalloc(&p->b_ih, sizeof(float) * 3 * d_h);
   if (e == hipSuccess) e = hipMalloc(&p->b_hh, sizeof(float) * 3 * d_h);
@@ -252,8 +289,8 @@ dt_status dt_workspace_size(const dt_plan *plan, int batch, size_t *bytes) {
   return DT_OK;
 }
 
-dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const float *h0, float T,
-                        void *workspace, size_t ws_bytes, dt_tree *out, void *stream) {
+static dt_status check_build_args(const dt_plan *plan, const void *logits, int batch,
+                                  const float *h0, float T, const dt_tree *out) {
   if (!plan || !logits || !out) return fail(DT_ERR_NULL, "plan, logits and out are required");
   if (!out->tokens || !out->parents || !out->depth || !out->position_ids || !out->mask ||
       !out->scores || !out->n_nodes || !out->status)
@@ -261,14 +298,16 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   if (batch < 1 || batch > plan->max_batch)
     return fail(DT_ERR_SHAPE, "batch %d outside [1, max_batch=%d]", batch, plan->max_batch);
   if (!(T == T)) return fail(DT_ERR_SHAPE, "temperature is NaN");
-  const size_t need = dt::carve(plan, batch, nullptr).bytes;
-  if (!workspace || ws_bytes < need)
-    return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
-  if (!aligned(workspace, 256)) return fail(DT_ERR_ALIGN, "workspace must be 256-byte aligned");
   if (!aligned(logits, dsize(plan->ldt)) || (h0 && !aligned(h0, 4)) || !aligned(out->tokens, 4) ||
       !aligned(out->parents, 4) || !aligned(out->depth, 4) || !aligned(out->position_ids, 4) ||
       !aligned(out->scores, 4) || !aligned(out->n_nodes, 4) || !aligned(out->status, 4))
     return fail(DT_ERR_ALIGN, "logits and outputs must be naturally aligned");
+  return DT_OK;
+}
+
+// The launches of one dt_build_tree call on a checked, large enough workspace.
+static dt_status build_tree_on(dt_plan *plan, const void *logits, int batch, const float *h0,
+                               float T, void *workspace, dt_tree *out, void *stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
   dt::Workspace ws = dt::carve(plan, batch, static_cast<char *>(workspace));
@@ -312,6 +351,39 @@ dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const floa
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   if (prof) plan->profiled_calls++;
   return DT_OK;
+}
+
+dt_status dt_build_tree(dt_plan *plan, const void *logits, int batch, const float *h0, float T,
+                        void *workspace, size_t ws_bytes, dt_tree *out, void *stream) {
+  const dt_status st = check_build_args(plan, logits, batch, h0, T, out);
+  if (st != DT_OK) return st;
+  const size_t need = dt::carve(plan, batch, nullptr).bytes;
+  if (!workspace || ws_bytes < need)
+    return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
+  if (!aligned(workspace, 256)) return fail(DT_ERR_ALIGN, "workspace must be 256-byte aligned");
+  return build_tree_on(plan, logits, batch, h0, T, workspace, out, stream);
+}
+
+dt_status dt_build_tree_noalloc(dt_plan *plan, const void *logits, int batch, const float *h0,
+                                float T, dt_tree *out, void *stream) {
+  const dt_status st = check_build_args(plan, logits, batch, h0, T, out);
+  if (st != DT_OK) return st;
+  const size_t need = dt::carve(plan, batch, nullptr).bytes;
+  if (need > kScratchBytes)
+    return fail(DT_ERR_WORKSPACE,
+                "batch %d needs %zu bytes of workspace, more than the %zu-byte scratch of "
+                "dt_build_tree_noalloc; use dt_build_tree with a workspace", batch, need,
+                kScratchBytes);
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  if (dev != plan->device)
+    return fail(DT_ERR_SHAPE, "the current device (%d) is not the plan's device (%d)", dev,
+                plan->device);
+  void *ws = nullptr;
+  e = scratch_address(dev, &ws);  // resolved when the plan was created: a table lookup
+  if (e != hipSuccess) return hip_fail(e, "scratch address");
+  return build_tree_on(plan, logits, batch, h0, T, ws, out, stream);
 }
 
 dt_status dt_scan_workspace_size(int rows, int V, int M, size_t *bytes) {

@@ -95,6 +95,7 @@ struct dt_plan {
   void *whh_t;      // W_hh in MFMA A-fragment order (see pack_whh_*_kernel)
   void *whh_rm;     // [3dh][dh] W_hh as given (weights dtype), for the Domino-head path
   int num_cus;
+  int device;               // the device the plan was created on (its memory lives there)
   int profiling;            // > 0: record stage events on every profiling-th dt_build_tree call
   int calls_since;          // dt_build_tree calls since profiling was enabled
   int profiled_calls;       // calls recorded since profiling was enabled
