@@ -4,17 +4,30 @@
 One step = one dt_build_tree call over one batch of resident synthetic logits:
 top-M scan, row merge, expansion and emission (every kernel of the path).  The
 default workload is the Qwen3-8B-shaped single stream (L=16, V=151936, M=64,
-B=16, T=1, d_e=4096, d_h=512).  Logit buffers rotate through >= 512 MB so the
-256 MB Infinity Cache cannot serve the scan.
+B=16, T=1, d_e=4096, d_h=512).
 
-The K timed calls are captured into one HIP graph and timed as one replay
-(--eager: launched one by one); the same K calls also run eagerly first, which
-gives the per-call GPU times and the stage durations (every 8th call launches
-its two kernels with start and end events, so a stage is one kernel's execution
-time), and the graph's output is checked against theirs.
+Timing.  After the warm-up the K calls run once eagerly: per-call GPU times
+from torch events, and each kernel's execution time from HIP events the
+library takes at the kernel's start and end on its launch stream (every call
+when K < 64, else every 8th).  The same K calls are then captured into one HIP
+graph, replayed once untimed and checked against the eager pass, and timed as
+one replay: `value` = trees/s over that replay's wall clock.  Logit buffers
+rotate through >= 512 MB, and a 1 GiB device copy runs between the untimed and
+the timed replay, so the timed scan never finds its logits in the 256 MB
+Infinity Cache, whatever K is.  A short pass with expansion statistics on then
+gives the dependent expansion steps per tree, the expanded nodes and the depth
+histogram of the trees built.
 
-Prints ONE JSON line: trees/s for the whole job, the per-kernel roofline of the
-dominant kernel and the CPU oracle timed on a bounded sample.
+The CPU baseline (the oracle as it stands, float64 numpy, one BLAS thread per
+worker) runs first, before the GPU is touched: a single-core leg and an
+all-core leg over a fork pool of min(nproc, 16) workers, on trees of the same
+workload.
+
+Prints ONE JSON line: trees/s for the whole job, the roofline of the dominant
+kernel (the expansion at one tree per call: fp32-precision MFMA work, priced
+against the fp32 peak; it is a chain of dependent steps, so the line's
+`latency` block carries us per dependent step and the occupancy), the scan's
+HBM roofline, and the CPU baseline.
 
 --scorer marg|static times the ablation arms; --scorer head times
 dt_build_tree_head (Domino's own rank-256 SiLU head over [H_d; S], d_H = d_e,
@@ -33,11 +46,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+FP32_PEAK_TFLOPS = 157.3    # dense fp32 (MFMA and vector) of the MI355X
 PROFILES = os.path.join(ROOT, "profiles")
 SCORERS = {"cond": 0, "marg": 1, "static": 2, "head": 3}
+WORKLOADS = ["tiny", "qwen3_4b", "qwen3_8b", "budget64", "concurrent", "deep", "deep_concurrent"]
 HEAD_RANK = 256   # the paper's bottleneck rank for Domino's own head
-PROFILE_EVERY = 8   # kernel start/end events on every 8th eager call
+MAX_WORKERS = 16  # CPU share of one GPU on the benchmark box
+STATS_CALLS = 32  # calls of the statistics pass
 
 
 def parse():
@@ -45,14 +60,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=300)
     ap.add_argument("--warmup", type=int, default=30)
-    ap.add_argument("--workload", default="qwen3_8b",
-                    choices=["tiny", "qwen3_4b", "qwen3_8b", "budget64", "concurrent"])
+    ap.add_argument("--workload", default="qwen3_8b", choices=WORKLOADS)
     ap.add_argument("--rotate-mb", type=float, default=512.0,
                     help="logit bytes cycled through in the timed loop")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="single-core oracle leg; the all-core leg takes about half of it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--scorer", default="cond", choices=list(SCORERS),
-                    help="children function: cond (DominoTree), marg or static (the ablation arms)")
+                    help="children function: cond (DominoTree), marg or static (the ablation "
+                         "arms), head (Domino's own head)")
     ap.add_argument("--eager", action="store_true",
                     help="time the K calls launched one by one instead of one HIP-graph replay")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -60,18 +76,13 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic(plan_cfg, stage):
-    """Algorithmic work of one launch of a stage: (bytes or flops, unit, bound)."""
-    c = plan_cfg
-    rows = c["batch"] * c["L"]
-    if stage == "scan":
-        return rows * c["V"] * c["logit_bytes"], "bytes", "hbm"
-    # expansion: MFMA work of Alg. 1's expansions (GRU hidden GEMV + slice correction;
-    # Domino's own head: W_1^S S and W_2[cand] . y in place of the linear head)
-    n = c["expanded_nodes_per_call"]
-    if c.get("rank"):
-        return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["rank"] * (c["d_h"] + c["M"])), "flops", "mfma"
-    return n * 2.0 * (3 * c["d_h"] * c["d_h"] + c["M"] * c["d_h"]), "flops", "mfma"
+def expansion_flops(cfg, nodes):
+    """fp32-precision MFMA work of `nodes` expansions (W_hh . S for the GRU plus
+    the slice correction U . S; Domino's own head: W_1^S S and W_2[cand] . y)."""
+    dh, M = cfg["d_h"], cfg["M"]
+    if cfg.get("rank"):
+        return nodes * 2.0 * (3 * dh * dh + cfg["rank"] * (dh + M))
+    return nodes * 2.0 * (3 * dh * dh + M * dh)
 
 
 def source_digest(files):
@@ -97,33 +108,79 @@ def traffic_from_profiles(workload, stage):
         return None
 
 
-def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None):
-    """The oracle as it stands, one BLAS thread, on trees of the same workload."""
-    import numpy as np
-    from threadpoolctl import threadpool_limits
+def cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
+
+# ---- CPU baseline: the oracle, one BLAS thread per worker ----------------------
+_CPU = {}   # inputs of the oracle legs (inherited by the forked workers)
+
+
+def _oracle_tree(n):
     import oracle
+    c = _CPU
+    wl = c["wl"]
+    buf = c["bufs"][(n // wl.batch) % len(c["bufs"])]
+    t = n % wl.batch
+    oracle.build_tree(buf[t], wl.weights.emb, wl.weights.dtype, c["wd"],
+                      None if wl.h0 is None else wl.h0[t], wl.M, wl.B, wl.T,
+                      logits_dtype=wl.logits_dtype, scorer=c["scorer"],
+                      H=None if c["head"] is None else c["head"][1][t])
+
+
+def _worker(args):
+    """Trees built by one pool worker in `seconds` (tree indices start at `first`)."""
+    first, stride, seconds = args
+    from threadpoolctl import threadpool_limits
+    n, t0 = 0, time.perf_counter()
+    with threadpool_limits(limits=1):
+        while True:
+            _oracle_tree(first + n * stride)
+            n += 1
+            if time.perf_counter() - t0 >= seconds and n >= 2:
+                return n, time.perf_counter() - t0
+
+
+def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None):
+    """The oracle as it stands: a single-core leg, then an all-core fork pool."""
+    import multiprocessing as mp
     w = wl.weights
     wd = dict(w_ih=w.w_ih, w_hh=w.w_hh, b_ih=w.b_ih, b_hh=w.b_hh, w_c=w.w_c, b_c=w.b_c,
               dtype=w.dtype)
     if head is not None:
         wd.update(w1=head[0].w1, w2=head[0].w2)
-    n = 0
-    t0 = time.perf_counter()
-    with threadpool_limits(limits=1):
-        while True:
-            buf = bufs_host[(n // wl.batch) % len(bufs_host)]
-            t = n % wl.batch
-            oracle.build_tree(buf[t], w.emb, w.dtype, wd, None if wl.h0 is None else wl.h0[t],
-                              wl.M, wl.B, wl.T, logits_dtype=wl.logits_dtype, scorer=scorer,
-                              H=None if head is None else head[1][t])
-            n += 1
-            el = time.perf_counter() - t0
-            if el >= seconds and n >= 3:
-                break
-    return {"value": n / el, "unit": "trees/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} trees of the {wl_name} workload (first rotation buffers), "
-                      f"float64 numpy oracle, 1 BLAS thread, {el:.1f} s"}
+    _CPU.update(wl=wl, bufs=bufs_host, wd=wd, scorer=scorer, head=head)
+    n1, el1 = _worker((0, 1, seconds))
+    nproc = os.cpu_count() or 1
+    workers = max(1, min(nproc, MAX_WORKERS))
+    leg = max(2.0, seconds / 2)
+    with mp.get_context("fork").Pool(workers) as pool:
+        t0 = time.perf_counter()
+        res = pool.map(_worker, [(1000 + i, workers, leg) for i in range(workers)])
+        wall = time.perf_counter() - t0
+    nall = sum(n for n, _ in res)
+    return {"value": nall / wall, "unit": "trees/s", "cores": workers, "kind": "oracle",
+            "sample": f"{nall} trees of the {wl_name} workload on {workers} worker processes "
+                      f"({wall:.1f} s wall), float64 numpy oracle, 1 BLAS thread each; "
+                      f"single core: {n1} trees in {el1:.1f} s",
+            "single_core": {"value": n1 / el1, "unit": "trees/s", "cores": 1},
+            "nproc": nproc, "cpu_model": cpu_model()}
+
+
+def group_size(d_h, num_cus, batch):
+    """Workgroups per tree of the expansion kernel (the library's rule): the largest
+    power of two <= 16 with >= 32 hidden units (a multiple of 16) per member and
+    a grid of at most one workgroup per CU."""
+    G = 16
+    while G > 1 and (d_h // G < 32 or (d_h // G) % 16 != 0 or 8 * G * ((batch + 7) // 8) > num_cus):
+        G //= 2
+    return G
 
 
 def main():
@@ -135,15 +192,33 @@ def main():
         sys.exit(2)
 
     import numpy as np
-    import torch
 
-    from paper_2607_08642_amd import binding, synth
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    dev = torch.device("cuda:0")
+    from paper_2607_08642_amd import synth
 
     wl = synth.WORKLOADS[args.workload]()
     w = wl.weights
     d = w.dtype
+    head = None
+    if args.scorer == "head":
+        # Domino's own head (dt_build_tree_head): d_H = the drafter's width,
+        # rank 256, synthetic hidden states
+        hw = synth.domino_head(43, w.V, w.d_e, w.d_h, HEAD_RANK, d, w2_scale=0.5)
+        hH = synth.hidden_states(43, wl.batch, wl.L, w.d_e, d)
+        head = (hw, hH)
+    per_buf = wl.logits.nbytes
+    nbuf = max(1, math.ceil(args.rotate_mb * 2**20 / per_buf))
+    bufs_host = [wl.logits] + [synth.logits_buffer(wl.name, i, wl.batch) for i in range(1, nbuf)]
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds, SCORERS[args.scorer], head)
+
+    # ---- the GPU from here on -------------------------------------------------
+    import torch
+
+    from paper_2607_08642_amd import binding
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
 
     def up(a, dt):
         if a is None:
@@ -157,17 +232,8 @@ def main():
                         up(w.w_c, d), up(w.b_c, d), L=wl.L, M=wl.M, B=wl.B,
                         logits_dtype=wl.logits_dtype, max_batch=wl.batch,
                         scorer=0 if args.scorer == "head" else SCORERS[args.scorer])
-    head = None
-    if args.scorer == "head":
-        # Domino's own head (dt_build_tree_head): d_H = the drafter's width,
-        # rank 256, synthetic hidden states
-        hw = synth.domino_head(43, w.V, w.d_e, w.d_h, HEAD_RANK, d, w2_scale=0.5)
-        hH = synth.hidden_states(43, wl.batch, wl.L, w.d_e, d)
-        head = (hw, hH)
-        w1, w2, Hdev = up(hw.w1, d), up(hw.w2, d), up(hH, d)
-    per_buf = wl.logits.nbytes
-    nbuf = max(1, math.ceil(args.rotate_mb * 2**20 / per_buf))
-    bufs_host = [wl.logits] + [synth.logits_buffer(wl.name, i, wl.batch) for i in range(1, nbuf)]
+    if head is not None:
+        w1, w2, Hdev = up(head[0].w1, d), up(head[0].w2, d), up(head[1], d)
     bufs = [up(b, wl.logits_dtype) for b in bufs_host]
     h0 = None if wl.h0 is None else torch.from_numpy(wl.h0).to(dev)
     out = binding.Tree.empty(wl.batch, wl.B, dev)
@@ -187,10 +253,11 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # eager pass over the same K calls: per-call GPU times and the stage
-    # events the library records on the launch stream (every PROFILE_EVERY-th call)
+    # eager pass over the K calls: per-call GPU times, and the kernels' own start
+    # and end events on the launch stream
+    profile_every = 1 if args.steps < 64 else 8
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    plan.set_profiling(PROFILE_EVERY)
+    plan.set_profiling(profile_every)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -200,10 +267,14 @@ def main():
     torch.cuda.synchronize()
     eager_wall = time.perf_counter() - t0
     per_call = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]) * 1e3  # us
-    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the sampled calls
+    stage_us = {k: v * 1e3 for k, v in plan.stage_ms().items()}  # mean over the profiled calls
+    profiled = (args.steps + profile_every - 1) // profile_every
     plan.set_profiling(0)
     eager_last = {k: getattr(out, k).cpu().clone() for k in ("tokens", "parents", "scores", "mask")}
 
+    # a read and a write of 1 GiB: nothing of the logits is left in the caches
+    flush_src = torch.empty(2**30 // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    flush_dst = torch.empty_like(flush_src)
     if args.eager:
         wall = eager_wall
     else:
@@ -219,32 +290,82 @@ def main():
         for k, v in eager_last.items():
             if not torch.equal(getattr(out, k).cpu(), v):
                 raise RuntimeError(f"graph replay differs from the eager calls in {k}")
+        flush_dst.copy_(flush_src)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         graph.replay()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        del graph
+    del flush_src, flush_dst
 
-    # expansions Alg. 1 performs: the root plus every popped node above depth L
-    # (the kernel's extra speculative expansions are not counted as useful work)
-    dep = out.depth.cpu().numpy()
-    nn = out.n_nodes.cpu().numpy()
-    expanded = int(sum(int(np.sum(dep[t, :nn[t]] < wl.L)) + 1 for t in range(wl.batch)))
-    rows = wl.batch * wl.L
+    # statistics pass: expansion steps and expanded nodes per tree (the
+    # kernel's own count, speculative expansions included), depth histogram
+    steps_tree, exp_tree, steps_call = [], [], []
+    dhist = np.zeros(wl.L + 1, np.int64)
+    alg_nodes = []
+    ncalls = min(STATS_CALLS, nbuf)
+    if head is None:
+        plan.set_profiling(1)
+        for i in range(ncalls):
+            step(i)
+            st, ex = plan.expand_stats(wl.batch)
+            steps_tree += st
+            exp_tree += ex
+            steps_call.append(max(st))
+            dep = out.depth.cpu().numpy()
+            nn = out.n_nodes.cpu().numpy()
+            for t in range(wl.batch):
+                dhist += np.bincount(dep[t, :nn[t]], minlength=wl.L + 1)
+                # Alg. 1's expansions: the root plus every popped node above depth L
+                alg_nodes.append(int(np.sum(dep[t, :nn[t]] < wl.L)) + 1)
+        plan.set_profiling(0)
+    else:
+        for i in range(ncalls):
+            step(i)
+            dep = out.depth.cpu().numpy()
+            nn = out.n_nodes.cpu().numpy()
+            for t in range(wl.batch):
+                dhist += np.bincount(dep[t, :nn[t]], minlength=wl.L + 1)
+                alg_nodes.append(int(np.sum(dep[t, :nn[t]] < wl.L)) + 1)
+    torch.cuda.synchronize()
+
     cfg = dict(batch=wl.batch, L=wl.L, V=w.V, M=wl.M, d_e=w.d_e, d_h=w.d_h,
                logit_bytes=2 if wl.logits_dtype == synth.DT_BF16 else 4,
-               expanded_nodes_per_call=expanded, rank=HEAD_RANK if head is not None else 0)
+               rank=HEAD_RANK if head is not None else 0)
+    rows = wl.batch * wl.L
     scan_bytes = rows * w.V * cfg["logit_bytes"]
-    dom = max(stage_us, key=stage_us.get)
-    work, unit, bound = algorithmic(cfg, dom)
-    dur_s = stage_us[dom] * 1e-6
-    if unit == "bytes":
-        achieved, peak, runit = work / dur_s / 1e9, HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved = work / dur_s / 1e12
-        peak = MFMA_PEAK_TFLOPS["bf16" if d == synth.DT_BF16 else "f32"]
-        runit = "TFLOP/s"
-    scan_us = stage_us["scan"]
+    scan_us, exp_us = stage_us["scan"], stage_us["expand"]
+    # expansions per call Alg. 1 performs (the kernel's speculative extra ones are
+    # not counted as useful work)
+    alg_per_call = float(np.mean(alg_nodes)) * wl.batch
+    exp_flops = expansion_flops(cfg, alg_per_call)
+    exp_roof = {"kernel": "head_tree" if head is not None else "expand",
+                "bound": "alu" if head is not None else "mfma",
+                "achieved": exp_flops / (exp_us * 1e-6) / 1e12, "peak": FP32_PEAK_TFLOPS,
+                "unit": "TFLOP/s"}
+    exp_roof["frac"] = exp_roof["achieved"] / exp_roof["peak"]
+    exp_roof["traffic"] = None if head is not None else traffic_from_profiles(wl.name, "expand")
+    scan_gbps = scan_bytes / (scan_us * 1e-6) / 1e9
+    scan_roof = {"kernel": "scan", "bound": "hbm", "achieved": scan_gbps, "peak": HBM_PEAK_GBS,
+                 "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBS,
+                 "traffic": traffic_from_profiles(wl.name, "scan")}
+    dom_is_scan = scan_us > exp_us
+    num_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    G = group_size(w.d_h, num_cus, wl.batch)
+    latency = {"expand_us": exp_us, "scan_us": scan_us}
+    if steps_call:
+        latency.update({
+            "steps_per_tree_mean": float(np.mean(steps_tree)),
+            "steps_per_call_max_mean": float(np.mean(steps_call)),
+            "us_per_step": exp_us / float(np.mean(steps_call)),
+            "expanded_nodes_per_tree_mean": float(np.mean(exp_tree)),
+            "alg_expansions_per_tree_mean": float(np.mean(alg_nodes)),
+            "us_per_pop": exp_us / wl.B,   # per tree: the trees of a call run side by side
+            "workgroups_per_tree": G, "grid": (8 * G * ((wl.batch + 7) // 8)) if G > 1 else wl.batch,
+            "waves_per_workgroup": 8, "num_cus": num_cus,
+            "stats_calls": ncalls,
+        })
     trees = wl.batch * args.steps
     res = {
         "metric": "draft trees built/sec",
@@ -268,34 +389,24 @@ def main():
                   "gpu_us_per_call_p50": float(np.percentile(per_call, 50)),
                   "gpu_us_per_call_p99": float(np.percentile(per_call, 99))},
         "stages_us": stage_us,
+        "stage_calls_profiled": profiled,
+        "scan_gbps": scan_gbps,
+        "scan_hbm_frac": scan_gbps / HBM_PEAK_GBS,
+        "roofline": scan_roof if dom_is_scan else exp_roof,
+        "scan_roofline": scan_roof,
+        "expand_roofline": exp_roof,
+        "latency": latency,
+        "depth_hist": dhist.tolist(),
     }
-    res.update({
-        "scan_gbps": scan_bytes / (scan_us * 1e-6) / 1e9,
-        "scan_hbm_frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-        "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
-                     "unit": runit, "frac": achieved / peak,
-                     "traffic": traffic_from_profiles(wl.name, dom)},
-        "scan_roofline": {"kernel": "scan", "bound": "hbm",
-                          "achieved": scan_bytes / (scan_us * 1e-6) / 1e9,
-                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                          "frac": scan_bytes / (scan_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                          "traffic": traffic_from_profiles(wl.name, "scan")},
-    })
     if head is not None:
-        # stage "expand" is the head path's tree kernel; no counter record is kept for it
         res["config"].update(d_H=w.d_e, rank=HEAD_RANK)
-        res["roofline"]["kernel"] = "head_tree"
-        res["roofline"]["traffic"] = None
-
     if args.copy_calibration:
         x = torch.empty(256 * 2**20 // 4, dtype=torch.float32, device=dev).fill_(1.0)
         y = torch.empty_like(x)
         y.copy_(x)
         torch.cuda.synchronize()
-
-    if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds,
-                                           SCORERS[args.scorer], head)
+    if cpu is not None:
+        res["cpu_baseline"] = cpu
     plan.close()
     print(json.dumps(res), flush=True)
 

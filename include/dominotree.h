@@ -213,6 +213,16 @@ void dt_plan_destroy(dt_plan *plan);
 dt_status dt_plan_set_profiling(dt_plan *plan, int every);
 dt_status dt_plan_stage_ms(dt_plan *plan, float *ms);
 
+/* Expansion statistics of the last profiled dt_build_tree call (measurement
+ * aid; profiling on, see dt_plan_set_profiling): per tree, the dependent
+ * expansion steps the kernel ran (the root's included; each step expands up to
+ * 16 nodes of one depth) and the nodes it expanded (the root included, and the
+ * speculative expansions of nodes that were not popped).  Writes n <= the last
+ * profiled call's batch entries to the host arrays steps[] and expanded[];
+ * waits for that call.  DT_ERR_SHAPE if no call was profiled since profiling
+ * was enabled. */
+dt_status dt_plan_expand_stats(dt_plan *plan, int32_t *steps, int32_t *expanded, int n);
+
 /* Workspace (bytes) for dt_scan_topm over `rows` rows. */
 dt_status dt_scan_workspace_size(int rows, int V, int M, size_t *bytes);
 

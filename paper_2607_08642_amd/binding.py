@@ -34,7 +34,8 @@ STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
 EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_create",
            "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
            "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm", "dt_head_workspace_size",
-           "dt_build_tree_head", "dt_build_tree_noalloc")
+           "dt_build_tree_head", "dt_build_tree_noalloc",
+           "dt_plan_expand_stats")
 STAGES = ("scan", "expand")
 
 
@@ -109,6 +110,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dt_build_tree_head.argtypes = [vp, vp, ci, vp, ctypes.POINTER(dt_domino_head), vp, cf, vp,
                                        sz, ctypes.POINTER(dt_tree), vp]
     lib.dt_scan_topm.argtypes = [vp, ci, ci, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
+    lib.dt_plan_expand_stats.restype = ci
+    lib.dt_plan_expand_stats.argtypes = [vp, vp, vp, ci]
     lib.dt_build_tree_noalloc.restype = ci
     lib.dt_build_tree_noalloc.argtypes = [vp, vp, ci, vp, cf, ctypes.POINTER(dt_tree), vp]
     if lib.dt_abi_version() != ABI_VERSION:
@@ -285,6 +288,13 @@ class Plan:
         ms = (ctypes.c_float * 2)()
         _check(self._lib.dt_plan_stage_ms(self.handle, ms))
         return dict(zip(STAGES, list(ms)))
+
+    def expand_stats(self, n: int):
+        """(steps, expanded) per tree of the last profiled call, as int lists."""
+        steps = (ctypes.c_int32 * n)()
+        expanded = (ctypes.c_int32 * n)()
+        _check(self._lib.dt_plan_expand_stats(self.handle, steps, expanded, n))
+        return list(steps), list(expanded)
 
     def close(self) -> None:
         if getattr(self, "handle", None):

@@ -237,7 +237,12 @@ dt_status dt_plan_set_profiling(dt_plan *p, int enable) {
       if (e != hipSuccess) return hip_fail(e, "event create");
     }
   }
+  if (enable && !p->stats) {
+    const hipError_t e = hipMalloc(&p->stats, sizeof(int32_t) * 2 * p->max_batch);
+    if (e != hipSuccess) return hip_fail(e, "stats buffer");
+  }
   p->profiling = enable > 0 ? enable : 0;
+  p->stats_batch = 0;
   p->profiled_calls = 0;
   p->calls_since = 0;
   return DT_OK;
@@ -262,8 +267,31 @@ dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
   return DT_OK;
 }
 
+dt_status dt_plan_expand_stats(dt_plan *p, int32_t *steps, int32_t *expanded, int n) {
+  if (!p || !steps || !expanded) return fail(DT_ERR_NULL, "plan, steps and expanded are required");
+  if (!p->stats || p->stats_batch == 0) return fail(DT_ERR_SHAPE, "no profiled dt_build_tree call yet");
+  if (n < 1 || n > p->stats_batch)
+    return fail(DT_ERR_SHAPE, "n %d outside [1, %d] (trees of the last profiled call)", n,
+                p->stats_batch);
+  hipError_t e0 = hipDeviceSynchronize();  // the profiled call may sit on any stream
+  if (e0 != hipSuccess) return hip_fail(e0, "device synchronize");
+  int32_t buf[2 * 256];
+  for (int t0 = 0; t0 < n; t0 += 256) {
+    const int m = n - t0 < 256 ? n - t0 : 256;
+    const hipError_t e =
+        hipMemcpy(buf, p->stats + 2 * t0, sizeof(int32_t) * 2 * m, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "stats copy");
+    for (int i = 0; i < m; ++i) {
+      steps[t0 + i] = buf[2 * i];
+      expanded[t0 + i] = buf[2 * i + 1];
+    }
+  }
+  return DT_OK;
+}
+
 void dt_plan_destroy(dt_plan *p) {
   if (!p) return;
+  if (p->stats) (void)hipFree(p->stats);
   if (p->ev) {
     for (int i = 0; i < 4 * dt::kProfSlots; ++i)
       if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
@@ -345,6 +373,10 @@ static dt_status build_tree_on(dt_plan *plan, const void *logits, int batch, con
     mode.menu_in = ws.menus;
     mode.skip_merge = 1;
     mode.bar = ws.bar + nbar;
+  }
+  if (prof) {
+    mode.stats = plan->stats;
+    plan->stats_batch = batch;
   }
   e = dt::launch_expand(plan, batch, h0, inv_tau, ws, out, s, prof ? ev[2] : nullptr,
                         prof ? ev[3] : nullptr, mode);

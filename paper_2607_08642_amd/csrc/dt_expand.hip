@@ -57,6 +57,7 @@ struct ExpArgs {
   int nocorr, emit, skip_merge;
   const float *menu_in;  // [batch][L][MP]
   float *menu_out;       // [batch][L][MP]
+  int32_t *stats;        // [batch][2] expansion steps and expanded nodes per tree, or null
   float inv_tau, c2;  // c2 = log2(e) / tau
   const uint64_t *ckeys;
   const float2 *ctail;
@@ -1156,6 +1157,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   // without taking scores below vB, and vB only grows, so it can never be
   // popped.
   expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
+  int nsteps = 1;
   for (;;) {
     const float vB = update_vb(false);
     if (wave == 0) {
@@ -1226,6 +1228,11 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     const int nc2 = scal[S_NC];
     if (nc2 == 0) continue;
     expand_chunk(cl, nc2, ndepth[cl[0]]);
+    ++nsteps;
+  }
+  if (a.stats && member == 0 && tid == 0) {
+    a.stats[2 * t] = nsteps;
+    a.stats[2 * t + 1] = scal[S_NEXP] + 1;  // the root and every expanded node
   }
   if (member != 0 || !a.emit) return;
 
@@ -1419,6 +1426,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.skip_merge = mode.skip_merge;
   a.menu_in = mode.menu_in;
   a.menu_out = mode.menu_out;
+  a.stats = mode.stats;
   a.dh = p->d_h;
   a.G = expand_group_size(p->d_h, p->num_cus, batch);
   a.norm_mode = p->norm_mode;

@@ -100,6 +100,9 @@ struct dt_plan {
   int calls_since;          // dt_build_tree calls since profiling was enabled
   int profiled_calls;       // calls recorded since profiling was enabled
   hipEvent_t *ev;           // [kProfSlots][4] start and end of both kernels, one slot per call (ring)
+  int32_t *stats;           // [max_batch][2] expansion steps and expanded nodes of the last
+                            // profiled call (device; allocated when profiling is enabled)
+  int stats_batch;          // trees of the last profiled call
 };
 
 namespace dt {
@@ -165,6 +168,7 @@ struct ExpMode {
   int skip_merge = 0;             // the rows were merged by an earlier launch of the call
   int k = 0, B = 0;               // 0: the plan's
   int32_t *bar = nullptr;         // this launch's counters (zeroed), nullptr: ws.bar
+  int32_t *stats = nullptr;       // [batch][2] steps and expanded nodes per tree (profiling)
 };
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s,

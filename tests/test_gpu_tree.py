@@ -183,6 +183,24 @@ def test_deep_tree_at_qwen_shape(k):
     assert depth >= (16 if k == 1 else 9), depth
 
 
+def test_expand_stats_count_the_chain():
+    # k = 1 over L = 16 is a chain: the root step plus one step per node above
+    # depth L, each expanding exactly one node (the statistics the bench reads)
+    wl = qwen("deep")
+    dw = DeviceWorkload(wl, max_children=1)
+    try:
+        with pytest.raises(binding.DTError):
+            dw.plan.expand_stats(1)             # nothing profiled yet
+        dw.plan.set_profiling(1)
+        got = dw.run()
+        steps, expanded = dw.plan.expand_stats(1)
+        dw.plan.set_profiling(0)
+    finally:
+        dw.close()
+    assert int(got["depth"][0].max()) == 16
+    assert steps == [16] and expanded == [16], (steps, expanded)
+
+
 def test_deep_concurrent_all_trees():
     wl = qwen("deep_concurrent")
     kinds, got = run_case(wl, name="deep_concurrent", tol=QWEN_TOL)
