@@ -90,6 +90,12 @@ struct Lds {
 };
 
 __host__ __device__ inline int mp_of(int M) { return (M + 63) / 64 * 64; }
+// Row stride (floats) of the parent states staged in LDS: rows of d_h = 256 n
+// floats would put a lane group's 16 nodes on one bank (the MFMA B operand
+// reads one row per lane); four floats of padding spread them over all banks.
+// (The staging copies 256 floats per instruction, so only then can a row be
+// padded.)
+__host__ __device__ inline int sp_stride(int dh) { return dh % 256 == 0 ? dh + 4 : dh; }
 
 // The U rows of a depth's candidates (this member's units) are staged into LDS
 // with the parent states when the slice and all rows' ids are small.
@@ -141,7 +147,7 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
   // region reused by the prologue's merge
   const int reuse = o;
   l.gpart = take(UW / 16 < NW ? NW * 3 * 256 * 4 : 0);  // k-split partial gates
-  l.Sp = take(CH * dh * 4);
+  l.Sp = take(CH * sp_stride(dh) * 4);
   l.Sn = take(CH * UW * 4);
   l.ell = take(CH * MP * 4);
   l.rnk = take(CH * MP * 2);
@@ -354,7 +360,7 @@ struct Gates<uint16_t> {  // bf16 W_hh: 16x16x32 bf16 MFMA, S split as hi + mid 
   static __device__ inline void run_pre(const ExpArgs &a, const float *Sp, const Pre &p, int ks0,
                                         int ks1, f32x4 (&acc)[3]) {
     const int lane = threadIdx.x & 63;
-    const float *srow = Sp + (lane & 15) * a.dh + (lane >> 4) * 8;
+    const float *srow = Sp + (lane & 15) * sp_stride(a.dh) + (lane >> 4) * 8;
 #pragma unroll
     for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -366,7 +372,7 @@ struct Gates<uint16_t> {  // bf16 W_hh: 16x16x32 bf16 MFMA, S split as hi + mid 
     const int lane = threadIdx.x & 63;
     const int nks = a.dh / 32;
     const uint4 *W = static_cast<const uint4 *>(a.whh);
-    const float *srow = Sp + (lane & 15) * a.dh + (lane >> 4) * 8;
+    const float *srow = Sp + (lane & 15) * sp_stride(a.dh) + (lane >> 4) * 8;
 #pragma unroll
     for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
     constexpr int PF = 2;  // k-steps of weights in flight at once
@@ -401,7 +407,7 @@ struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per 
     const int lane = threadIdx.x & 63;
     const int nq = a.dh / 16;
     const float4 *W = static_cast<const float4 *>(a.whh);
-    const float *srow = Sp + (lane & 15) * a.dh + (lane >> 4) * 4;
+    const float *srow = Sp + (lane & 15) * sp_stride(a.dh) + (lane >> 4) * 4;
 #pragma unroll
     for (int g = 0; g < 3; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int q = 2 * ks0; q < 2 * ks1; ++q) {
@@ -475,6 +481,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   const int MP = mp_of(M);
   const int UW = dh / G;       // hidden units of this member
   const int NG = UW / 16;      // unit groups of this member
+  const int SPS = sp_stride(dh);
   const bool use_pin = pin_fits(dh, G);
   const float NEG_INF = -__builtin_huge_valf();
 
@@ -614,31 +621,34 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   }
 
   // ---- one expansion step: up to 16 nodes, all at depth d (d = 0: the root) ---
+  // this wave's share of W_hh . S: unit group gu (-1: none) over k steps [gk0, gk1);
+  // when that fits kPre k steps its weight fragments stay in registers (wpre)
+  // for the whole launch: the same fragments serve every step
+  const int nks = dh / 32;
+  int gu = -1, gk0 = 0, gk1 = nks;
+  if (NG >= NW) {
+    if (wave < NG) gu = wave;
+  } else if (wave < NG * (NW / NG)) {
+    const int WPG = NW / NG, f = wave / NG;
+    gu = wave % NG;
+    gk0 = (nks * f) / WPG;
+    gk1 = (nks * (f + 1)) / WPG;
+  }
+  typename Gates<TW>::Pre wpre;
+  const bool wkeep = !a.nocorr && Gates<TW>::kPre > 0 && use_pin && gu >= 0 &&
+                     gk1 - gk0 <= Gates<TW>::kPre;
   int pb = 0;  // partial-buffer parity
   auto expand_chunk = [&](const int16_t *cn, int nc, int d) {
     // one batched round trip: the merged row of depth d (the children's
     // candidates and tail) and the parent path states of the chunk's nodes
     const int32_t *ccand = rcand;
     const float *ccandv = rcandv;
-    // this wave's share of W_hh . S: unit group gu (-1: none) over k steps [gk0, gk1);
-    // weights that fit kPre steps are loaded now, in the staging round trip
-    const int nks = dh / 32;
-    int gu = -1, gk0 = 0, gk1 = nks;
-    if (NG >= NW) {
-      if (wave < NG) gu = wave;
-    } else if (wave < NG * (NW / NG)) {
-      const int WPG = NW / NG, f = wave / NG;
-      gu = wave % NG;
-      gk0 = (nks * f) / WPG;
-      gk1 = (nks * (f + 1)) / WPG;
-    }
-    typename Gates<TW>::Pre wpre;
-    const bool wearly = !a.nocorr && Gates<TW>::kPre > 0 && use_pin && d > 0 && gu >= 0 &&
-                        gk1 - gk0 <= Gates<TW>::kPre;
+    // (this wave's W_hh fragments, when they fit kPre k steps, are in wpre:
+    // loaded once before the first step and kept in registers)
+    const bool wearly = wkeep && d > 0;
     // the root with no h0: its state is zero, so U . S = 0 and the correction is
     // the E[v] . b_c the row merge already added -- no exchange
     const bool nocorr = a.nocorr || (d == 0 && a.h0 == nullptr);
-    if (wearly) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);
     if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
     {
       // all loads are issued before the first LDS write (one wait)
@@ -666,9 +676,11 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
             const int par = nparent[cn[c]];
             if (par >= 0) slot = nstate[par];
           }
+          // (one row, or whole rows when unpadded: the 256 floats are contiguous)
+          const int c0 = (i * 256) / dh;
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              rs, (__attribute__((address_space(3))) void *)(Sp + i * 256), 16,
-              (slot * dh + k) * 4, 0, 0, kSc1);
+              rs, (__attribute__((address_space(3))) void *)(Sp + c0 * SPS + (i * 256 - c0 * dh)),
+              16, (slot * dh + k) * 4, 0, 0, kSc1);
         }
       }
       // this member's U slice of depth d's candidates, straight into LDS
@@ -743,7 +755,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           const float r = sigmoid_fast(xr[i] + gh[0][i]);
           const float z = sigmoid_fast(xz[i] + gh[1][i]);
           const float n = tanh_fast(xn[i] + r * (gh[2][i] + xb[i]));
-          const float hprev = Sp[c * dh + j0 + i];
+          const float hprev = Sp[c * SPS + j0 + i];
           sv[i] = (1.0f - z) * n + z * hprev;
           Sn[c * UW + u4 + i] = sv[i];
         }
@@ -819,7 +831,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
             const float r = sigmoid_fast(xr + gs[0]);
             const float z = sigmoid_fast(xz + gs[1]);
             const float n = tanh_fast(xn + r * (gs[2] + xb));
-            sv = (1.0f - z) * n + z * Sp[cc * dh + j];
+            sv = (1.0f - z) * n + z * Sp[cc * SPS + j];
             Sn[cc * UW + u] = sv;
           }
           const float s1 = sel::dpp_f<0x55>(sv), s2 = sel::dpp_f<0xAA>(sv), s3 = sel::dpp_f<0xFF>(sv);
@@ -1156,6 +1168,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   // >= vB, all at the depth of the first of them.  A node the cursor passes
   // without taking scores below vB, and vB only grows, so it can never be
   // popped.
+  if (wkeep) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);  // in flight during the root step
   expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
   int nsteps = 1;
   for (;;) {
