@@ -213,6 +213,26 @@ void dt_plan_destroy(dt_plan *plan);
 dt_status dt_plan_set_profiling(dt_plan *plan, int every);
 dt_status dt_plan_stage_ms(dt_plan *plan, float *ms);
 
+/* The adaptive budget: CaDDTree's cost-aware stopping rule (section 2.5)
+ * inlined into the conditional pop loop (section 3.4).  With it set, a tree
+ * keeps popping best-first while
+ *   theta(n) = (1 + Phi(n)) / (C_d + C_v(n)),  Phi(n) = sum_{s <= n} exp(g_s)
+ * improves on theta(n - 1), g_s the cumulative log-prob of pop s; the first
+ * pop that does not improve theta (theta(n) <= theta(n - 1)) is not kept, and
+ * the plan's B is the cap.  The tree is the first n* pops of the fixed-budget
+ * tree (n_nodes = n*, possibly 0; rows past it are padding).  For a convex C_v
+ * theta is unimodal and n* is its argmax; otherwise n* is its first local
+ * maximum.  The paper gives no cost model: the caller passes it.
+ *   c_draft: C_d (the draft cost of a round, any unit);
+ *   c_verify: host array of n = B + 1 floats, C_v(0), ..., C_v(B) (same unit);
+ *   C_d + C_v(i) must be positive and finite (DT_ERR_SHAPE otherwise);
+ *   c_verify = NULL turns the rule off (fixed budget B, the default).
+ * Applies to dt_build_tree, dt_build_tree_noalloc and dt_build_tree_head calls
+ * launched after it (waits for the copy; not a stream operation, so set it
+ * before capturing calls into a graph: a captured call keeps the setting it
+ * was captured with, reading the cost values current at replay). */
+dt_status dt_plan_set_adaptive_budget(dt_plan *plan, float c_draft, const float *c_verify, int n);
+
 /* Expansion statistics of the last profiled dt_build_tree call (measurement
  * aid; profiling on, see dt_plan_set_profiling): per tree, the dependent
  * expansion steps the kernel ran (the root's included; each step expands up to

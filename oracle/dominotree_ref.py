@@ -30,6 +30,11 @@ own order:
   over the concatenation of the drafter's hidden state at the position and
   the path state, delta = W_2 SiLU(W_1 [H_d; S]), with W_2's rows gathered
   for the depth's slice.  The paper prints no biases, so there are none.
+* The adaptive budget (CaDDTree's stopping rule, section 2.5, carried into
+  the conditional pop loop, section 3.4): with the cost model (C_d, C_v(n))
+  given, the loop keeps Phi(n) = sum of pi_s = exp(g_s) over the nodes popped
+  so far and stops the first time theta(n) = (1 + Phi(n)) / (C_d + C_v(n))
+  does not improve on theta(n - 1); that node is not kept.  B is the cap.
 
 Readings of the paper that this file fixes (the paper is silent on them):
 
@@ -49,6 +54,10 @@ Readings of the paper that this file fixes (the paper is silent on them):
   logits hold NaN or +inf gets status NONFINITE and no nodes.
 * Padding rows: token -1, parent -1, depth 0, position pos_offset,
   score -inf, all-zero mask row.
+* Adaptive budget: pi_s is the node's cumulative path probability exp(g_s)
+  (the paper sums the heap's cumulative path log-probs); "stops improving"
+  is theta(n) <= theta(n-1); the tree may stop at 0 nodes; theta(0) uses
+  C_v(0); the cost model is an input (the paper gives none).
 
 Pins: see tests/test_oracle_*.py (library routines, brute force, closed forms,
 the greedy chain, the factorised tree, a frontier builder, a hand-derived
@@ -301,12 +310,15 @@ def _empty_tree(B: int, pos_offset: int, status: int):
 def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                h0: Optional[np.ndarray], M: int, B: int, T: float,
                max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
-               logits_dtype: int = DT_F32, scorer: int = SCORER_COND, H: Optional[np.ndarray] = None):
+               logits_dtype: int = DT_F32, scorer: int = SCORER_COND, H: Optional[np.ndarray] = None,
+               budget_costs=None):
     """Build one draft tree (Alg. 1) and emit it in pop order.
 
     X: [L, V] stored marginal logits of one tree; emb: [V, d_e]; weights: dict
     with w_ih, w_hh, b_ih, b_hh, w_c, b_c, dtype (HEAD: also w1 [r, d_H + d_h]
     and w2 [V, r]); h0: [d_h] or None (zeros); H: [L, d_H], HEAD only.
+    budget_costs: None (fixed budget B) or (C_d, C_v[0..B]) for the adaptive
+    budget, B then being the cap.
     Returns a dict of emitted arrays plus the smallest decisive score gap.
     """
     Xd = widen(X, logits_dtype)
@@ -331,7 +343,20 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
         next_id += 1
     # Alg. 1 step 4: pop the best entry, add it to the tree, push its children
     tree = []          # (token, g, slot, depth, parent pop index, ell, ell_out, rank)
+    if budget_costs is not None:
+        c_d, c_v = float(budget_costs[0]), np.asarray(budget_costs[1], np.float64)
+        phi = 0.0
+        theta = 1.0 / (c_d + c_v[0])   # theta(0): the empty tree
     while len(tree) < B and heap:
+        if budget_costs is not None:
+            # adaptive budget: theta(n) with the best entry as node n
+            n = len(tree) + 1
+            th = (1.0 + phi + math.exp(-heap[0][0])) / (c_d + c_v[n])
+            gaps.append(("budget", abs(th - theta) / theta))
+            if th <= theta:
+                break            # theta stops improving: node n is not kept
+            phi += math.exp(-heap[0][0])
+            theta = th
         neg_g, _, (tok, g, m, S, d, parent, ell, eo, r) = heapq.heappop(heap)
         i = len(tree)
         tree.append((tok, g, m, d, parent, ell, eo, r))
@@ -347,7 +372,7 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     excluded = -math.inf
     if heap:
         excluded = -heap[0][0]
-        if len(tree) == B:
+        if len(tree) == B or (budget_costs is not None and tree):
             gaps.append(("boundary", tree[-1][1] - excluded))
     out = _emit(tree, B, pos_offset, min(v for _, v in gaps) if gaps else math.inf)
     out["gaps"] = gaps
@@ -381,12 +406,12 @@ def build_trees(logits: np.ndarray, logits_dtype: int, emb: np.ndarray, emb_dtyp
                 weights: dict, h0: Optional[np.ndarray], M: int, B: int, T: float,
                 max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
                 trees: Optional[Sequence[int]] = None, scorer: int = SCORER_COND,
-                H: Optional[np.ndarray] = None):
+                H: Optional[np.ndarray] = None, budget_costs=None):
     """build_tree over the batch (or the listed tree indices); H: [b, L, d_H]."""
     idx = range(logits.shape[0]) if trees is None else trees
     return [build_tree(logits[t], emb, emb_dtype, weights, None if h0 is None else h0[t],
                        M, B, T, max_children, norm_mode, pos_offset, logits_dtype, scorer,
-                       None if H is None else H[t])
+                       None if H is None else H[t], budget_costs)
             for t in idx]
 
 

@@ -35,7 +35,7 @@ EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_creat
            "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
            "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm", "dt_head_workspace_size",
            "dt_build_tree_head", "dt_build_tree_noalloc",
-           "dt_plan_expand_stats")
+           "dt_plan_expand_stats", "dt_plan_set_adaptive_budget")
 STAGES = ("scan", "expand")
 
 
@@ -110,6 +110,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dt_build_tree_head.argtypes = [vp, vp, ci, vp, ctypes.POINTER(dt_domino_head), vp, cf, vp,
                                        sz, ctypes.POINTER(dt_tree), vp]
     lib.dt_scan_topm.argtypes = [vp, ci, ci, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
+    lib.dt_plan_set_adaptive_budget.restype = ci
+    lib.dt_plan_set_adaptive_budget.argtypes = [vp, cf, ctypes.POINTER(cf), ci]
     lib.dt_plan_expand_stats.restype = ci
     lib.dt_plan_expand_stats.argtypes = [vp, vp, vp, ci]
     lib.dt_build_tree_noalloc.restype = ci
@@ -288,6 +290,14 @@ class Plan:
         ms = (ctypes.c_float * 2)()
         _check(self._lib.dt_plan_stage_ms(self.handle, ms))
         return dict(zip(STAGES, list(ms)))
+
+    def set_adaptive_budget(self, c_draft: float = 0.0, c_verify=None) -> None:
+        """CaDDTree's stopping rule with cost model (C_d, C_v(0..B)); None: fixed budget."""
+        if c_verify is None:
+            _check(self._lib.dt_plan_set_adaptive_budget(self.handle, 0.0, None, 0))
+            return
+        cv = (ctypes.c_float * len(c_verify))(*[float(x) for x in c_verify])
+        _check(self._lib.dt_plan_set_adaptive_budget(self.handle, float(c_draft), cv, len(c_verify)))
 
     def expand_stats(self, n: int):
         """(steps, expanded) per tree of the last profiled call, as int lists."""

@@ -267,6 +267,31 @@ dt_status dt_plan_stage_ms(dt_plan *p, float *ms) {
   return DT_OK;
 }
 
+dt_status dt_plan_set_adaptive_budget(dt_plan *p, float c_draft, const float *c_verify, int n) {
+  if (!p) return fail(DT_ERR_NULL, "plan is required");
+  if (!c_verify) {
+    p->cost = nullptr;  // (the buffer stays allocated until the plan is destroyed)
+    return DT_OK;
+  }
+  if (n != p->B + 1) return fail(DT_ERR_SHAPE, "c_verify needs B + 1 = %d entries, got %d", p->B + 1, n);
+  float host[dt::kMaxB + 2];
+  host[0] = c_draft;
+  for (int i = 0; i < n; ++i) {
+    const float den = c_draft + c_verify[i];
+    if (!(den > 0.0f) || !(den < __builtin_huge_valf()))
+      return fail(DT_ERR_SHAPE, "C_d + C_v(%d) = %g must be positive and finite", i, (double)den);
+    host[1 + i] = c_verify[i];
+  }
+  if (!p->cost_buf) {
+    const hipError_t e = hipMalloc(&p->cost_buf, sizeof(float) * (dt::kMaxB + 2));
+    if (e != hipSuccess) return hip_fail(e, "cost buffer");
+  }
+  const hipError_t e = hipMemcpy(p->cost_buf, host, sizeof(float) * (n + 1), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "cost copy");
+  p->cost = p->cost_buf;
+  return DT_OK;
+}
+
 dt_status dt_plan_expand_stats(dt_plan *p, int32_t *steps, int32_t *expanded, int n) {
   if (!p || !steps || !expanded) return fail(DT_ERR_NULL, "plan, steps and expanded are required");
   if (!p->stats || p->stats_batch == 0) return fail(DT_ERR_SHAPE, "no profiled dt_build_tree call yet");
@@ -292,6 +317,7 @@ dt_status dt_plan_expand_stats(dt_plan *p, int32_t *steps, int32_t *expanded, in
 void dt_plan_destroy(dt_plan *p) {
   if (!p) return;
   if (p->stats) (void)hipFree(p->stats);
+  if (p->cost_buf) (void)hipFree(p->cost_buf);
   if (p->ev) {
     for (int i = 0; i < 4 * dt::kProfSlots; ++i)
       if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);

@@ -58,6 +58,7 @@ struct ExpArgs {
   const float *menu_in;  // [batch][L][MP]
   float *menu_out;       // [batch][L][MP]
   int32_t *stats;        // [batch][2] expansion steps and expanded nodes per tree, or null
+  const float *cost;     // adaptive budget: C_d, C_v(0..B) (device), or null (fixed budget)
   float inv_tau, c2;  // c2 = log2(e) / tau
   const uint64_t *ckeys;
   const float2 *ctail;
@@ -1363,7 +1364,27 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         wave_sync();
       }
     }
-    if (lane == 0) scal[S_NPOP] = npop;
+    if (lane == 0) {
+      int keep = npop;
+      if (a.cost) {
+        // the adaptive budget (CaDDTree's stopping rule, section 2.5, in the pop
+        // loop, section 3.4): pop n is kept while theta(n) = (1 + Phi(n)) /
+        // (C_d + C_v(n)) improves on theta(n - 1), Phi(n) = sum of exp(g) over
+        // the first n pops.  The rule only truncates the pop sequence.
+        const float cd = a.cost[0];
+        float phi = 0.0f, theta = 1.0f / (cd + a.cost[1]);
+        keep = 0;
+        for (int i = 0; i < npop; ++i) {
+          const float pi = exp_hw(ng[order[i]]);
+          const float th = (1.0f + phi + pi) / (cd + a.cost[2 + i]);
+          if (!(th > theta)) break;
+          phi += pi;
+          theta = th;
+          keep = i + 1;
+        }
+      }
+      scal[S_NPOP] = keep;
+    }
   }
   __syncthreads();
 
@@ -1440,6 +1461,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.menu_in = mode.menu_in;
   a.menu_out = mode.menu_out;
   a.stats = mode.stats;
+  a.cost = mode.emit ? p->cost : nullptr;
   a.dh = p->d_h;
   a.G = expand_group_size(p->d_h, p->num_cus, batch);
   a.norm_mode = p->norm_mode;

@@ -191,6 +191,7 @@ struct HeadArgs {
   float *ghs;             // [batch][B + 1][3dh]: W_hh S of the same slots
   int L, M, B, k, dh, d_H, rank, norm_mode, pos_offset;
   float c2, inv_tau;      // c2 = log2(e) / tau
+  const float *cost;      // adaptive budget: C_d, C_v(0..B) (device), or null (fixed budget)
   dt_tree out;
 };
 
@@ -375,6 +376,10 @@ __global__ __launch_bounds__(kHT) void head_tree_kernel(HeadArgs a) {
     };
 
     children(-1, 0, 0.0f);
+    // adaptive budget (CaDDTree's stopping rule, section 2.5, in the pop loop,
+    // section 3.4): Phi and theta of the nodes popped so far (every thread
+    // holds the same values)
+    float phi = 0.0f, theta = a.cost ? 1.0f / (a.cost[0] + a.cost[1]) : 0.0f;
     for (;;) {
       // pop the best entry: (g desc, insertion asc) is key desc
       const int ne = scal[H_NE];
@@ -391,6 +396,14 @@ __global__ __launch_bounds__(kHT) void head_tree_kernel(HeadArgs a) {
       if (best == 0ull || npop >= B) break;
       const int e = (int)key_index(best);
       const float g = key_value(best);
+      if (a.cost) {
+        // theta(n) with this entry as node n; stop (not kept) when it does not improve
+        const float pi = __builtin_amdgcn_exp2f(1.44269504088896341f * g);
+        const float th = (1.0f + phi + pi) / (a.cost[0] + a.cost[2 + npop]);
+        if (!(th > theta)) break;
+        phi += pi;
+        theta = th;
+      }
       const int tok = htok[e], dep = hdep[e], par = hpar[e];
       if (tid == 0) {
         hkey[e] = 0ull;
@@ -511,6 +524,7 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
   a.rank = hd.rank;
   a.norm_mode = p->norm_mode;
   a.pos_offset = p->pos_offset;
+  a.cost = p->cost;
   a.inv_tau = inv_tau;
   a.c2 = 1.4426950408889634f * inv_tau;
   a.out = *out;

@@ -100,6 +100,9 @@ struct dt_plan {
   int calls_since;          // dt_build_tree calls since profiling was enabled
   int profiled_calls;       // calls recorded since profiling was enabled
   hipEvent_t *ev;           // [kProfSlots][4] start and end of both kernels, one slot per call (ring)
+  float *cost;              // adaptive budget (dt_plan_set_adaptive_budget): [B + 2] device
+                            // floats C_d, C_v(0..B); null = fixed budget
+  float *cost_buf;          // its buffer (allocated on first use, freed with the plan)
   int32_t *stats;           // [max_batch][2] expansion steps and expanded nodes of the last
                             // profiled call (device; allocated when profiling is enabled)
   int stats_batch;          // trees of the last profiled call

@@ -80,6 +80,7 @@ def compare_tree(wl, t, got, kw, tol=None, name=""):
     variable PARITY_LOG set, one JSON line per tree is appended to that file."""
     tol = score_tol(wl) if tol is None else tol
     ref = run_oracle(wl, t, **kw)
+    kw = {k: v for k, v in kw.items() if k != "budget_costs"}   # (not a re-scoring input)
     B = wl.B
     n = int(got["n_nodes"][t])
     assert int(got["status"][t]) == ref["status"], (got["status"][t], ref["status"])

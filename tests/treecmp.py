@@ -42,7 +42,9 @@ def bands(scores, n: int, B: int, excluded: float, gap: float):
     band = np.zeros(n, np.int64)
     for i in range(1, n):
         band[i] = band[i - 1] + (1 if scores[i - 1] - scores[i] > gap else 0)
-    crossing = n == B and excluded > -math.inf and scores[n - 1] - excluded <= gap
+    # (an excluded entry exists when the budget, or the adaptive budget's stop,
+    # ended the pops; an exhausted candidate tree leaves none)
+    crossing = excluded > -math.inf and scores[n - 1] - excluded <= gap
     return band, crossing
 
 
