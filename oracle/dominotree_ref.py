@@ -35,6 +35,11 @@ own order:
   given, the loop keeps Phi(n) = sum of pi_s = exp(g_s) over the nodes popped
   so far and stops the first time theta(n) = (1 + Phi(n)) / (C_d + C_v(n))
   does not improve on theta(n - 1); that node is not kept.  B is the cap.
+* The frontier builder (Appendix B, frontier ledger and selection; section
+  4.5.1, batched construction for serving): W lanes advance depth by depth;
+  every child a lane scores goes into a ledger; the top W of each depth
+  become the next lanes; the tree is the ledger's global top B.  With W >= B
+  it selects the heap's node set.
 
 Readings of the paper that this file fixes (the paper is silent on them):
 
@@ -54,6 +59,11 @@ Readings of the paper that this file fixes (the paper is silent on them):
   logits hold NaN or +inf gets status NONFINITE and no nodes.
 * Padding rows: token -1, parent -1, depth 0, position pos_offset,
   score -inf, all-zero mask row.
+* Frontier builder: lanes keep ledger order (a lane's children follow the
+  children of the lanes before it); the top W of a depth are taken by
+  (g desc, ledger order); the final top B by (g desc, depth asc, ledger order)
+  -- the depth-then-lane tie rule -- and the tree is emitted in that order
+  (parents first: a child never scores above its parent).  D = L depths.
 * Adaptive budget: pi_s is the node's cumulative path probability exp(g_s)
   (the paper sums the heap's cumulative path log-probs); "stops improving"
   is theta(n) <= theta(n-1); the tree may stop at 0 nodes; theta(0) uses
@@ -311,7 +321,7 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
                h0: Optional[np.ndarray], M: int, B: int, T: float,
                max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
                logits_dtype: int = DT_F32, scorer: int = SCORER_COND, H: Optional[np.ndarray] = None,
-               budget_costs=None):
+               budget_costs=None, frontier_width: int = 0):
     """Build one draft tree (Alg. 1) and emit it in pop order.
 
     X: [L, V] stored marginal logits of one tree; emb: [V, d_e]; weights: dict
@@ -319,6 +329,8 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     and w2 [V, r]); h0: [d_h] or None (zeros); H: [L, d_H], HEAD only.
     budget_costs: None (fixed budget B) or (C_d, C_v[0..B]) for the adaptive
     budget, B then being the cap.
+    frontier_width: 0 (the heap of Alg. 1) or W >= 1 (the frontier builder of
+    Appendix B with W lanes; not combined with budget_costs).
     Returns a dict of emitted arrays plus the smallest decisive score gap.
     """
     Xd = widen(X, logits_dtype)
@@ -332,6 +344,10 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     S0 = np.zeros(d_h) if h0 is None else np.asarray(h0, np.float64)
     if scorer == SCORER_STATIC:
         model.static_menus(S0)
+    if frontier_width > 0:
+        if budget_costs is not None:
+            raise ValueError("the adaptive budget applies to the heap builder only")
+        return _frontier_tree(model, S0, k, B, frontier_width, pos_offset)
 
     gaps: list = []    # (kind, value): the decisive score gaps
     heap = []          # entries (-g, insertion id, payload)
@@ -380,6 +396,49 @@ def build_tree(X: np.ndarray, emb: np.ndarray, emb_dtype: int, weights: dict,
     return out
 
 
+def _frontier_tree(model, S0, k: int, B: int, W: int, pos_offset: int):
+    """The frontier builder (Appendix B): W lanes per depth, a ledger of every
+    scored child, the global top B of the ledger."""
+    gaps: list = []
+    # ledger entries: [g, depth, token, parent ledger index, ell, ell_out, rank, slot]
+    ledger = []
+    lanes = [(-1, S0, 0.0)]        # (ledger index of the lane's node, path state, g)
+    for d in range(1, model.L + 1):
+        row = []                   # ledger indices scored at this depth, in ledger order
+        states = {}
+        for li, S, g in lanes:
+            kids, ell_out = model.children(S, d, k, gaps)
+            for r, (tok, ell, m, cS) in enumerate(kids):
+                row.append(len(ledger))
+                states[len(ledger)] = cS
+                ledger.append([g + ell, d, tok, li, ell, ell_out, r, m])
+        if not row or d == model.L:
+            break
+        # the top W of this depth by (g desc, ledger order) advance, in ledger order
+        best = sorted(row, key=lambda e: (-ledger[e][0], e))
+        if len(best) > W:
+            gaps.append(("frontier", ledger[best[W - 1]][0] - ledger[best[W]][0]))
+        keep = sorted(best[:W])
+        lanes = [(e, states[e], ledger[e][0]) for e in keep]
+    # the tree: the ledger's global top B by (g desc, depth asc, ledger order)
+    order = sorted(range(len(ledger)), key=lambda e: (-ledger[e][0], ledger[e][1], e))
+    sel = order[:B]
+    pos = {e: i for i, e in enumerate(sel)}
+    tree = []
+    for e in sel:
+        g, d, tok, li, ell, eo, r, m = ledger[e]
+        tree.append((tok, g, m, d, -1 if li < 0 else pos[li], ell, eo, r))
+    for i in range(len(tree) - 1):
+        gaps.append(("pop", tree[i][1] - tree[i + 1][1]))
+    excluded = ledger[order[B]][0] if len(order) > B else -math.inf
+    if len(order) > B:
+        gaps.append(("boundary", tree[-1][1] - excluded))
+    out = _emit(tree, B, pos_offset, min(v for _, v in gaps) if gaps else math.inf)
+    out["gaps"] = gaps
+    out["excluded"] = excluded
+    return out
+
+
 def _emit(tree, B: int, pos_offset: int, min_gap: float):
     """Pop-order arrays and the ancestor-or-self mask (section 3.5)."""
     out = _empty_tree(B, pos_offset, 0)
@@ -406,12 +465,12 @@ def build_trees(logits: np.ndarray, logits_dtype: int, emb: np.ndarray, emb_dtyp
                 weights: dict, h0: Optional[np.ndarray], M: int, B: int, T: float,
                 max_children: int = 0, norm_mode: int = NORM_TAIL, pos_offset: int = 0,
                 trees: Optional[Sequence[int]] = None, scorer: int = SCORER_COND,
-                H: Optional[np.ndarray] = None, budget_costs=None):
+                H: Optional[np.ndarray] = None, budget_costs=None, frontier_width: int = 0):
     """build_tree over the batch (or the listed tree indices); H: [b, L, d_H]."""
     idx = range(logits.shape[0]) if trees is None else trees
     return [build_tree(logits[t], emb, emb_dtype, weights, None if h0 is None else h0[t],
                        M, B, T, max_children, norm_mode, pos_offset, logits_dtype, scorer,
-                       None if H is None else H[t], budget_costs)
+                       None if H is None else H[t], budget_costs, frontier_width)
             for t in idx]
 
 
