@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 1
+#define DT_ABI_VERSION 2
 
 typedef enum { DT_F32 = 0, DT_BF16 = 1 } dt_dtype;
 
@@ -78,8 +78,9 @@ typedef enum {
                                  hundreds of exactly tied scores can cause it.  The tree
                                  is still a valid best-first tree but exact ties may be
                                  resolved differently from insertion order. */
-#define DT_TREE_TIMEOUT 0x4   /* a cross-workgroup wait gave up after its spin limit;
-                                 the tree's contents are then unspecified */
+#define DT_TREE_TIMEOUT 0x4   /* a cross-workgroup wait gave up after its spin limit
+                                 (dt_options.debug_spin_limit): the tree is emitted
+                                 with no nodes, like a non-finite one */
 
 /* normalisation of the corrected slice (dt_options.norm_mode) */
 #define DT_NORM_TAIL 0  /* logZ includes the uncorrected out-of-slice mass R_d */
@@ -116,6 +117,20 @@ typedef struct {
   int norm_mode;    /* DT_NORM_TAIL (default) or DT_NORM_SLICE */
   int pos_offset;   /* position_ids = pos_offset + depth */
   int scorer;       /* DT_SCORER_COND (default, 0), DT_SCORER_MARG or DT_SCORER_STATIC */
+  int frontier_width;   /* 0 (default): the best-first heap of Alg. 1.  W >= 1: the
+                           frontier builder of Appendix B (the serving builder of
+                           section 4.5.1): depth by depth, only the W best nodes of
+                           the depth (score desc, then the order in which they were
+                           scored) are expanded, every scored child is a candidate,
+                           and the tree is the B best candidates by (score desc,
+                           depth asc, scoring order), emitted in that order.  W >= B
+                           gives the heap's tree (exact score ties aside); W < B an
+                           approximation of it.  Not with dt_build_tree_head or the
+                           adaptive budget. */
+  int debug_spin_limit; /* polls before a wait of the workgroups that build a tree
+                           together gives up (0: the default, about 2^18 polls,
+                           ~0.3 s); a tree whose wait gave up carries DT_TREE_TIMEOUT
+                           and no nodes.  A small value exercises that path. */
 } dt_options;
 
 /* Output tree of every batch entry b (device pointers, caller-owned).

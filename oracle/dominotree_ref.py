@@ -403,6 +403,7 @@ def _frontier_tree(model, S0, k: int, B: int, W: int, pos_offset: int):
     # ledger entries: [g, depth, token, parent ledger index, ell, ell_out, rank, slot]
     ledger = []
     lanes = [(-1, S0, 0.0)]        # (ledger index of the lane's node, path state, g)
+    cuts = []                      # (depth, W-th minus (W+1)-th score of the depth)
     for d in range(1, model.L + 1):
         row = []                   # ledger indices scored at this depth, in ledger order
         states = {}
@@ -418,6 +419,7 @@ def _frontier_tree(model, S0, k: int, B: int, W: int, pos_offset: int):
         best = sorted(row, key=lambda e: (-ledger[e][0], e))
         if len(best) > W:
             gaps.append(("frontier", ledger[best[W - 1]][0] - ledger[best[W]][0]))
+            cuts.append((d, ledger[best[W - 1]][0] - ledger[best[W]][0]))
         keep = sorted(best[:W])
         lanes = [(e, states[e], ledger[e][0]) for e in keep]
     # the tree: the ledger's global top B by (g desc, depth asc, ledger order)
@@ -436,6 +438,7 @@ def _frontier_tree(model, S0, k: int, B: int, W: int, pos_offset: int):
     out = _emit(tree, B, pos_offset, min(v for _, v in gaps) if gaps else math.inf)
     out["gaps"] = gaps
     out["excluded"] = excluded
+    out["frontier_cut"] = cuts
     return out
 
 

@@ -25,7 +25,7 @@ DT_SCORER_STATIC = 2
 DT_TREE_NONFINITE = 0x1
 DT_TREE_TRUNCATED = 0x2
 DT_TREE_TIMEOUT = 0x4
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
           -4: "DT_ERR_UNSUPPORTED", -5: "DT_ERR_WORKSPACE", -6: "DT_ERR_ALIGN", -7: "DT_ERR_HIP"}
@@ -61,7 +61,8 @@ class dt_domino_head(ctypes.Structure):
 
 class dt_options(ctypes.Structure):
     _fields_ = [("max_children", ctypes.c_int), ("norm_mode", ctypes.c_int),
-                ("pos_offset", ctypes.c_int), ("scorer", ctypes.c_int)]
+                ("pos_offset", ctypes.c_int), ("scorer", ctypes.c_int),
+                ("frontier_width", ctypes.c_int), ("debug_spin_limit", ctypes.c_int)]
 
 
 class dt_tree(ctypes.Structure):
@@ -189,7 +190,8 @@ class Plan:
     def __init__(self, emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c, *, L: int, M: int, B: int,
                  logits_dtype: int, max_batch: int = 1, max_children: int = 0,
                  norm_mode: int = DT_NORM_TAIL, pos_offset: int = 0,
-                 scorer: int = DT_SCORER_COND):
+                 scorer: int = DT_SCORER_COND, frontier_width: int = 0,
+                 debug_spin_limit: int = 0):
         lib = load()
         self._lib = lib
         self.emb = emb
@@ -200,7 +202,8 @@ class Plan:
         wdt = _dtype_code(emb)
         gru = dt_gru(_ptr(w_ih), _ptr(w_hh), _ptr(b_ih), _ptr(b_hh), self.d_e, self.d_h)
         head = dt_head(_ptr(w_c), _ptr(b_c))
-        opts = dt_options(max_children, norm_mode, pos_offset, scorer)
+        opts = dt_options(max_children, norm_mode, pos_offset, scorer, frontier_width,
+                          debug_spin_limit)
         h = ctypes.c_void_p()
         _check(lib.dt_plan_create(ctypes.byref(h), _ptr(emb), self.V, self.d_e, ctypes.byref(gru),
                                   ctypes.byref(head), wdt, L, M, B, logits_dtype, max_batch,
@@ -320,7 +323,7 @@ class Plan:
 
 def build_tree(marginal_logits, emb, gru_weights, correction_head, L: int, M: int, B: int,
                T: float, h0=None, max_children: int = 0, norm_mode: int = DT_NORM_TAIL,
-               pos_offset: int = 0, scorer: int = DT_SCORER_COND) -> Tree:
+               pos_offset: int = 0, scorer: int = DT_SCORER_COND, frontier_width: int = 0) -> Tree:
     """One-shot form of the paper's build_tree(...) -> tree (creates and drops a plan).
 
     gru_weights = (w_ih, w_hh, b_ih, b_hh); correction_head = (w_c, b_c).
@@ -330,7 +333,7 @@ def build_tree(marginal_logits, emb, gru_weights, correction_head, L: int, M: in
     plan = Plan(emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c, L=L, M=M, B=B,
                 logits_dtype=_dtype_code(marginal_logits), max_batch=marginal_logits.shape[0],
                 max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset,
-                scorer=scorer)
+                scorer=scorer, frontier_width=frontier_width)
     try:
         return plan.build_tree(marginal_logits, T, h0)
     finally:

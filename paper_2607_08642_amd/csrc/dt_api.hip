@@ -135,9 +135,11 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
       d_h > dt::kMaxDh || d_h % 32 != 0)
     return fail(DT_ERR_UNSUPPORTED,
                 "outside the envelope (M<=256, B<=256, L<=64, d_e<=8192, 32<=d_h<=1024, d_h%%32==0)");
-  dt_options o = {0, DT_NORM_TAIL, 0, 0};
+  dt_options o = {0, DT_NORM_TAIL, 0, 0, 0, 0};
   if (opts) o = *opts;
   if (o.max_children < 0) return fail(DT_ERR_SHAPE, "max_children must be >= 0");
+  if (o.frontier_width < 0 || o.debug_spin_limit < 0)
+    return fail(DT_ERR_SHAPE, "frontier_width and debug_spin_limit must be >= 0");
   if (o.norm_mode != DT_NORM_TAIL && o.norm_mode != DT_NORM_SLICE)
     return fail(DT_ERR_UNSUPPORTED, "norm_mode must be DT_NORM_TAIL or DT_NORM_SLICE");
   if (o.scorer != DT_SCORER_COND && o.scorer != DT_SCORER_MARG && o.scorer != DT_SCORER_STATIC)
@@ -147,22 +149,25 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
       !aligned(head->w, ws) || (gru->b_ih && !aligned(gru->b_ih, ws)) ||
       (gru->b_hh && !aligned(gru->b_hh, ws)) || (head->b && !aligned(head->b, ws)))
     return fail(DT_ERR_ALIGN, "emb must be 16-byte aligned, weights naturally aligned");
-  int dev = 0, ncu = 0, maxlds = 0;
+  int dev = 0, ncu = 0, maxlds = 0, nxcd = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&nxcd, hipDeviceAttributeNumberOfXccs, dev);
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return hip_fail(e, "device query");
+  if (nxcd < 1 || nxcd > dt::kMaxXcd)
+    return fail(DT_ERR_UNSUPPORTED, "device reports %d XCDs; 1 to %d are supported", nxcd, dt::kMaxXcd);
   const int nchunks = dt::scan_geom(1, V, M).nchunks;
   if (dt::merge_lds_bytes(dt::scan_geom(1, V, M)) > (size_t)dt::kMergeLdsMax)
     return fail(DT_ERR_UNSUPPORTED, "the row merge of V and M needs %zu bytes of LDS, more than %d",
                 dt::merge_lds_bytes(dt::scan_geom(1, V, M)), dt::kMergeLdsMax);
   // the expansion's LDS for every group size a batch in [1, max_batch] can use
   size_t lds_need = 0;
-  for (int G = dt::expand_group_size(d_h, ncu, max_batch);; G *= 2) {
+  for (int G = dt::expand_group_size(d_h, ncu, nxcd, max_batch);; G *= 2) {
     const size_t b = dt::expand_lds_bytes(d_h, G, M, nchunks, L);
     lds_need = b > lds_need ? b : lds_need;
-    if (G == dt::expand_group_size(d_h, ncu, 1)) break;
+    if (G == dt::expand_group_size(d_h, ncu, nxcd, 1)) break;
   }
   if (lds_need > (size_t)maxlds)
     return fail(DT_ERR_UNSUPPORTED,
@@ -192,6 +197,9 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   p->nf_pad = (p->nf + dt::kFoldBN - 1) / dt::kFoldBN * dt::kFoldBN;
   p->has_bc = head->b != nullptr;
   p->num_cus = ncu;
+  p->num_xcd = nxcd;
+  p->frontier_w = o.frontier_width;
+  p->spin_limit = o.debug_spin_limit;
   p->device = dev;
   void *scratch_ptr = nullptr;
   e = scratch_address(dev, &scratch_ptr);  // once per device: dt_build_tree_noalloc's workspace
@@ -274,6 +282,8 @@ dt_status dt_plan_set_adaptive_budget(dt_plan *p, float c_draft, const float *c_
     return DT_OK;
   }
   if (n != p->B + 1) return fail(DT_ERR_SHAPE, "c_verify needs B + 1 = %d entries, got %d", p->B + 1, n);
+  if (p->frontier_w > 0)
+    return fail(DT_ERR_UNSUPPORTED, "the adaptive budget applies to the heap builder (frontier_width 0)");
   float host[dt::kMaxB + 2];
   host[0] = c_draft;
   for (int i = 0; i < n; ++i) {
@@ -497,8 +507,9 @@ static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head
       hd->rank % 8 != 0)
     return fail(DT_ERR_SHAPE, "need 8 <= d_H <= 8192 and 8 <= rank <= 1024, multiples of 8 (d_H=%d rank=%d)",
                 hd->d_H, hd->rank);
-  if (plan->scorer != DT_SCORER_COND)
-    return fail(DT_ERR_UNSUPPORTED, "the Domino head needs a plan created with DT_SCORER_COND");
+  if (plan->scorer != DT_SCORER_COND || plan->frontier_w != 0)
+    return fail(DT_ERR_UNSUPPORTED,
+                "the Domino head needs a plan created with DT_SCORER_COND and frontier_width 0");
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
   if (!dt::sel::wave_merge_fits(g.nchunks, plan->M))
     return fail(DT_ERR_UNSUPPORTED, "the Domino head needs M <= 64 and <= 16 scan segments per row (M=%d, %d)",

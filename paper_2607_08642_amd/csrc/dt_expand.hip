@@ -44,12 +44,14 @@ constexpr int NT = kExpThreads;
 constexpr int NW = NT / 64;
 constexpr int NC = kNodeCap;
 constexpr int CH = kChunkNodes;
-constexpr int kSpinLimit = 1 << 18;  // ~0.3 s: a wait this long means a fault
+constexpr int kSpinLimit = 1 << 18;  // default bound of a wait (~0.3 s): longer means a fault
 static_assert(CH == 16, "MFMA column count");
 static_assert(CH == 2 * NW, "children step: two nodes per wave");
 
 struct ExpArgs {
   int L, M, B, k, dh, G, norm_mode, pos_offset, ecap, batch, nchunks, nxcd;
+  int W;           // frontier width (Appendix B's frontier builder); 0: the heap of Alg. 1
+  int spin_limit;  // polls before a cross-workgroup wait gives up (DT_TREE_TIMEOUT)
   int use_us;  // U slices of the expanded depth staged into LDS (see us_fits)
   // ablation-arm modes (ExpMode): no correction (the marginals, or menu_in's
   // per-depth menus); menu_out: every expanded node's slot log-probs; emit = 0:
@@ -290,7 +292,7 @@ __device__ inline Compact block_compact(bool pred, int *wcnt) {
 
 // Relaxed-atomic barrier of the G members of a tree.  Each thread first waits
 // for its own stores (device-scope stores are then visible at device scope).
-__device__ inline void group_barrier(int32_t *ctr, int G, int &nbar, int *status) {
+__device__ inline void group_barrier(int32_t *ctr, int G, int &nbar, int *status, int limit) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   ++nbar;
@@ -299,7 +301,7 @@ __device__ inline void group_barrier(int32_t *ctr, int G, int &nbar, int *status
     const int target = G * nbar;
     int spins = 0;
     while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      if (++spins > kSpinLimit) {
+      if (++spins > limit) {
         *status |= DT_TREE_TIMEOUT;
         break;
       }
@@ -572,8 +574,11 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       if (tid + q * NT < UW) st_dev(root + member * UW + tid + q * NT, h0v[q]);
     if (use_pin && tid < UW) bhn[tid] = bhv;
   }
-  group_barrier(ctr, G, nbar, &scal[S_STATUS]);
-  {
+  group_barrier(ctr, G, nbar, &scal[S_STATUS], a.spin_limit);
+  // (a wait that gave up: the other members' rows may be missing, so nothing of
+  // them is read; the tree is emitted empty below)
+  const bool timed_out = scal[S_STATUS] & DT_TREE_TIMEOUT;
+  if (!timed_out) {
     // one round trip: the row flags and (U slices staged) every row's candidate ids
     const __amdgpu_buffer_rsrc_t rfl = dev_rsrc(a.rflag + (size_t)t * L);
     const __amdgpu_buffer_rsrc_t rid = dev_rsrc(a.cand + (size_t)t * L * M);
@@ -604,8 +609,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   float *osc = o.scores + (size_t)t * B;
   uint8_t *omask = o.mask + (size_t)t * B * B;
 
-  if (scal[S_STATUS] & DT_TREE_NONFINITE) {
-    if (member != 0) return;
+  // a tree with no nodes: non-finite logits, or a wait that gave up
+  auto emit_empty = [&]() {
     for (int i = tid; i < B; i += NT) {
       otok[i] = -1;
       opar[i] = -1;
@@ -618,6 +623,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       o.n_nodes[t] = 0;
       o.status[t] = scal[S_STATUS];
     }
+  };
+  if (scal[S_STATUS] & (DT_TREE_NONFINITE | DT_TREE_TIMEOUT)) {
+    if (member == 0 && a.emit) emit_empty();
     return;
   }
 
@@ -870,7 +878,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
                  make_float4(acc[0], acc[1], acc[2], acc[3]));
     }
-    if (!nocorr) group_barrier(ctr, G, nbar, &scal[S_STATUS]);
+    if (!nocorr) group_barrier(ctr, G, nbar, &scal[S_STATUS], a.spin_limit);
+    if (scal[S_STATUS] & DT_TREE_TIMEOUT) return;  // (uniform: read after the barrier)
     // 3. children of each node: normalise, rank, keep the top-k above vB
     const float vB = scalf[S_VB];
     const float R = scalf[S_R];
@@ -1173,14 +1182,33 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
   int nsteps = 1;
   for (;;) {
+    if (scal[S_STATUS] & DT_TREE_TIMEOUT) break;
     const float vB = update_vb(false);
+    if (a.W > 0) {
+      // Frontier builder (Appendix B): only the top W nodes of their depth, by
+      // (score desc, table order), become lanes.  The table is depth-ordered,
+      // and a depth's row is complete once the cursor reaches it (every node of
+      // the depth above has been passed), which is when the flags are used.
+      // Nodes the table dropped (below vB) rank below every node that can still
+      // be taken, so counting the table gives the ledger's rank.
+      const int nn = scal[S_NN];
+      for (int i = tid; i < nn; i += NT) {
+        const int di = ndepth[i];
+        const float gi = ng[i];
+        int r = 0;
+        for (int j = i - 1; j >= 0 && ndepth[j] == di && r < a.W; --j) r += ng[j] >= gi;
+        for (int j = i + 1; j < nn && ndepth[j] == di && r < a.W; ++j) r += ng[j] > gi;
+        ins[i] = (uint8_t)(r < a.W);
+      }
+      __syncthreads();
+    }
     if (wave == 0) {
       const int nn = scal[S_NN];
       int p = scal[S_CUR], c = 0, dsel = -1;
       bool done = false;
       while (!done && p < nn) {
         const int i = p + lane;
-        const bool ok = i < nn && !nexp[i] && ndepth[i] < L && ng[i] >= vB;
+        const bool ok = i < nn && !nexp[i] && ndepth[i] < L && ng[i] >= vB && (a.W == 0 || ins[i]);
         const int di = ok ? (int)ndepth[i] : -1;
         const uint64_t bal = __ballot(ok);
         if (bal == 0) {
@@ -1244,6 +1272,12 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     expand_chunk(cl, nc2, ndepth[cl[0]]);
     ++nsteps;
   }
+  if (scal[S_STATUS] & DT_TREE_TIMEOUT) {
+    // a wait gave up: the tree may hold parts of members that had not written
+    // them; it is emitted empty
+    if (member == 0 && a.emit) emit_empty();
+    return;
+  }
   if (a.stats && member == 0 && tid == 0) {
     a.stats[2 * t] = nsteps;
     a.stats[2 * t + 1] = scal[S_NEXP] + 1;  // the root and every expanded node
@@ -1258,7 +1292,36 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   // with a node per lane in registers; otherwise it scans the node table.
   // (vB is current: it is refreshed after every expansion step.)
   const int nn = scal[S_NN];
-  if (wave == 0) {
+  if (a.W > 0) {
+    // frontier builder: the ledger's global top B by (score desc, depth asc,
+    // table order) -- a parent ranks before its children -- in that order
+    const float vB = scalf[S_VB];
+    for (int i = tid; i < nn; i += NT) {
+      const float gi = ng[i];
+      const int di = ndepth[i];
+      int r = B;
+      if (gi >= vB) {
+        r = 0;
+        for (int j = 0; j < nn && r < B; ++j) {
+          const float gj = ng[j];
+          r += (gj > gi) | ((gj == gi) & ((ndepth[j] < di) | ((ndepth[j] == di) & (j < i))));
+        }
+      }
+      newidx[i] = (int16_t)(r < B ? r : -1);
+      if (r < B) order[r] = (int16_t)i;
+    }
+    if (tid == 0) scal[S_NPOP] = 0;
+    __syncthreads();
+    int sel = 0;  // selected nodes this thread holds: min(B, nodes >= vB) in all
+    for (int i = tid; i < nn; i += NT) {
+      if (newidx[i] >= 0) {
+        const int par = nparent[i];
+        ppi[i] = (int16_t)(par >= 0 ? newidx[par] : -1);
+        ++sel;
+      }
+    }
+    if (sel) atomicAdd(&scal[S_NPOP], sel);
+  } else if (wave == 0) {
     const float vB = scalf[S_VB];
     const int listed = scal[S_LIST];
     int ncand = 0;
@@ -1428,11 +1491,12 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 
 }  // namespace
 
-int expand_group_size(int d_h, int num_cus, int batch) {
-  // largest power-of-two group (<= 16, >= 32 units per member) whose grid fits
-  // one workgroup per CU
+int expand_group_size(int d_h, int num_cus, int num_xcd, int batch) {
+  // largest power-of-two group (<= 16, >= 32 units per member) whose grid
+  // (every XCD holding the same number of tree slots) fits one workgroup per CU
   int G = 16;
-  while (G > 1 && (d_h / G < 32 || (d_h / G) % 16 != 0 || 8 * G * ((batch + 7) / 8) > num_cus))
+  while (G > 1 && (d_h / G < 32 || (d_h / G) % 16 != 0 ||
+                   num_xcd * G * ((batch + num_xcd - 1) / num_xcd) > num_cus))
     G >>= 1;
   return G;
 }
@@ -1442,7 +1506,7 @@ size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L) {
 }
 
 size_t expand_part_bytes(const dt_plan *p, int batch) {
-  const int G = expand_group_size(p->d_h, p->num_cus, batch);
+  const int G = expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch);
   return (size_t)batch * 2 * G * CH * mp_of(p->M) * sizeof(float);
 }
 
@@ -1461,15 +1525,17 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.menu_in = mode.menu_in;
   a.menu_out = mode.menu_out;
   a.stats = mode.stats;
-  a.cost = mode.emit ? p->cost : nullptr;
+  a.cost = (mode.emit && p->frontier_w == 0) ? p->cost : nullptr;
   a.dh = p->d_h;
-  a.G = expand_group_size(p->d_h, p->num_cus, batch);
+  a.G = expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch);
   a.norm_mode = p->norm_mode;
   a.pos_offset = p->pos_offset;
   a.ecap = ws.ecap;
   a.batch = batch;
   a.nchunks = g.nchunks;
-  a.nxcd = 8;
+  a.nxcd = p->num_xcd;
+  a.W = mode.emit ? p->frontier_w : 0;
+  a.spin_limit = p->spin_limit > 0 ? p->spin_limit : kSpinLimit;
   a.use_us = us_fits(p->d_h, a.G, p->M, p->L) && (size_t)p->V * p->d_h * 4 < (size_t)1 << 31;
   a.inv_tau = inv_tau;
   a.c2 = 1.4426950408889634f * inv_tau;
@@ -1512,7 +1578,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   // G > 1: the grid is at most one workgroup per CU (expand_group_size), so
   // every member is resident on an otherwise idle device; members take their
   // slots in start order and every wait is bounded (DT_TREE_TIMEOUT).
-  const int grid = a.G > 1 ? 8 * a.G * ((batch + 7) / 8) : batch;
+  const int grid = a.G > 1 ? a.nxcd * a.G * ((batch + a.nxcd - 1) / a.nxcd) : batch;
   void *args[] = {&a};
   if (t0)
     e = hipExtLaunchKernel(fn, dim3(grid), dim3(NT), args, lds, s, t0, t1, 0);

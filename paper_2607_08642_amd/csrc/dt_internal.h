@@ -38,6 +38,7 @@ constexpr int kExpThreads = 512;
 constexpr int kNodeCap = 1536;       // live nodes per tree kept in LDS
 constexpr int kChunkNodes = 16;      // nodes expanded together (shared weight pass)
 constexpr int kBarStride = 64;       // ints per tree of barrier counters (own cache lines)
+constexpr int kMaxXcd = 8;           // member-slot counters: 16 ints per XCD in 2 x kBarStride
 constexpr int kProfSlots = 1024;     // profiled calls kept for stage averages
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -95,6 +96,9 @@ struct dt_plan {
   void *whh_t;      // W_hh in MFMA A-fragment order (see pack_whh_*_kernel)
   void *whh_rm;     // [3dh][dh] W_hh as given (weights dtype), for the Domino-head path
   int num_cus;
+  int num_xcd;              // XCDs of the device (workgroups are dealt to them round-robin)
+  int frontier_w;           // dt_options.frontier_width (0: the heap builder)
+  int spin_limit;           // dt_options.debug_spin_limit (0: the default)
   int device;               // the device the plan was created on (its memory lives there)
   int profiling;            // > 0: record stage events on every profiling-th dt_build_tree call
   int calls_since;          // dt_build_tree calls since profiling was enabled
@@ -177,7 +181,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
                          const Workspace &ws, const dt_tree *out, hipStream_t s,
                          hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
                          const ExpMode &mode = ExpMode());
-int expand_group_size(int d_h, int num_cus, int batch);
+int expand_group_size(int d_h, int num_cus, int num_xcd, int batch);
 size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L);
 size_t expand_part_bytes(const dt_plan *p, int batch);
 hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);

@@ -29,7 +29,8 @@ def to_dev(a: np.ndarray, dtype: int, device="cuda"):
 
 
 class DeviceWorkload:
-    def __init__(self, wl, max_children=0, norm_mode=0, pos_offset=0, scorer=0):
+    def __init__(self, wl, max_children=0, norm_mode=0, pos_offset=0, scorer=0, frontier_width=0,
+                 debug_spin_limit=0):
         w = wl.weights
         self.wl = wl
         d = synth.DT_BF16 if w.dtype == synth.DT_BF16 else synth.DT_F32
@@ -47,9 +48,12 @@ class DeviceWorkload:
         self.plan = binding.Plan(self.emb, self.w_ih, self.w_hh, self.b_ih, self.b_hh, self.w_c,
                                  self.b_c, L=wl.L, M=wl.M, B=wl.B, logits_dtype=wl.logits_dtype,
                                  max_batch=wl.batch, max_children=max_children,
-                                 norm_mode=norm_mode, pos_offset=pos_offset, scorer=pscorer)
+                                 norm_mode=norm_mode, pos_offset=pos_offset, scorer=pscorer,
+                                 frontier_width=frontier_width, debug_spin_limit=debug_spin_limit)
         self.kw = dict(max_children=max_children, norm_mode=norm_mode, pos_offset=pos_offset,
                        scorer=scorer)
+        if frontier_width:
+            self.kw["frontier_width"] = frontier_width
 
     def run(self):
         if self.kw["scorer"] == oracle.SCORER_HEAD:
@@ -80,7 +84,7 @@ def compare_tree(wl, t, got, kw, tol=None, name=""):
     variable PARITY_LOG set, one JSON line per tree is appended to that file."""
     tol = score_tol(wl) if tol is None else tol
     ref = run_oracle(wl, t, **kw)
-    kw = {k: v for k, v in kw.items() if k != "budget_costs"}   # (not a re-scoring input)
+    kw = {k: v for k, v in kw.items() if k not in ("budget_costs", "frontier_width")}  # (not re-scoring inputs)
     B = wl.B
     n = int(got["n_nodes"][t])
     assert int(got["status"][t]) == ref["status"], (got["status"][t], ref["status"])

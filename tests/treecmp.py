@@ -50,11 +50,16 @@ def bands(scores, n: int, B: int, excluded: float, gap: float):
 
 def soft_nodes(ref, n: int, gap: float):
     """Nodes whose log-prob lies within gap of their expansion's top-k cut, and
-    every node below one: another builder may keep a different child there."""
+    every node below one: another builder may keep a different child there.
+    For the frontier builder also every node deeper than a depth whose top-W cut
+    is that close: another lane may advance there."""
     soft = np.zeros(n, bool)
+    cut_depths = [d for d, v in ref.get("frontier_cut", []) if v <= gap]
+    shallow = min(cut_depths) if cut_depths else None
     for i in range(n):
         p = int(ref["parents"][i])
-        soft[i] = (ref["ell"][i] - ref["ell_out"][i] <= gap) or (p >= 0 and soft[p])
+        soft[i] = (ref["ell"][i] - ref["ell_out"][i] <= gap) or (p >= 0 and soft[p]) or \
+            (shallow is not None and int(ref["depth"][i]) > shallow)
     return soft
 
 
