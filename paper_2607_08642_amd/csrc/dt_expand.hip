@@ -83,7 +83,7 @@ struct ExpArgs {
 
 // LDS carve (byte offsets), identical on host and device
 struct Lds {
-  int ng, ntok, nparent, nstate, nslot, ndepth, nrank, nexp, newidx, elist;
+  int ng, ntok, nparent, nstate, nslot, ndepth, nrank, nexp, newidx, elist, elist2;
   int ins, popd, ppi, order, anc;
   int rcand, rcandv;  // the merged row of the depth being expanded
   int rowids, uslice;  // all rows' candidate ids; this member's U slice of one depth
@@ -132,6 +132,7 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
   l.nexp = take(NC);
   l.newidx = take(NC * 2);
   l.elist = take(NC * 2);
+  l.elist2 = take(NC * 2);
   l.ins = take(NC);
   l.popd = take(NC);
   l.ppi = take(NC * 2);
@@ -163,11 +164,13 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
 }
 
 // scalar slots in LDS
-enum { S_NN, S_VB, S_NEXP, S_STATUS, S_LIST, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR, S_CNT0 };
-// after the per-wave slots S_CNT0 ..: two counters of the nodes a vB count
-// lists (used alternately by consecutive counts)
-constexpr int S_NTOP = S_CNT0 + kExpThreads / 64;
-static_assert(S_NTOP + 2 <= 32, "scalar slots below the reduction area");
+enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NCAND, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR, S_CNT0 };
+// after the per-wave slots S_CNT0 ..: which candidate buffer holds the list,
+// the next list's count, and where the last append started
+constexpr int S_CLIST = S_CNT0 + kExpThreads / 64;
+constexpr int S_NNEXT = S_CLIST + 1;
+constexpr int S_ABASE = S_CLIST + 2;
+static_assert(S_ABASE + 1 <= 32, "scalar slots below the reduction area");
 
 
 // GRU activations on the hardware exp2 and reciprocal (about 1 ulp each):
@@ -456,6 +459,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   uint8_t *nexp = reinterpret_cast<uint8_t *>(smem + ly.nexp);
   int16_t *newidx = reinterpret_cast<int16_t *>(smem + ly.newidx);
   int16_t *elist = reinterpret_cast<int16_t *>(smem + ly.elist);
+  int16_t *elist2 = reinterpret_cast<int16_t *>(smem + ly.elist2);
   uint8_t *ins = reinterpret_cast<uint8_t *>(smem + ly.ins);
   uint8_t *popd = reinterpret_cast<uint8_t *>(smem + ly.popd);
   int16_t *ppi = reinterpret_cast<int16_t *>(smem + ly.ppi);
@@ -522,9 +526,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scal[S_NEXP] = 0;
     scal[S_STOP] = 0;
     scal[S_CUR] = 0;
-    scal[S_LIST] = -1;
-    scal[S_NTOP] = 0;
-    scal[S_NTOP + 1] = 0;
+    scal[S_NCAND] = 0;  // no candidates yet (vB is -inf)
+    scal[S_CLIST] = 0;
+    scal[S_ABASE] = 0;
   }
   __syncthreads();
 
@@ -1033,9 +1037,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       node_children(c1, p1);
     else if (lane == 0)
       wcnt[c1] = 0;
+    // (read before the barrier: thread 0 rewrites it after the barrier)
+    const int base = scal[S_NN];
     __syncthreads();
     // 4. append children (node order, then rank order) to the node table
-    const int base = scal[S_NN];
     int tot = 0;
     for (int c = 0; c < nc; ++c) tot += wcnt[c];
     for (int c = wave; c < nc; c += NW) {
@@ -1063,7 +1068,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         }
       }
     }
-    __syncthreads();
+    // (these writes touch no entry the appends above write)
     if (tid == 0) {
       int nn = base + tot;
       if (nn > NC) {
@@ -1071,56 +1076,75 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         scal[S_STATUS] |= DT_TREE_TRUNCATED;  // table overflow (massive exact ties)
       }
       scal[S_NN] = nn;
+      scal[S_ABASE] = base;
       if (d > 0) scal[S_NEXP] += nc;
     }
     if (d > 0 && tid < nc) nexp[cn[tid]] = 1;
     __syncthreads();
   };
 
-  // ---- vB = B-th best known score; drop nodes below it when room is needed --
-  // Returns vB to every thread (S_VB is written for readers past the next barrier).
-  // A count also lists the nodes scoring >= vB in elist (S_LIST names the
-  // counter holding their number; -1 once the table has changed under it).
-  int vbcall = 0;
-  auto update_vb = [&](bool compact) -> float {
+  // ---- vB = B-th best known score ---------------------------------------------
+  // The nodes scoring >= vB -- the candidates, the only nodes that can still be
+  // popped or expanded -- stay listed in one of two buffers (S_CLIST names it,
+  // S_NCAND their number).  A new vB ranks the old candidates and the children
+  // appended since, which all scored >= the old vB when they were appended; no
+  // other node can be among the B best.  (If more than the gather buffer holds,
+  // every node of the table is ranked instead.)  Returns vB to every thread;
+  // S_VB and the list are written for readers past the next barrier.
+  const int kGather = CH * MP;  // floats of `ell`, free between expansion steps
+  auto update_vb = [&]() -> float {
     const int nn = scal[S_NN];
-    float vB = scalf[S_VB];
-    if (nn >= B) {
-      const int slot = S_NTOP + (vbcall & 1);
-      float best = __builtin_huge_valf();
-      const float4 *g4 = reinterpret_cast<const float4 *>(ng);
-      const int n4 = nn >> 2;
-      for (int i = tid; i < nn; i += NT) {
-        const float gi = ng[i];
-        int cnt = 0;
+    const int ncand = scal[S_NCAND];
+    const int abase = scal[S_ABASE];
+    const int16_t *cur = scal[S_CLIST] ? elist2 : elist;
+    int16_t *nxt = scal[S_CLIST] ? elist : elist2;
+    const int ntot = ncand + (nn - abase);
+    const bool incr = ntot <= kGather;
+    const int nr = incr ? ntot : nn;  // nodes ranked
+    float *cg = ell;
+    if (incr)
+      for (int q = tid; q < ntot; q += NT) cg[q] = ng[q < ncand ? cur[q] : abase + q - ncand];
+    if (tid == 0) scal[S_NNEXT] = 0;
+    __syncthreads();
+    const float *src = incr ? cg : ng;
+    const float4 *g4 = reinterpret_cast<const float4 *>(src);
+    const int n4 = nr >> 2;
+    float best = __builtin_huge_valf();
+    for (int q = tid; q < nr; q += NT) {
+      const float gi = src[q];
+      int cnt = 0;
 #pragma unroll 4
-        for (int j = 0; j < n4; ++j) {
-          const float4 v = g4[j];
-          cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
-        }
-        for (int j = n4 * 4; j < nn; ++j) cnt += ng[j] > gi;
-        if (cnt < B) {
-          best = fminf(best, gi);
-          elist[atomicAdd(&scal[slot], 1)] = (int16_t)i;
-        }
+      for (int j = 0; j < n4; ++j) {  // (no early exit: the loads stay in flight together)
+        const float4 v = g4[j];
+        cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
       }
-      best = wave_min_f(best);
-      if (lane == 0) scalf[S_CNT0 + wave] = best;
-      __syncthreads();
-      vB = scalf[S_CNT0];
-#pragma unroll
-      for (int w = 1; w < NW; ++w) vB = fminf(vB, scalf[S_CNT0 + w]);
-      if (tid == 0) {
-        scalf[S_VB] = vB;
-        scal[S_LIST] = compact ? -1 : slot;
-        scal[S_NTOP + ((vbcall & 1) ^ 1)] = 0;  // the next count's counter
+      for (int j = n4 * 4; j < nr; ++j) cnt += src[j] > gi;
+      if (cnt < B) {  // among the B best (ties included): a candidate
+        best = fminf(best, gi);
+        nxt[atomicAdd(&scal[S_NNEXT], 1)] = (int16_t)(incr ? (q < ncand ? cur[q] : abase + q - ncand) : q);
       }
-      ++vbcall;
-    } else if (tid == 0) {
-      scal[S_LIST] = -1;
     }
-    if (!compact || nn < B) return vB;
-    // keep g >= vB (parents always score at least their children: links stay valid)
+    best = wave_min_f(best);
+    if (lane == 0) scalf[S_CNT0 + wave] = best;
+    __syncthreads();
+    float vB = scalf[S_CNT0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) vB = fminf(vB, scalf[S_CNT0 + w]);
+    if (nn < B) vB = -__builtin_huge_valf();  // fewer than B known: every node qualifies
+    if (tid == 0) {
+      scalf[S_VB] = vB;
+      scal[S_NCAND] = scal[S_NNEXT];
+      scal[S_CLIST] ^= 1;
+      scal[S_ABASE] = nn;  // (a repeated call ranks no node twice)
+    }
+    return vB;
+  };
+
+  // ---- drop the nodes below vB to make room (parents always score at least
+  // their children, so the links stay valid); the candidate list is renumbered
+  auto compact_table = [&]() {
+    const int nn = scal[S_NN];
+    const float vB = scalf[S_VB];
     for (int r0 = 0; r0 < nn; r0 += NT) {
       const int i = r0 + tid;
       const bool keep = i < nn && ng[i] >= vB;
@@ -1165,10 +1189,16 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         nexp[j] = (uint8_t)re[q];
       }
     }
+    // every candidate scores >= vB, so it is kept
+    int16_t *cur = scal[S_CLIST] ? elist2 : elist;
+    const int ncand = scal[S_NCAND];
+    for (int q = tid; q < ncand; q += NT) cur[q] = newidx[cur[q]];
     __syncthreads();
-    if (tid == 0) scal[S_NN] = kept;
+    if (tid == 0) {
+      scal[S_NN] = kept;
+      scal[S_ABASE] = kept;
+    }
     __syncthreads();
-    return vB;
   };
 
   // ---- phase A ---------------------------------------------------------------
@@ -1183,7 +1213,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int nsteps = 1;
   for (;;) {
     if (scal[S_STATUS] & DT_TREE_TIMEOUT) break;
-    const float vB = update_vb(false);
+    const float vB = update_vb();
     if (a.W > 0) {
       // Frontier builder (Appendix B): only the top W nodes of their depth, by
       // (score desc, table order), become lanes.  The table is depth-ordered,
@@ -1255,7 +1285,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     if (scal[S_NN] + nc * a.k > NC - CH) {
       // make room for this chunk's children; the cursor restarts (nodes it
       // passed are expanded or below vB, and are passed again)
-      update_vb(true);
+      compact_table();
       if (tid == 0) {
         int c2 = 0;
         for (int c = 0; c < nc; ++c) {
@@ -1322,30 +1352,16 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     }
     if (sel) atomicAdd(&scal[S_NPOP], sel);
   } else if (wave == 0) {
-    const float vB = scalf[S_VB];
-    const int listed = scal[S_LIST];
-    int ncand = 0;
-    if (listed >= 0) {
-      ncand = scal[listed];  // the last vB count listed them (in any order)
-    } else {
-      for (int r0 = 0; r0 < nn; r0 += 64) {
-        const int i = r0 + lane;
-        const bool in = i < nn && ng[i] >= vB;
-        const uint64_t bal = __ballot(in);
-        const int at = ncand + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
-        if (in && at < 64) elist[at] = (int16_t)i;
-        ncand += __popcll(bal);
-      }
-    }
-    wave_sync();
+    // the candidates (every node scoring >= vB) are listed, in any order
+    const int ncand = scal[S_NCAND];
+    const int16_t *clist = scal[S_CLIST] ? elist2 : elist;
     int npop = 0;
     bool done = false;
     if (ncand <= 64) {
       // Without exact score ties the pops are simply the candidates by score
       // (a parent scores strictly above its children, so it is popped first).
       const bool have = lane < ncand;
-      const int me = have ? elist[lane] : -1;
+      const int me = have ? clist[lane] : -1;
       const float gm = have ? ng[me] : NEG_INF;
       Sn[lane] = gm;
       wave_sync();
@@ -1371,7 +1387,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     }
     if (!done && ncand <= 64) {
       const bool have = lane < ncand;
-      const int me = have ? elist[lane] : -1;
+      const int me = have ? clist[lane] : -1;
       const int par = have ? nparent[me] : -2;
       const uint64_t gkey = have ? ((uint64_t)ordered_bits(ng[me]) << 32) |
                                        ((uint64_t)((~(uint32_t)nrank[me]) & 0xFFu) << 11) |
