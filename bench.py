@@ -31,7 +31,10 @@ HBM roofline, and the CPU baseline.
 
 --scorer marg|static times the ablation arms; --scorer head times
 dt_build_tree_head (Domino's own rank-256 SiLU head over [H_d; S], d_H = d_e,
-synthetic hidden states); its stage "expand" is the head path's tree kernel.
+synthetic hidden states); its stage "expand" is the tree kernel: the expansion
+kernel with the head's correction at the Qwen shapes (rank 256 split 16 or 32
+per member), else the one-workgroup head kernel.  --max-children k caps the
+children of a node (0: the slice, M).
 """
 from __future__ import annotations
 
@@ -66,6 +69,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="single-core oracle leg; the all-core leg takes about half of it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--max-children", type=int, default=0,
+                    help="children per expanded node (k); 0: all M slots")
     ap.add_argument("--scorer", default="cond", choices=list(SCORERS),
                     help="children function: cond (DominoTree), marg or static (the ablation "
                          "arms), head (Domino's own head)")
@@ -130,7 +135,7 @@ def _oracle_tree(n):
     t = n % wl.batch
     oracle.build_tree(buf[t], wl.weights.emb, wl.weights.dtype, c["wd"],
                       None if wl.h0 is None else wl.h0[t], wl.M, wl.B, wl.T,
-                      logits_dtype=wl.logits_dtype, scorer=c["scorer"],
+                      max_children=c["k"], logits_dtype=wl.logits_dtype, scorer=c["scorer"],
                       H=None if c["head"] is None else c["head"][1][t])
 
 
@@ -147,7 +152,7 @@ def _worker(args):
                 return n, time.perf_counter() - t0
 
 
-def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None):
+def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None, k=0):
     """The oracle as it stands: a single-core leg, then an all-core fork pool."""
     import multiprocessing as mp
     w = wl.weights
@@ -155,7 +160,7 @@ def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None):
               dtype=w.dtype)
     if head is not None:
         wd.update(w1=head[0].w1, w2=head[0].w2)
-    _CPU.update(wl=wl, bufs=bufs_host, wd=wd, scorer=scorer, head=head)
+    _CPU.update(wl=wl, bufs=bufs_host, wd=wd, scorer=scorer, head=head, k=k)
     n1, el1 = _worker((0, 1, seconds))
     nproc = os.cpu_count() or 1
     workers = max(1, min(nproc, MAX_WORKERS))
@@ -171,6 +176,12 @@ def cpu_baseline(wl_name, wl, bufs_host, seconds, scorer=0, head=None):
                       f"single core: {n1} trees in {el1:.1f} s",
             "single_core": {"value": n1 / el1, "unit": "trees/s", "cores": 1},
             "nproc": nproc, "cpu_model": cpu_model()}
+
+
+def head_on_expand(rank, G):
+    """Whether dt_build_tree_head runs on the expansion kernel (the library's
+    rule: rank a multiple of 16 G with 16, 32 or 64 ranks per member)."""
+    return rank % (16 * G) == 0 and rank // G in (16, 32, 64)
 
 
 def group_size(d_h, num_cus, batch):
@@ -211,7 +222,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds, SCORERS[args.scorer], head)
+        cpu = cpu_baseline(wl.name, wl, bufs_host, args.cpu_seconds, SCORERS[args.scorer], head,
+                           args.max_children)
 
     # ---- the GPU from here on -------------------------------------------------
     import torch
@@ -231,6 +243,7 @@ def main():
     plan = binding.Plan(emb, up(w.w_ih, d), up(w.w_hh, d), up(w.b_ih, d), up(w.b_hh, d),
                         up(w.w_c, d), up(w.b_c, d), L=wl.L, M=wl.M, B=wl.B,
                         logits_dtype=wl.logits_dtype, max_batch=wl.batch,
+                        max_children=args.max_children,
                         scorer=0 if args.scorer == "head" else SCORERS[args.scorer])
     if head is not None:
         w1, w2, Hdev = up(head[0].w1, d), up(head[0].w2, d), up(head[1], d)
@@ -305,7 +318,10 @@ def main():
     dhist = np.zeros(wl.L + 1, np.int64)
     alg_nodes = []
     ncalls = min(STATS_CALLS, nbuf)
-    if head is None:
+    num_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    G = group_size(w.d_h, num_cus, wl.batch)
+    head_fast = head is not None and head_on_expand(HEAD_RANK, G)
+    if head is None or head_fast:
         plan.set_profiling(1)
         for i in range(ncalls):
             step(i)
@@ -340,19 +356,19 @@ def main():
     # not counted as useful work)
     alg_per_call = float(np.mean(alg_nodes)) * wl.batch
     exp_flops = expansion_flops(cfg, alg_per_call)
-    exp_roof = {"kernel": "head_tree" if head is not None else "expand",
-                "bound": "alu" if head is not None else "mfma",
+    slow_head = head is not None and not head_fast
+    exp_roof = {"kernel": "head_tree" if slow_head else "expand",
+                "bound": "alu" if slow_head else "mfma",
                 "achieved": exp_flops / (exp_us * 1e-6) / 1e12, "peak": FP32_PEAK_TFLOPS,
                 "unit": "TFLOP/s"}
     exp_roof["frac"] = exp_roof["achieved"] / exp_roof["peak"]
-    exp_roof["traffic"] = None if head is not None else traffic_from_profiles(wl.name, "expand")
+    exp_roof["traffic"] = None if head is not None or args.max_children else \
+        traffic_from_profiles(wl.name, "expand")
     scan_gbps = scan_bytes / (scan_us * 1e-6) / 1e9
     scan_roof = {"kernel": "scan", "bound": "hbm", "achieved": scan_gbps, "peak": HBM_PEAK_GBS,
                  "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBS,
                  "traffic": traffic_from_profiles(wl.name, "scan")}
     dom_is_scan = scan_us > exp_us
-    num_cus = torch.cuda.get_device_properties(0).multi_processor_count
-    G = group_size(w.d_h, num_cus, wl.batch)
     latency = {"expand_us": exp_us, "scan_us": scan_us}
     if steps_call:
         latency.update({
@@ -400,6 +416,9 @@ def main():
     }
     if head is not None:
         res["config"].update(d_H=w.d_e, rank=HEAD_RANK)
+    if args.max_children:
+        res["config"]["k"] = args.max_children
+        res["config"]["workload"] += f"-k{args.max_children}"
     if args.copy_calibration:
         x = torch.empty(256 * 2**20 // 4, dtype=torch.float32, device=dev).fill_(1.0)
         y = torch.empty_like(x)

@@ -297,14 +297,23 @@ dt_status dt_head_workspace_size(const dt_plan *plan, int batch, const dt_domino
  *      depth as logits row d;
  *   the other arguments are those of dt_build_tree; the plan's linear head
  *   (dt_head) is not used, its GRU is.
- * One workgroup builds each tree, popping the heap one node at a time.
- * Envelope beyond dt_plan_create's: M <= 64; the scan's segments per row
- * <= 16 (true for V <= 163840 at any batch); k * (B + 1) <= 4096; the plan
- * created with DT_SCORER_COND; the kernel's LDS must fit the device.
- * DT_ERR_UNSUPPORTED otherwise.  Stream-ordered and capturable like
- * dt_build_tree (three kernels, no memset or copy).  Stage timing
+ * The plan must be created with DT_SCORER_COND and frontier_width 0.  Two
+ * tree kernels exist; the call takes the first whose envelope holds:
+ *  - dt_build_tree's expansion kernel with this head as the correction: the
+ *    same G workgroups per tree as dt_build_tree (G = 16 at d_h = 512 and
+ *    batch <= 16, 8 at batch 32), each owning rank / G ranks of the
+ *    bottleneck; needs rank a multiple of 16 G with rank / G in {16, 32, 64},
+ *    V * rank * (weight bytes) < 2^31 and its LDS to fit the device.  The
+ *    envelope of dt_build_tree holds otherwise (any M, B the plan allows).
+ *  - one workgroup per tree popping the heap one node at a time: M <= 64,
+ *    the scan's segments per row <= 16 (true for V <= 163840 at any batch),
+ *    k * (B + 1) <= 4096, and its LDS must fit the device.
+ * DT_ERR_UNSUPPORTED when neither holds.  dt_head_workspace_size gives the
+ * workspace of the kernel the call will take.  Stream-ordered and capturable
+ * like dt_build_tree (three kernels, no memset or copy).  Stage timing
  * (dt_plan_set_profiling) counts these calls too: stage 0 = the scan,
- * stage 1 = the tree kernel (the projection between them is not timed). */
+ * stage 1 = the tree kernel (the projection between them is not timed);
+ * dt_plan_expand_stats reports the expansion kernel's steps when it ran. */
 dt_status dt_build_tree_head(dt_plan *plan, const void *marginal_logits, int batch, const void *H,
                              const dt_domino_head *head, const float *h0, float T,
                              void *workspace, size_t ws_bytes, dt_tree *out, void *stream);

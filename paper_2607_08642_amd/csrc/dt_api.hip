@@ -497,8 +497,43 @@ dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, in
   return DT_OK;
 }
 
-// checks shared by dt_head_workspace_size and dt_build_tree_head
-static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head *hd) {
+// Domino's head on the expansion kernel (the default path's member split and
+// speculative expansion): G members per tree, member j owning ranks
+// [j rank / G, (j + 1) rank / G).  Returns G, or 0 when the shape is outside
+// that kernel's envelope and the one-workgroup head kernel builds the tree.
+static int head_fast_group(const dt_plan *p, int batch, const dt_domino_head *hd, int maxlds) {
+  const int G = dt::expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch);
+  if (hd->rank % (16 * G) != 0) return 0;
+  const int rj = hd->rank / G;
+  if (rj != 16 && rj != 32 && rj != 64) return 0;  // whole MFMA tiles; 64 % (lanes per W_2 row) == 0
+  const int es = dsize(p->wdt);
+  if ((size_t)p->V * hd->rank * es >= ((size_t)1 << 31)) return 0;  // buffer offsets of W_2 rows
+  const dt::ScanGeom g = dt::scan_geom(batch * p->L, p->V, p->M);
+  if (dt::expand_lds_bytes(p->d_h, G, p->M, g.nchunks, p->L, rj, es) > (size_t)maxlds) return 0;
+  return G;
+}
+
+struct HeadFastWs {
+  dt::Workspace ws;  // the default path's (scan lists, states, exchange, counters)
+  float *a;          // [batch * L][rank] W_1^H H
+  float *hpart;      // [batch][2][G][16][rank] partial W_1^S S of each member
+  size_t bytes;
+};
+static HeadFastWs carve_head_fast(const dt_plan *p, int batch, int rank, int G, char *base) {
+  HeadFastWs h;
+  h.ws = dt::carve(p, batch, base);
+  size_t o = h.ws.bytes;
+  h.a = base ? reinterpret_cast<float *>(base + o) : nullptr;
+  o += dt::align_up((size_t)batch * p->L * rank * sizeof(float), 256);
+  h.hpart = base ? reinterpret_cast<float *>(base + o) : nullptr;
+  o += dt::align_up((size_t)batch * 2 * G * 16 * rank * sizeof(float), 256);
+  h.bytes = o;
+  return h;
+}
+
+// checks shared by dt_head_workspace_size and dt_build_tree_head; *G the
+// fast path's group size (0: the one-workgroup head kernel)
+static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head *hd, int *G) {
   if (!plan || !hd) return fail(DT_ERR_NULL, "plan and head are required");
   if (!hd->w1 || !hd->w2) return fail(DT_ERR_NULL, "head.w1 and head.w2 are required");
   if (batch < 1 || batch > plan->max_batch)
@@ -510,6 +545,16 @@ static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head
   if (plan->scorer != DT_SCORER_COND || plan->frontier_w != 0)
     return fail(DT_ERR_UNSUPPORTED,
                 "the Domino head needs a plan created with DT_SCORER_COND and frontier_width 0");
+  int dev = 0, maxlds = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  if ((size_t)4 * 4 * hd->d_H > (size_t)maxlds)
+    return fail(DT_ERR_UNSUPPORTED, "the projection W_1^H H needs %d bytes of LDS, the device has %d",
+                16 * hd->d_H, maxlds);
+  *G = head_fast_group(plan, batch, hd, maxlds);
+  if (*G > 0) return DT_OK;
+  // the one-workgroup head kernel
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
   if (!dt::sel::wave_merge_fits(g.nchunks, plan->M))
     return fail(DT_ERR_UNSUPPORTED, "the Domino head needs M <= 64 and <= 16 scan segments per row (M=%d, %d)",
@@ -517,22 +562,24 @@ static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head
   if ((size_t)plan->k * (plan->B + 1) > (size_t)dt::kHeadCap)
     return fail(DT_ERR_UNSUPPORTED, "k * (B + 1) = %d exceeds the heap's %d entries",
                 plan->k * (plan->B + 1), dt::kHeadCap);
-  int dev = 0, maxlds = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-  if (e != hipSuccess) return hip_fail(e, "device query");
   const size_t lds = dt::head_lds_bytes(plan->L, plan->B, plan->d_h, hd->rank);
-  if (lds > (size_t)maxlds || (size_t)4 * 4 * hd->d_H > (size_t)maxlds)
+  if (lds > (size_t)maxlds)
     return fail(DT_ERR_UNSUPPORTED, "the Domino head needs %zu bytes of LDS, the device has %d", lds, maxlds);
   return DT_OK;
+}
+
+static size_t head_ws_bytes(const dt_plan *plan, int batch, const dt_domino_head *hd, int G) {
+  return G > 0 ? carve_head_fast(plan, batch, hd->rank, G, nullptr).bytes
+               : dt::carve_head(plan, batch, hd->rank, nullptr).bytes;
 }
 
 dt_status dt_head_workspace_size(const dt_plan *plan, int batch, const dt_domino_head *head,
                                  size_t *bytes) {
   if (!bytes) return fail(DT_ERR_NULL, "bytes is required");
-  const dt_status st = head_check(plan, batch, head);
+  int G = 0;
+  const dt_status st = head_check(plan, batch, head, &G);
   if (st != DT_OK) return st;
-  *bytes = dt::carve_head(plan, batch, head->rank, nullptr).bytes;
+  *bytes = head_ws_bytes(plan, batch, head, G);
   return DT_OK;
 }
 
@@ -543,10 +590,11 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
   if (!out->tokens || !out->parents || !out->depth || !out->position_ids || !out->mask ||
       !out->scores || !out->n_nodes || !out->status)
     return fail(DT_ERR_NULL, "every dt_tree output pointer is required");
-  const dt_status st = head_check(plan, batch, head);
+  int G = 0;
+  const dt_status st = head_check(plan, batch, head, &G);
   if (st != DT_OK) return st;
   if (!(T == T)) return fail(DT_ERR_SHAPE, "temperature is NaN");
-  const size_t need = dt::carve_head(plan, batch, head->rank, nullptr).bytes;
+  const size_t need = head_ws_bytes(plan, batch, head, G);
   if (!workspace || ws_bytes < need)
     return fail(DT_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
   if (!aligned(workspace, 256)) return fail(DT_ERR_ALIGN, "workspace must be 256-byte aligned");
@@ -558,7 +606,6 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
     return fail(DT_ERR_ALIGN, "logits and outputs must be naturally aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const float inv_tau = T > 0.0f ? 1.0f / T : 1.0f;
-  const dt::HeadWorkspace hw = dt::carve_head(plan, batch, head->rank, static_cast<char *>(workspace));
   const dt::ScanGeom g = dt::scan_geom(batch * plan->L, plan->V, plan->M);
   // stage timing as in dt_build_tree: stage 0 the scan, stage 1 the tree kernel
   bool prof = false;
@@ -569,6 +616,30 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
     if (cs == hipStreamCaptureStatusNone) prof = (plan->calls_since++ % plan->profiling) == 0;
   }
   hipEvent_t *ev = prof ? plan->ev + 4 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
+  if (G > 0) {
+    // the scan (clearing the expansion's barrier counters), a_d = W_1^H H_d,
+    // then the default path's expansion kernel with Domino's head
+    const HeadFastWs hf = carve_head_fast(plan, batch, head->rank, G, static_cast<char *>(workspace));
+    const int nbar = (batch + 2) * dt::kBarStride;
+    hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hf.ws, hf.ws.bar, 2 * nbar, s,
+                                          prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
+    if (e != hipSuccess) return hip_fail(e, "scan launch");
+    e = dt::launch_head_proj(plan, batch, H, *head, hf.a, s);
+    if (e != hipSuccess) return hip_fail(e, "head projection launch");
+    dt::HeadIn hin{head->w1, head->w2, hf.a, hf.hpart, head->rank, head->d_H};
+    dt::ExpMode mode;
+    mode.head = &hin;
+    if (prof) {
+      mode.stats = plan->stats;
+      plan->stats_batch = batch;
+    }
+    e = dt::launch_expand(plan, batch, h0, inv_tau, hf.ws, out, s, prof ? ev[2] : nullptr,
+                          prof ? ev[3] : nullptr, mode);
+    if (e != hipSuccess) return hip_fail(e, "expand launch (Domino head)");
+    if (prof) plan->profiled_calls++;
+    return DT_OK;
+  }
+  const dt::HeadWorkspace hw = dt::carve_head(plan, batch, head->rank, static_cast<char *>(workspace));
   hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hw.scan, nullptr, 0, s,
                                         prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "scan launch");

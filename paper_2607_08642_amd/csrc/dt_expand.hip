@@ -51,6 +51,14 @@ static_assert(CH == 2 * NW, "children step: two nodes per wave");
 struct ExpArgs {
   int L, M, B, k, dh, G, norm_mode, pos_offset, ecap, batch, nchunks, nxcd;
   int W;           // frontier width (Appendix B's frontier builder); 0: the heap of Alg. 1
+  int use_ids;     // every row's candidate ids staged in LDS (the U slices, or Domino's head)
+  // Domino's own head (section 2.3; HEAD instances): delta_m = W_2[cand_m] . y,
+  // y = SiLU(a_d + W_1^S S); member j owns the rank slice [j RJ, (j + 1) RJ)
+  int rank, RJ, ld1, d_H;
+  const void *w1;   // [rank][ld1] (weights dtype); columns d_H .. d_H + dh act on S
+  const void *w2;   // [V][rank] (weights dtype)
+  const float *ha;  // [batch * L][rank] a_d = W_1^H H_d
+  float *hpart;     // [batch][2][G][CH][rank] partial W_1^S S of each member
   int spin_limit;  // polls before a cross-workgroup wait gives up (DT_TREE_TIMEOUT)
   int use_us;  // U slices of the expanded depth staged into LDS (see us_fits)
   // ablation-arm modes (ExpMode): no correction (the marginals, or menu_in's
@@ -88,6 +96,7 @@ struct Lds {
   int rcand, rcandv;  // the merged row of the depth being expanded
   int rowids, uslice;  // all rows' candidate ids; this member's U slice of one depth
   int pin, bhn;        // GRU inputs P of the chunk's nodes (this member's units); b_hn
+  int hw2, hys, ha;    // Domino's head: W_2 rows (rank slice, weights dtype), y slice, a_d slice
   int gpart, Sp, Sn, ell, rnk, chunk, scal, total;
   int sortbuf;  // aliases gpart.. (prologue only)
 };
@@ -112,7 +121,9 @@ __host__ __device__ inline bool us_fits(int dh, int G, int M, int L) {
   return MP * (dh / G) * 4 <= 16384 && L * MP * 4 <= 8192;
 }
 
-__host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int L) {
+// rj > 0: a HEAD instance with rank slice rj and weights of wbytes bytes
+__host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int L, int rj = 0,
+                                          int wbytes = 0) {
   Lds l;
   int o = 0;
   auto take = [&](int bytes) {
@@ -141,8 +152,11 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
   l.rcand = take(MP * 4);
   l.rcandv = take(MP * 4);
   const bool us = us_fits(dh, G, M, L);
-  l.rowids = take(us ? L * MP * 4 : 0);
-  l.uslice = take(us ? MP * UW * 4 : 0);
+  l.rowids = take((us || rj) ? L * MP * 4 : 0);
+  l.uslice = take(us && !rj ? MP * UW * 4 : 0);
+  l.hw2 = take(rj ? MP * rj * wbytes : 0);
+  l.hys = take(rj ? CH * rj * 4 : 0);
+  l.ha = take(rj ? rj * 4 : 0);
   const bool pin = pin_fits(dh, G);
   l.pin = take(pin ? CH * kPinSlot * 4 : 0);
   l.bhn = take(pin ? UW * 4 : 0);
@@ -250,6 +264,13 @@ __device__ inline GruIn load_gru_in(const float *prow, const float *b_hh, int dh
   g.b = *reinterpret_cast<const float4 *>(b_hh + 2 * dh + j0);
   return g;
 }
+// four consecutive weights widened to fp32 (bf16: 8 bytes; fp32: 16 bytes)
+__device__ inline float4 load4w(const uint16_t *p) {
+  const uint2 q = *reinterpret_cast<const uint2 *>(p);
+  return make_float4(__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xFFFF0000u),
+                     __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xFFFF0000u));
+}
+__device__ inline float4 load4w(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ inline void st_dev16(__amdgpu_buffer_rsrc_t r, int byte_off, float4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, kSc1);
 }
@@ -434,7 +455,8 @@ struct Gates<float> {  // fp32 W_hh: 16x16x4 fp32 MFMA, k-groups of 16, two per 
 // every loop bound over them become constants); 0 takes them from the arguments.
 // ARMS compiles the ablation-arm modes in (nocorr, menu_in, menu_out, emit,
 // skip_merge); without it they are fixed off and cost nothing.
-template <typename TW, int SDH, int SG, int SM, int SL, bool ARMS>
+// HEAD scores with Domino's own head (a different correction; no ablation arms).
+template <typename TW, int SDH, int SG, int SM, int SL, bool ARMS, bool HEAD = false>
 __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   if constexpr (!ARMS) {
     a.nocorr = 0;
@@ -448,7 +470,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   if constexpr (SM > 0) a.M = SM;
   if constexpr (SL > 0) a.L = SL;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const Lds ly = lds_layout(a.dh, a.G, a.M, a.nchunks, a.L);
+  const Lds ly = lds_layout(a.dh, a.G, a.M, a.nchunks, a.L, HEAD ? a.RJ : 0, HEAD ? (int)sizeof(TW) : 0);
   float *ng = reinterpret_cast<float *>(smem + ly.ng);
   int32_t *ntok = reinterpret_cast<int32_t *>(smem + ly.ntok);
   int16_t *nparent = reinterpret_cast<int16_t *>(smem + ly.nparent);
@@ -475,6 +497,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int32_t *rowids = reinterpret_cast<int32_t *>(smem + ly.rowids);
   float *Us = reinterpret_cast<float *>(smem + ly.uslice);
   float *pin = reinterpret_cast<float *>(smem + ly.pin);
+  char *hw2 = smem + ly.hw2;
+  float *hys = reinterpret_cast<float *>(smem + ly.hys);
+  float *has = reinterpret_cast<float *>(smem + ly.ha);
   float *bhn = reinterpret_cast<float *>(smem + ly.bhn);
   int16_t *cl = reinterpret_cast<int16_t *>(smem + ly.chunk);
   int *scal = reinterpret_cast<int *>(smem + ly.scal);
@@ -594,13 +619,13 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     for (int q = 0; q < kIdsPer; ++q) {
       const int i = tid + q * NT;
       const int d = i / MP, m = i - d * MP;
-      ids[q] = (a.use_us && i < L * MP && m < M) ? __builtin_bit_cast(int, ld_dev4(rid, (d * M + m) * 4)) : 0;
+      ids[q] = (a.use_ids && i < L * MP && m < M) ? __builtin_bit_cast(int, ld_dev4(rid, (d * M + m) * 4)) : 0;
     }
     if (f) atomicOr(&scal[S_STATUS], f);
 #pragma unroll
     for (int q = 0; q < kIdsPer; ++q) {
       const int i = tid + q * NT;
-      if (a.use_us && i < L * MP) rowids[i] = ids[q] > 0 ? ids[q] : 0;  // dead slots (-1) read row 0, unused
+      if (a.use_ids && i < L * MP) rowids[i] = ids[q] > 0 ? ids[q] : 0;  // dead slots (-1) read row 0, unused
     }
   }
   __syncthreads();
@@ -661,7 +686,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     const bool wearly = wkeep && d > 0;
     // the root with no h0: its state is zero, so U . S = 0 and the correction is
     // the E[v] . b_c the row merge already added -- no exchange
-    const bool nocorr = a.nocorr || (d == 0 && a.h0 == nullptr);
+    // (Domino's head is not zero at a zero state: SiLU(a_d))
+    const bool nocorr = a.nocorr || (!HEAD && d == 0 && a.h0 == nullptr);
     if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
     {
       // all loads are issued before the first LDS write (one wait)
@@ -708,6 +734,25 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
               (rowids[d * MP + m] * dh + member * UW + k) * 4, 0, 0, 0);
         }
       }
+      // Domino's head: this member's rank slice of the W_2 rows of depth d's
+      // candidates straight into LDS (16 bytes per lane, lpr lanes per row),
+      // and of the depth's a_d
+      float hav = 0.0f;
+      if constexpr (HEAD) {
+        if (d < L) {
+          const int es = (int)sizeof(TW);
+          const int lpr = a.RJ * es / 16;  // lanes per row
+          const __amdgpu_buffer_rsrc_t rw2 =
+              __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.w2), 0, 0x7FFFFFF0, 0x00020000);
+          for (int i = wave; i < MP * lpr / 64; i += NW) {
+            const int m = i * (64 / lpr) + lane / lpr, part = lane - (lane / lpr) * lpr;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rw2, (__attribute__((address_space(3))) void *)(hw2 + i * 1024), 16,
+                (rowids[d * MP + m] * a.rank + member * a.RJ) * es + part * 16, 0, 0, 0);
+          }
+          if (tid < a.RJ) hav = a.ha[((size_t)t * L + d) * a.rank + member * a.RJ + tid];
+        }
+      }
       // GRU inputs of the chunk's nodes straight into LDS, one wave instruction
       // per node: lane l < 3 UW/4 takes 4 floats of gate l / (UW/4); the other
       // lanes re-read the first 16 bytes into the slot's unused tail
@@ -730,6 +775,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       if (tid == NT - 1) scalf[S_R] = rt;
       __builtin_amdgcn_s_waitcnt(0);  // includes the LDS writes of the loads above
+      if (HEAD && tid < a.RJ) has[tid] = hav;
     }
     __syncthreads();
     // 1. path states of this member's units: S = GRU(S_parent, E[token]) (section 2.3)
@@ -860,7 +906,66 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // parts of member j: a [CH][MP] block of their own (no line is shared by two writers)
     const __amdgpu_buffer_rsrc_t rmy =
         dev_rsrc(a.part + (((size_t)t * 2 + pb) * G + member) * CH * MP);
-    for (int rt = nocorr ? RT : wave; rt < RT; rt += NW) {
+    if constexpr (HEAD) {
+      // Domino's head (section 2.3).  (a) this member's part of W_1^S S_c over
+      // its units, 16 ranks per MFMA tile, published for the other members
+      const __amdgpu_buffer_rsrc_t rhp =
+          dev_rsrc(a.hpart + (((size_t)t * 2 + pb) * G + member) * CH * a.rank);
+      for (int rt = wave; rt < a.rank / 16; rt += NW) {
+        const int r = rt * 16 + (lane & 15);
+        const int c = lane & 15, kq = (lane >> 4) * 4;
+        const TW *w1r = static_cast<const TW *>(a.w1) + (size_t)r * a.ld1 + a.d_H + member * UW;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < nq; ++q) {
+          const float4 av = load4w(w1r + q * 16 + kq);
+          const float4 bv = *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+        }
+        // lane l, register i: rank rt*16 + (l/16)*4 + i of node l%16
+        if (c < nc)
+          st_dev16(rhp, (c * a.rank + rt * 16 + (lane >> 4) * 4) * 4,
+                   make_float4(acc[0], acc[1], acc[2], acc[3]));
+      }
+      group_barrier(ctr, G, nbar, &scal[S_STATUS], a.spin_limit);
+      if (scal[S_STATUS] & DT_TREE_TIMEOUT) return;  // (uniform: read after the barrier)
+      // (b) this member's rank slice of y = SiLU(a_d + W_1^S S) for the chunk's
+      // nodes: the G parts summed in member order
+      const int RJ = a.RJ, RJ4 = RJ / 4;
+      const __amdgpu_buffer_rsrc_t rha = dev_rsrc(a.hpart + ((size_t)t * 2 + pb) * G * CH * a.rank);
+      for (int e = tid; e < CH * RJ4; e += NT) {
+        const int c = e / RJ4, r4 = (e - c * RJ4) * 4;
+        float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int m2 = 0; m2 < G; ++m2)
+          sum += ld_dev16(rha, ((m2 * CH + c) * a.rank + member * RJ + r4) * 4);
+        const float x[4] = {has[r4] + sum.x, has[r4 + 1] + sum.y, has[r4 + 2] + sum.z,
+                            has[r4 + 3] + sum.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hys[c * RJ + r4 + i] = x[i] * sigmoid_fast(x[i]);
+      }
+      __syncthreads();
+      // (c) this member's part of delta[c][m] = W_2[cand_m] . y over its rank slice
+      for (int rt = wave; rt < RT; rt += NW) {
+        const int m = rt * 16 + (lane & 15);
+        const int c = lane & 15, kq = (lane >> 4) * 4;
+        const TW *w2row = reinterpret_cast<const TW *>(hw2) + m * RJ;  // slots >= M: unused
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < RJ / 16; ++q) {
+          const float4 av = load4w(w2row + q * 16 + kq);
+          const float4 bv = *reinterpret_cast<const float4 *>(hys + c * RJ + q * 16 + kq);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+        }
+        if (c < nc)
+          st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
+                   make_float4(acc[0], acc[1], acc[2], acc[3]));
+      }
+    }
+    for (int rt = (nocorr || HEAD) ? RT : wave; rt < RT; rt += NW) {
       const int m = rt * 16 + (lane & 15);
       const int c = lane & 15, kq = (lane >> 4) * 4;
       const float *urow = a.U_all + (size_t)(m < M ? ccand[m] : 0) * dh + member * UW;
@@ -1517,8 +1622,8 @@ int expand_group_size(int d_h, int num_cus, int num_xcd, int batch) {
   return G;
 }
 
-size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L) {
-  return (size_t)lds_layout(dh, G, M, nchunks, L).total;
+size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L, int rj, int wbytes) {
+  return (size_t)lds_layout(dh, G, M, nchunks, L, rj, wbytes).total;
 }
 
 size_t expand_part_bytes(const dt_plan *p, int batch) {
@@ -1552,7 +1657,23 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.nxcd = p->num_xcd;
   a.W = mode.emit ? p->frontier_w : 0;
   a.spin_limit = p->spin_limit > 0 ? p->spin_limit : kSpinLimit;
-  a.use_us = us_fits(p->d_h, a.G, p->M, p->L) && (size_t)p->V * p->d_h * 4 < (size_t)1 << 31;
+  a.use_us = !mode.head && us_fits(p->d_h, a.G, p->M, p->L) &&
+             (size_t)p->V * p->d_h * 4 < (size_t)1 << 31;
+  a.use_ids = a.use_us || mode.head != nullptr;
+  a.rank = a.RJ = a.ld1 = a.d_H = 0;
+  a.w1 = a.w2 = nullptr;
+  a.ha = nullptr;
+  a.hpart = nullptr;
+  if (mode.head) {
+    a.rank = mode.head->rank;
+    a.RJ = mode.head->rank / a.G;
+    a.d_H = mode.head->d_H;
+    a.ld1 = mode.head->d_H + p->d_h;
+    a.w1 = mode.head->w1;
+    a.w2 = mode.head->w2;
+    a.ha = mode.head->a;
+    a.hpart = mode.head->hpart;
+  }
   a.inv_tau = inv_tau;
   a.c2 = 1.4426950408889634f * inv_tau;
   a.ckeys = ws.chunk_keys;
@@ -1565,7 +1686,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.P_all = p->P_all;
   a.U_all = p->U_all;
   // (the marginals carry no E[v] . b_c term)
-  a.c_all = (mode.nocorr && !mode.menu_in) ? nullptr : p->c_all;
+  a.c_all = ((mode.nocorr && !mode.menu_in) || mode.head) ? nullptr : p->c_all;
   a.whh = p->whh_t;
   a.b_hh = p->b_hh;
   a.h0 = h0;
@@ -1573,12 +1694,22 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.part = ws.part;
   a.bar = mode.bar ? mode.bar : ws.bar;
   a.out = *out;
-  const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks, p->L);
+  const size_t lds = expand_lds_bytes(p->d_h, a.G, p->M, g.nchunks, p->L, mode.head ? a.RJ : 0,
+                                      mode.head ? (p->wdt == DT_BF16 ? 2 : 4) : 0);
   // shapes with a compiled specialisation: Qwen3 drafters (d_h = 512, M = 64,
   // L = 16) with bf16 weights at G = 16 (one to eight trees) and G = 8
   const void *fn;
   const bool arms = mode.nocorr || mode.menu_in || mode.menu_out || !mode.emit || mode.skip_merge;
-  if (arms)
+  const bool qwen = p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16;
+  if (mode.head) {
+    if (qwen && a.G == 16)
+      fn = (const void *)expand_kernel<uint16_t, 512, 16, 64, 16, false, true>;
+    else if (qwen && a.G == 8)
+      fn = (const void *)expand_kernel<uint16_t, 512, 8, 64, 16, false, true>;
+    else
+      fn = p->wdt == DT_BF16 ? (const void *)expand_kernel<uint16_t, 0, 0, 0, 0, false, true>
+                             : (const void *)expand_kernel<float, 0, 0, 0, 0, false, true>;
+  } else if (arms)
     fn = p->wdt == DT_BF16 ? (const void *)expand_kernel<uint16_t, 0, 0, 0, 0, true>
                            : (const void *)expand_kernel<float, 0, 0, 0, 0, true>;
   else if (p->wdt == DT_BF16 && a.dh == 512 && a.M == 64 && a.L == 16 && a.G == 16)

@@ -482,12 +482,11 @@ HeadWorkspace carve_head(const dt_plan *p, int batch, int rank, char *base) {
   return hw;
 }
 
+// a[row][r] = W_1^H H_row for the batch's tree-depth rows
 template <typename T>
-static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
-                                const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
-                                hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
+static hipError_t launch_proj_t(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
+                                float *a_out, hipStream_t s) {
   const int rows = batch * p->L;
-  const ScanGeom g = scan_geom(rows, p->V, p->M);
   const size_t plds = (size_t)kProjRows * hd.d_H * sizeof(float);
   const int rblocks = (rows + kProjRows - 1) / kProjRows;
   const bool fine = (size_t)rblocks * ((hd.rank + kHT / 8 - 1) / (kHT / 8)) < (size_t)p->num_cus;
@@ -497,9 +496,17 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)plds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(proj, dim3(rblocks, (hd.rank + rpb - 1) / rpb), dim3(kHT), plds, s,
-                     static_cast<const T *>(hd.w1), static_cast<const T *>(H), hw.a, rows, hd.d_H,
+                     static_cast<const T *>(hd.w1), static_cast<const T *>(H), a_out, rows, hd.d_H,
                      hd.d_H + p->d_h, hd.rank);
-  e = hipGetLastError();
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
+                                const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
+                                hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
+  const ScanGeom g = scan_geom(batch * p->L, p->V, p->M);
+  hipError_t e = launch_proj_t<T>(p, batch, H, hd, hw.a, s);
   if (e != hipSuccess) return e;
   HeadArgs a;
   a.ckeys = hw.scan.chunk_keys;
@@ -537,6 +544,12 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
   else
     hipLaunchKernelGGL(head_tree_kernel<T>, dim3(batch), dim3(kHT), lds, s, a);
   return hipGetLastError();
+}
+
+hipError_t launch_head_proj(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
+                            float *a_out, hipStream_t s) {
+  return p->wdt == DT_BF16 ? launch_proj_t<uint16_t>(p, batch, H, hd, a_out, s)
+                           : launch_proj_t<float>(p, batch, H, hd, a_out, s);
 }
 
 hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,

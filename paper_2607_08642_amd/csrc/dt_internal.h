@@ -164,9 +164,20 @@ size_t head_lds_bytes(int L, int B, int dh, int rank);
 hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
                        const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
                        hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+// a[row][r] = W_1^H H_row for the batch's L rows per tree (Domino's head)
+hipError_t launch_head_proj(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
+                            float *a_out, hipStream_t s);
+// Domino's own head on the expansion kernel: its tensors for one launch
+struct HeadIn {
+  const void *w1, *w2;  // [rank][d_H + d_h], [V][rank] (weights dtype)
+  const float *a;       // [batch * L][rank] a_d = W_1^H H_d
+  float *hpart;         // [batch][2][G][16][rank] workspace
+  int rank, d_H;
+};
 // One expansion launch: DominoTree (the default), or, for the ablation arms,
 // without the correction (nocorr: the marginals, or menu_in's per-depth menus)
-// and/or writing every expanded depth's menu (menu_out; the greedy chain).
+// and/or writing every expanded depth's menu (menu_out; the greedy chain), or
+// with Domino's own head in place of the linear one (head).
 struct ExpMode {
   int nocorr = 0;                 // no GRU, no correction, no exchange
   const float *menu_in = nullptr;  // [batch][L][MP] normalised log-probs of each depth's slots
@@ -176,13 +187,14 @@ struct ExpMode {
   int k = 0, B = 0;               // 0: the plan's
   int32_t *bar = nullptr;         // this launch's counters (zeroed), nullptr: ws.bar
   int32_t *stats = nullptr;       // [batch][2] steps and expanded nodes per tree (profiling)
+  const HeadIn *head = nullptr;   // Domino's own head in place of the linear one
 };
 hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv_tau,
                          const Workspace &ws, const dt_tree *out, hipStream_t s,
                          hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
                          const ExpMode &mode = ExpMode());
 int expand_group_size(int d_h, int num_cus, int num_xcd, int batch);
-size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L);
+size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L, int rj = 0, int wbytes = 0);
 size_t expand_part_bytes(const dt_plan *p, int batch);
 hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);
 

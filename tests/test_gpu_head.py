@@ -2,6 +2,12 @@
 delta = W_2[cand] . SiLU(W_1 [H_d; S]) with a rank-r bottleneck) against the
 oracle's SCORER_HEAD, through the C ABI.
 
+Two kernels build these trees: the default path's expansion kernel with the
+head in place of the linear correction (the member split: each of a tree's G
+workgroups owns rank / G of the bottleneck; taken when rank / G is 16, 32 or
+64 and rank is a multiple of 16 G), and the one-workgroup head kernel for
+every other shape.  The sweep covers both (the case list notes which).
+
 The bar is the default path's: identical trees wherever the oracle's decisive
 score gaps exceed 1e-4, scores within 1e-4 (fp32) or 2e-2 (bf16); seeds with
 smaller gaps must give a valid best-first tree within tolerance.  Sizes span
@@ -29,7 +35,7 @@ def with_head(wl, seed, d_H, rank, w1_scale=None, w2_scale=None, h_std=1.0):
     return wl
 
 
-def run_head(wl, name, **kw):
+def run_head(wl, name, trees=None, tol=None, **kw):
     print(f"[head] {name} batch={wl.batch} L={wl.L} V={wl.weights.V} M={wl.M} B={wl.B} "
           f"T={wl.T} d_H={wl.head.d_H} rank={wl.head.rank} kw={kw}", flush=True)
     dw = DeviceWorkload(wl, scorer=HEAD, **kw)
@@ -37,7 +43,8 @@ def run_head(wl, name, **kw):
         got = dw.run()
     finally:
         dw.close()
-    kinds = [compare_tree(wl, t, got, dw.kw) for t in range(wl.batch)]
+    trees = range(wl.batch) if trees is None else trees
+    kinds = [compare_tree(wl, t, got, dw.kw, tol=tol, name=name) for t in trees]
     print(f"[head] {name}: {[k for k, _ in kinds]} max score err {max(e for _, e in kinds):.2e}",
           flush=True)
     return kinds, got
@@ -45,18 +52,23 @@ def run_head(wl, name, **kw):
 
 CASES = [
     # (seed, batch, L, V, M, B, T, d_e, d_h, dtype, d_H, rank, kw, extra)
-    (31, 1, 4, 300, 8, 8, 0.0, 64, 32, synth.DT_F32, 64, 32, {}, {}),
-    (32, 3, 6, 500, 16, 24, 0.7, 64, 64, synth.DT_F32, 96, 64, {}, dict(h0=True)),
-    (33, 2, 5, 1000, 64, 16, 1.0, 128, 64, synth.DT_BF16, 128, 256, {}, {}),
+    # (G members per tree: d_h 32 -> 1, 64 -> 2, 96 -> 2; "fast": the expansion kernel)
+    (31, 1, 4, 300, 8, 8, 0.0, 64, 32, synth.DT_F32, 64, 32, {}, {}),                  # fast, G 1
+    (32, 3, 6, 500, 16, 24, 0.7, 64, 64, synth.DT_F32, 96, 64, {}, dict(h0=True)),     # fast, G 2
+    (33, 2, 5, 1000, 64, 16, 1.0, 128, 64, synth.DT_BF16, 128, 256, {}, {}),           # rank / G 128
     (34, 4, 3, 200, 12, 10, 1.5, 40, 32, synth.DT_F32, 40, 16, dict(max_children=3), dict(h0=True)),
-    (35, 2, 8, 700, 32, 16, 0.0, 96, 64, synth.DT_BF16, 64, 64, dict(norm_mode=1), {}),
-    (36, 1, 1, 100, 8, 6, 0.0, 32, 32, synth.DT_F32, 16, 8, {}, {}),
+    (35, 2, 8, 700, 32, 16, 0.0, 96, 64, synth.DT_BF16, 64, 64, dict(norm_mode=1), {}),  # fast
+    (36, 1, 1, 100, 8, 6, 0.0, 32, 32, synth.DT_F32, 16, 8, {}, {}),                   # rank 8
     (37, 3, 10, 2000, 64, 48, 0.8, 64, 64, synth.DT_BF16, 64, 128, dict(pos_offset=11), dict(h0=True)),
-    (38, 2, 6, 300, 8, 6, 0.0, 64, 32, synth.DT_F32, 32, 16, dict(max_children=1), {}),
-    (39, 2, 4, 30000, 64, 20, 0.9, 64, 96, synth.DT_F32, 200, 40, {}, dict(h0=True)),
+    (38, 2, 6, 300, 8, 6, 0.0, 64, 32, synth.DT_F32, 32, 16, dict(max_children=1), {}),  # fast
+    (39, 2, 4, 30000, 64, 20, 0.9, 64, 96, synth.DT_F32, 200, 40, {}, dict(h0=True)),  # rank 40
     (40, 1, 3, 700, 5, 33, 1.2, 48, 32, synth.DT_F32, 8, 1024, dict(max_children=4), {}),
     # 256 tree-depth rows at rank 256: the projection's 8-lane grid (enough workgroups)
     (46, 16, 16, 2000, 16, 8, 0.7, 64, 32, synth.DT_BF16, 64, 256, {}, dict(h0=True)),
+    # the expansion kernel past the one-workgroup kernel's limits: M = 96 (two
+    # MFMA row tiles per 64 slots and a ragged third), k (B + 1) above its heap
+    (49, 2, 5, 3000, 96, 40, 0.6, 64, 64, synth.DT_BF16, 64, 64, {}, dict(h0=True)),   # fast, M 96
+    (50, 1, 6, 800, 24, 256, 1.0, 64, 32, synth.DT_F32, 32, 32, {}, {}),              # fast, B 256
 ]
 
 
@@ -107,10 +119,32 @@ def test_head_nonfinite_row():
     assert int(got["n_nodes"][0]) == wl.B and int(got["n_nodes"][2]) == wl.B
 
 
-def test_head_qwen3_8b_shape():
+QWEN_TOL = 1e-4   # fp32 arithmetic on bf16 weights: only the summation order differs
+
+
+@pytest.mark.parametrize("k", [0, 8, 16], ids=["kM", "k8", "k16"])
+def test_head_qwen3_8b_shape(k):
+    # one tree: 16 members of 16 ranks each (d_H 4096, d_h 512, rank 256, V 151936)
     wl = with_head(synth.WORKLOADS["qwen3_8b"](), 43, 4096, 256, w2_scale=0.5)
-    kinds, _ = run_head(wl, "head-qwen3_8b")
+    kinds, _ = run_head(wl, f"head-qwen3_8b-k{k}", tol=QWEN_TOL, max_children=k)
     assert kinds[0][0] == "exact"
+
+
+@pytest.mark.parametrize("k", [0, 8], ids=["kM", "k8"])
+def test_head_deep_qwen_shape(k):
+    # a chain-like tree of depth 8 at the same shape
+    wl = with_head(synth.deep(), 47, 4096, 256, w2_scale=0.5)
+    kinds, got = run_head(wl, f"head-deep-k{k}", tol=QWEN_TOL, max_children=k)
+    assert kinds[0][0] == "exact"
+    assert int(got["depth"][0].max()) >= 8
+
+
+def test_head_deep_concurrent_sampled():
+    # 32 trees per call: 8 members of 32 ranks each
+    wl = with_head(synth.deep_concurrent(), 48, 4096, 256, w2_scale=0.5)
+    kinds, _ = run_head(wl, "head-deep_concurrent", trees=[0, 5, 9, 17, 26, 31], tol=QWEN_TOL,
+                        max_children=8)
+    assert sum(k == "exact" for k, _ in kinds) >= 4, kinds
 
 
 def test_head_argument_errors():
@@ -142,13 +176,14 @@ def test_head_argument_errors():
         assert st == -5  # workspace too small
     finally:
         dw.close()
-    # a plan of another scorer, and M beyond the head path's 64
-    for scorer, M in ((1, 8), (0, 96)):
+    # a plan of another scorer; M beyond the one-workgroup kernel's 64 at a rank
+    # the expansion kernel cannot split (8), and the same M at one it can (16)
+    for scorer, M, rank, want in ((1, 8, 16, -4), (0, 96, 8, -4), (0, 96, 16, 0)):
         wl2 = synth.random_small(45, batch=1, L=3, V=300, M=M, B=8, T=0.0, d_e=32, d_h=32)
         dw = DeviceWorkload(wl2, scorer=scorer)
         try:
-            hd = binding.dt_domino_head(w1.data_ptr(), w2.data_ptr(), 32, 16)
+            hd = binding.dt_domino_head(w1.data_ptr(), w2.data_ptr(), 32, rank)
             assert dw.plan._lib.dt_head_workspace_size(dw.plan.handle, 1, ctypes.byref(hd),
-                                                       ctypes.byref(n)) == -4
+                                                       ctypes.byref(n)) == want, (scorer, M, rank)
         finally:
             dw.close()
