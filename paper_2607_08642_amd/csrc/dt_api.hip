@@ -549,9 +549,6 @@ static dt_status head_check(const dt_plan *plan, int batch, const dt_domino_head
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return hip_fail(e, "device query");
-  if ((size_t)4 * 4 * hd->d_H > (size_t)maxlds)
-    return fail(DT_ERR_UNSUPPORTED, "the projection W_1^H H needs %d bytes of LDS, the device has %d",
-                16 * hd->d_H, maxlds);
   *G = head_fast_group(plan, batch, hd, maxlds);
   if (*G > 0) return DT_OK;
   // the one-workgroup head kernel
@@ -617,15 +614,15 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
   }
   hipEvent_t *ev = prof ? plan->ev + 4 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
   if (G > 0) {
-    // the scan (clearing the expansion's barrier counters), a_d = W_1^H H_d,
-    // then the default path's expansion kernel with Domino's head
+    // the scan (clearing the expansion's barrier counters; its extra
+    // workgroups compute a_d = W_1^H H_d), then the default path's expansion
+    // kernel with Domino's head
     const HeadFastWs hf = carve_head_fast(plan, batch, head->rank, G, static_cast<char *>(workspace));
     const int nbar = (batch + 2) * dt::kBarStride;
+    const dt::HeadProj hp = dt::head_proj_args(plan, batch * plan->L, H, *head, hf.a);
     hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hf.ws, hf.ws.bar, 2 * nbar, s,
-                                          prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
+                                          prof ? ev[0] : nullptr, prof ? ev[1] : nullptr, &hp);
     if (e != hipSuccess) return hip_fail(e, "scan launch");
-    e = dt::launch_head_proj(plan, batch, H, *head, hf.a, s);
-    if (e != hipSuccess) return hip_fail(e, "head projection launch");
     dt::HeadIn hin{head->w1, head->w2, hf.a, hf.hpart, head->rank, head->d_H};
     dt::ExpMode mode;
     mode.head = &hin;
@@ -640,8 +637,9 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
     return DT_OK;
   }
   const dt::HeadWorkspace hw = dt::carve_head(plan, batch, head->rank, static_cast<char *>(workspace));
+  const dt::HeadProj hp = dt::head_proj_args(plan, batch * plan->L, H, *head, hw.a);
   hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hw.scan, nullptr, 0, s,
-                                        prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
+                                        prof ? ev[0] : nullptr, prof ? ev[1] : nullptr, &hp);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
   e = dt::launch_head(plan, batch, H, *head, h0, inv_tau, hw, out, s, prof ? ev[2] : nullptr,
                       prof ? ev[3] : nullptr);

@@ -264,6 +264,24 @@ __device__ inline GruIn load_gru_in(const float *prow, const float *b_hh, int dh
   g.b = *reinterpret_cast<const float4 *>(b_hh + 2 * dh + j0);
   return g;
 }
+// four consecutive weights as stored (bf16: 8 bytes; fp32: 16 bytes), and widened
+template <typename TW>
+struct W4;
+template <>
+struct W4<uint16_t> {
+  using T = uint2;
+  static __device__ inline T load(const uint16_t *p) { return *reinterpret_cast<const uint2 *>(p); }
+  static __device__ inline float4 widen(T q) {
+    return make_float4(__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xFFFF0000u),
+                       __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xFFFF0000u));
+  }
+};
+template <>
+struct W4<float> {
+  using T = float4;
+  static __device__ inline T load(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+  static __device__ inline float4 widen(T q) { return q; }
+};
 // four consecutive weights widened to fp32 (bf16: 8 bytes; fp32: 16 bytes)
 __device__ inline float4 load4w(const uint16_t *p) {
   const uint2 q = *reinterpret_cast<const uint2 *>(p);
@@ -675,6 +693,12 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   typename Gates<TW>::Pre wpre;
   const bool wkeep = !a.nocorr && Gates<TW>::kPre > 0 && use_pin && gu >= 0 &&
                      gk1 - gk0 <= Gates<TW>::kPre;
+  // Domino's head: this wave's W_1^S fragments (rank tiles wave and wave + NW,
+  // k groups q < UW / 16) stay in registers for the whole launch when they fit
+  // (compile-time shapes only: elsewhere the registers are better spent)
+  constexpr int kW1T = 2, kW1Q = 2;
+  typename W4<TW>::T w1f[kW1T][kW1Q];
+  const bool w1keep = HEAD && SDH > 0 && a.rank / 16 <= kW1T * NW && UW / 16 <= kW1Q;
   int pb = 0;  // partial-buffer parity
   auto expand_chunk = [&](const int16_t *cn, int nc, int d) {
     // one batched round trip: the merged row of depth d (the children's
@@ -908,58 +932,91 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         dev_rsrc(a.part + (((size_t)t * 2 + pb) * G + member) * CH * MP);
     if constexpr (HEAD) {
       // Domino's head (section 2.3).  (a) this member's part of W_1^S S_c over
-      // its units, 16 ranks per MFMA tile, published for the other members
-      const __amdgpu_buffer_rsrc_t rhp =
-          dev_rsrc(a.hpart + (((size_t)t * 2 + pb) * G + member) * CH * a.rank);
-      for (int rt = wave; rt < a.rank / 16; rt += NW) {
-        const int r = rt * 16 + (lane & 15);
-        const int c = lane & 15, kq = (lane >> 4) * 4;
-        const TW *w1r = static_cast<const TW *>(a.w1) + (size_t)r * a.ld1 + a.d_H + member * UW;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int q = 0; q < nq; ++q) {
-          const float4 av = load4w(w1r + q * 16 + kq);
-          const float4 bv = *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+      // its units, 16 ranks per MFMA tile, published for the other members.
+      // The exchange is reader-major: [reader j][writer][node c][RJ ranks], so
+      // the parts member j sums are one contiguous block of blk floats
+      const int RJ = a.RJ, RJ4 = RJ / 4, blk = G * CH * RJ;
+      const size_t tp = ((size_t)t * 2 + pb) * G * blk;
+      const __amdgpu_buffer_rsrc_t rhp = dev_rsrc(a.hpart + tp + member * CH * RJ);
+      const int c = lane & 15, kq = (lane >> 4) * 4;
+      auto mma4 = [&](f32x4 acc, float4 av, float4 bv) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+      };
+      // lane l, register i of a tile: rank rt*16 + (l/16)*4 + i of node l%16
+      // (the four ranks of a lane share one reader: RJ % 16 == 0)
+      auto publish = [&](int rt, f32x4 acc) {
+        if (c < nc) {
+          const int r = rt * 16 + (lane >> 4) * 4, j = r / RJ;
+          st_dev16(rhp, (j * blk + c * RJ + r - j * RJ) * 4, make_float4(acc[0], acc[1], acc[2], acc[3]));
         }
-        // lane l, register i: rank rt*16 + (l/16)*4 + i of node l%16
-        if (c < nc)
-          st_dev16(rhp, (c * a.rank + rt * 16 + (lane >> 4) * 4) * 4,
-                   make_float4(acc[0], acc[1], acc[2], acc[3]));
+      };
+      if (w1keep) {
+#pragma unroll
+        for (int j = 0; j < kW1T; ++j) {
+          const int rt = wave + j * NW;
+          if (rt < a.rank / 16) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < kW1Q; ++q)
+              if (q < nq)
+                acc = mma4(acc, W4<TW>::widen(w1f[j][q]),
+                           *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq));
+            publish(rt, acc);
+          }
+        }
+      } else {
+        for (int rt = wave; rt < a.rank / 16; rt += NW) {
+          const TW *w1r = static_cast<const TW *>(a.w1) + (size_t)(rt * 16 + c) * a.ld1 + a.d_H + member * UW;
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+          for (int q = 0; q < nq; ++q)
+            acc = mma4(acc, load4w(w1r + q * 16 + kq),
+                       *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq));
+          publish(rt, acc);
+        }
       }
       group_barrier(ctr, G, nbar, &scal[S_STATUS], a.spin_limit);
       if (scal[S_STATUS] & DT_TREE_TIMEOUT) return;  // (uniform: read after the barrier)
       // (b) this member's rank slice of y = SiLU(a_d + W_1^S S) for the chunk's
-      // nodes: the G parts summed in member order
-      const int RJ = a.RJ, RJ4 = RJ / 4;
-      const __amdgpu_buffer_rsrc_t rha = dev_rsrc(a.hpart + ((size_t)t * 2 + pb) * G * CH * a.rank);
-      for (int e = tid; e < CH * RJ4; e += NT) {
-        const int c = e / RJ4, r4 = (e - c * RJ4) * 4;
-        float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int m2 = 0; m2 < G; ++m2)
-          sum += ld_dev16(rha, ((m2 * CH + c) * a.rank + member * RJ + r4) * 4);
-        const float x[4] = {has[r4] + sum.x, has[r4 + 1] + sum.y, has[r4 + 2] + sum.z,
-                            has[r4 + 3] + sum.w};
+      // nodes.  An item is (node c, 4 ranks); P lanes of one wave share an item,
+      // each summing every P-th member's part, then a butterfly over the P lanes
+      // (the same sum in every lane: deterministic).  Columns c >= nc of y are
+      // not read back: their MFMA outputs are dropped.
+      {
+        const int P = G < 8 ? G : 8;  // (G is a power of two)
+        const int sub = lane & (P - 1), nitem = nc * RJ4;
+        const __amdgpu_buffer_rsrc_t rha = dev_rsrc(a.hpart + tp + (size_t)member * blk);
+        for (int e0 = wave * (64 / P); e0 < nitem; e0 += NW * (64 / P)) {  // (wave-uniform)
+          const int e = e0 + lane / P;
+          float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (e < nitem)
+            for (int m2 = sub; m2 < G; m2 += P) sum += ld_dev16(rha, (m2 * CH * RJ + e * 4) * 4);
+          for (int o = 1; o < P; o <<= 1) {
+            sum.x += __shfl_xor(sum.x, o);
+            sum.y += __shfl_xor(sum.y, o);
+            sum.z += __shfl_xor(sum.z, o);
+            sum.w += __shfl_xor(sum.w, o);
+          }
+          if (e < nitem && sub == 0) {
+            const int cc = e / RJ4, r4 = (e - cc * RJ4) * 4;  // e * 4 = cc * RJ + r4
+            const float x[4] = {has[r4] + sum.x, has[r4 + 1] + sum.y, has[r4 + 2] + sum.z,
+                                has[r4 + 3] + sum.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) hys[c * RJ + r4 + i] = x[i] * sigmoid_fast(x[i]);
+            for (int i = 0; i < 4; ++i) hys[cc * RJ + r4 + i] = x[i] * sigmoid_fast(x[i]);
+          }
+        }
       }
       __syncthreads();
       // (c) this member's part of delta[c][m] = W_2[cand_m] . y over its rank slice
       for (int rt = wave; rt < RT; rt += NW) {
-        const int m = rt * 16 + (lane & 15);
-        const int c = lane & 15, kq = (lane >> 4) * 4;
-        const TW *w2row = reinterpret_cast<const TW *>(hw2) + m * RJ;  // slots >= M: unused
+        const TW *w2row = reinterpret_cast<const TW *>(hw2) + (rt * 16 + c) * RJ;  // slots >= M: unused
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int q = 0; q < RJ / 16; ++q) {
-          const float4 av = load4w(w2row + q * 16 + kq);
-          const float4 bv = *reinterpret_cast<const float4 *>(hys + c * RJ + q * 16 + kq);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
-        }
+        for (int q = 0; q < RJ / 16; ++q)
+          acc = mma4(acc, load4w(w2row + q * 16 + kq),
+                     *reinterpret_cast<const float4 *>(hys + c * RJ + q * 16 + kq));
+        // (lane l, register i: slot rt*16 + (l/16)*4 + i of node l%16)
         if (c < nc)
           st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
                    make_float4(acc[0], acc[1], acc[2], acc[3]));
@@ -1314,6 +1371,17 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   // without taking scores below vB, and vB only grows, so it can never be
   // popped.
   if (wkeep) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);  // in flight during the root step
+  if (w1keep) {
+    const TW *w1m = static_cast<const TW *>(a.w1) + a.d_H + member * UW + (lane >> 4) * 4;
+#pragma unroll
+    for (int j = 0; j < kW1T; ++j)
+#pragma unroll
+      for (int q = 0; q < kW1Q; ++q) {
+        const int rt = wave + j * NW;
+        if (rt < a.rank / 16 && q < UW / 16)
+          w1f[j][q] = W4<TW>::load(w1m + (size_t)(rt * 16 + (lane & 15)) * a.ld1 + q * 16);
+      }
+  }
   expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
   int nsteps = 1;
   for (;;) {

@@ -5,11 +5,10 @@
 // E[v] . (W_c S + b_c).  Scoring, normalisation, ties and emission are the
 // same as the default path's (Alg. 1; section 3.2 for the slice).
 //
-// Two kernels follow the top-M scan:
-//   head_proj_kernel  a[row][r] = W_1^H H_row, the half of W_1 [H_d; S] that
-//                     does not depend on the path (once per tree and depth);
-//   head_tree_kernel  one workgroup per tree: the exact row merge, then the
-//                     best-first heap of Alg. 1 in LDS, one pop at a time.
+// This file holds the tree kernel for shapes the expansion kernel does not
+// take: one workgroup per tree, the exact row merge, then the best-first heap
+// of Alg. 1 in LDS, one pop at a time.  a[row][r] = W_1^H H_row, the half of
+// W_1 [H_d; S] that does not depend on the path, comes from the scan launch.
 // A pop advances the popped node's GRU state from its parent's state and
 // W_hh S_parent (kept per popped node, computed the first time one of its
 // children is popped), forms y = SiLU(a_d + W_1^S S) and the slice's
@@ -22,10 +21,7 @@
 namespace dt {
 namespace {
 
-constexpr int kHT = 512;        // threads of both kernels
-constexpr int kProjRows = 4;    // H rows per projection workgroup
-// lanes per rank in the projection: 8, or 32 when the 8-lane grid would leave
-// most CUs idle (few tree-depth rows)
+constexpr int kHT = 512;        // threads of the tree kernel
 
 __device__ inline void load8(const float *p, float (&v)[8]) {
   const float4 a = *reinterpret_cast<const float4 *>(p);
@@ -111,67 +107,6 @@ __device__ void rows_dot(const T *W, size_t ld, int nrows, int n, const float *x
       const float v = sum8(acc[i]);
       if (sub == 0 && r0 + i < nrows) out[r0 + i] = v;
     }
-  }
-}
-
-// a[row][r] = sum_j W_1[r][j] H[row][j] over the H half (j < d_H)
-template <typename T, int kProjLanes>
-__global__ __launch_bounds__(kHT) void head_proj_kernel(const T *__restrict__ w1,
-                                                        const T *__restrict__ H,
-                                                        float *__restrict__ a, int rows, int d_H,
-                                                        int ld1, int rank) {
-  extern __shared__ __attribute__((aligned(16))) float hs[];  // [kProjRows][d_H]
-  const int row0 = blockIdx.x * kProjRows;
-  const int nr = rows - row0 < kProjRows ? rows - row0 : kProjRows;
-  // the block's H rows, eight elements (16 or 32 bytes) per thread and step
-  // (d_H % 8 == 0: a group of eight never crosses a row)
-#pragma unroll 4
-  for (int i = threadIdx.x; i < kProjRows * d_H / 8; i += kHT) {
-    const int q = (8 * i) / d_H, j = 8 * i - q * d_H;
-    float v[8];
-    if (q < nr) {
-      load8(H + (size_t)(row0 + q) * d_H + j, v);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.0f;
-    }
-    float4 *dst = reinterpret_cast<float4 *>(hs + 8 * i);
-    dst[0] = make_float4(v[0], v[1], v[2], v[3]);
-    dst[1] = make_float4(v[4], v[5], v[6], v[7]);
-  }
-  __syncthreads();
-  constexpr int kProjRanks = kHT / kProjLanes;  // ranks per workgroup
-  const int grp = threadIdx.x / kProjLanes, sub = threadIdx.x % kProjLanes;
-  const int r = blockIdx.y * kProjRanks + grp;
-  if (r >= rank) return;  // (whole groups; no barrier follows)
-  const T *wr = w1 + (size_t)r * ld1;
-  float acc[kProjRows];
-#pragma unroll
-  for (int q = 0; q < kProjRows; ++q) acc[q] = 0.0f;
-  // eight chunks per lane in flight per pass (out-of-range ones read column 0 and count zero)
-  constexpr int kPU = 8;
-  constexpr int kStep = 8 * kProjLanes;  // columns per chunk step of the group
-  for (int c0 = sub * 8; c0 < d_H; c0 += kStep * kPU) {
-    float w[kPU][8];
-#pragma unroll
-    for (int j = 0; j < kPU; ++j) load8(wr + (c0 + kStep * j < d_H ? c0 + kStep * j : 0), w[j]);
-#pragma unroll
-    for (int j = 0; j < kPU; ++j) {
-      const int c = c0 + kStep * j < d_H ? c0 + kStep * j : 0;
-      const bool ok = c0 + kStep * j < d_H;
-#pragma unroll
-      for (int q = 0; q < kProjRows; ++q) {
-        const float v = dot8(w[j], hs + q * d_H + c);
-        acc[q] += ok ? v : 0.0f;
-      }
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < kProjRows; ++q) {
-    float s = acc[q];
-#pragma unroll
-    for (int o = 1; o < kProjLanes; o <<= 1) s += __shfl_xor(s, o);  // within the aligned group
-    if (sub == 0 && q < nr) a[(size_t)(row0 + q) * rank + r] = s;
   }
 }
 
@@ -482,32 +417,11 @@ HeadWorkspace carve_head(const dt_plan *p, int batch, int rank, char *base) {
   return hw;
 }
 
-// a[row][r] = W_1^H H_row for the batch's tree-depth rows
-template <typename T>
-static hipError_t launch_proj_t(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
-                                float *a_out, hipStream_t s) {
-  const int rows = batch * p->L;
-  const size_t plds = (size_t)kProjRows * hd.d_H * sizeof(float);
-  const int rblocks = (rows + kProjRows - 1) / kProjRows;
-  const bool fine = (size_t)rblocks * ((hd.rank + kHT / 8 - 1) / (kHT / 8)) < (size_t)p->num_cus;
-  auto proj = fine ? &head_proj_kernel<T, 32> : &head_proj_kernel<T, 8>;
-  const int rpb = fine ? kHT / 32 : kHT / 8;  // ranks per workgroup
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(proj),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)plds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(proj, dim3(rblocks, (hd.rank + rpb - 1) / rpb), dim3(kHT), plds, s,
-                     static_cast<const T *>(hd.w1), static_cast<const T *>(H), a_out, rows, hd.d_H,
-                     hd.d_H + p->d_h, hd.rank);
-  return hipGetLastError();
-}
-
 template <typename T>
 static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
                                 const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
                                 hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
   const ScanGeom g = scan_geom(batch * p->L, p->V, p->M);
-  hipError_t e = launch_proj_t<T>(p, batch, H, hd, hw.a, s);
-  if (e != hipSuccess) return e;
   HeadArgs a;
   a.ckeys = hw.scan.chunk_keys;
   a.ctail = hw.scan.chunk_tail;
@@ -536,7 +450,7 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
   a.c2 = 1.4426950408889634f * inv_tau;
   a.out = *out;
   const size_t lds = head_lds_bytes(p->L, p->B, p->d_h, hd.rank);
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&head_tree_kernel<T>),
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&head_tree_kernel<T>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (t0)
@@ -544,12 +458,6 @@ static hipError_t launch_head_t(const dt_plan *p, int batch, const void *H, cons
   else
     hipLaunchKernelGGL(head_tree_kernel<T>, dim3(batch), dim3(kHT), lds, s, a);
   return hipGetLastError();
-}
-
-hipError_t launch_head_proj(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
-                            float *a_out, hipStream_t s) {
-  return p->wdt == DT_BF16 ? launch_proj_t<uint16_t>(p, batch, H, hd, a_out, s)
-                           : launch_proj_t<float>(p, batch, H, hd, a_out, s);
 }
 
 hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,

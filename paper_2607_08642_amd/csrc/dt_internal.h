@@ -142,11 +142,20 @@ size_t carve_scan(char *base, const ScanGeom &g, Workspace *ws);
 Workspace carve(const dt_plan *p, int batch, char *base);
 
 // kernel launchers (return hipError_t of the launch)
+// Domino's head: a[row][r] = W_1^H H_row over the launch's rows, computed by
+// `extra` more workgroups per row of the scan launch
+struct HeadProj {
+  const void *w1, *H;  // [rank][ld1], [rows][d_H] (weights dtype wdt)
+  float *a;            // [rows][rank]
+  int d_H, ld1, rank, wdt, extra;
+};
+HeadProj head_proj_args(const dt_plan *p, int rows, const void *H, const dt_domino_head &hd, float *a_out);
 // kernel launchers; with t0/t1 the launch records HIP events at the kernel's
 // start and end (hipExtLaunchKernel), used for stage timing
 hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
                               const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s,
-                              hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+                              hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
+                              const HeadProj *hp = nullptr);
 hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s);
 hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
 // Domino-head path (dt_build_tree_head): heap entries per tree, workspace, launch
@@ -164,9 +173,6 @@ size_t head_lds_bytes(int L, int B, int dh, int rank);
 hipError_t launch_head(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
                        const float *h0, float inv_tau, const HeadWorkspace &hw, dt_tree *out,
                        hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
-// a[row][r] = W_1^H H_row for the batch's L rows per tree (Domino's head)
-hipError_t launch_head_proj(const dt_plan *p, int batch, const void *H, const dt_domino_head &hd,
-                            float *a_out, hipStream_t s);
 // Domino's own head on the expansion kernel: its tensors for one launch
 struct HeadIn {
   const void *w1, *w2;  // [rank][d_H + d_h], [V][rank] (weights dtype)

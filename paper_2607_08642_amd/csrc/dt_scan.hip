@@ -28,8 +28,15 @@
 // The per-row merge of the segment lists (merge_row and its register
 // variants) runs inside the expansion kernel, or in a small kernel of its own
 // for dt_scan_topm.
+//
+// For Domino's own head the launch carries extra workgroups (blockIdx.x >=
+// nchunks) that compute a[row][r] = W_1^H H_row, the half of W_1 [H_d; S] that
+// does not depend on the path (section 2.3): a small GEMM of 16 x 16 MFMA
+// tiles whose memory time hides under the scan's.
 #include "dt_select.h"
 #include <hip/hip_ext.h>
+
+#include <type_traits>
 
 namespace dt {
 
@@ -38,6 +45,66 @@ namespace {
 using sel::Tail;
 
 constexpr int kWaves = kScanThreads / 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One 16-rank x 16-row tile of a = W_1^H H (tile = rank tile + (rank tiles) x
+// row tile) with fp32 accumulation: the K = d_H columns split over the waves
+// in chunks of KC (one MFMA group: lane l holds KC/4 consecutive columns of
+// rank (tile row) l % 16 and of H row l % 16, at column group l / 16), the
+// wave partials summed in LDS (red: kWaves x 256 floats).  Out-of-range ranks,
+// rows and columns read as zeros and are not stored.  bf16: 16x16x32 bf16
+// MFMAs on the stored values (exact products); fp32: 16x16x4 fp32 MFMAs.
+template <typename TW>
+__device__ void head_proj_tile(const HeadProj &p, int rows, int tile, float *red) {
+  const int nrt = (p.rank + 15) / 16;
+  if (tile >= nrt * ((rows + 15) / 16)) return;  // (whole workgroup)
+  const int rt = tile % nrt, qt = tile / nrt;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4;
+  const int r = rt * 16 + (lane & 15), q = qt * 16 + (lane & 15);
+  const bool rok = r < p.rank, qok = q < rows;
+  const TW *wr = static_cast<const TW *>(p.w1) + (size_t)(rok ? r : 0) * p.ld1;
+  const TW *hr = static_cast<const TW *>(p.H) + (size_t)(qok ? q : 0) * p.d_H;
+  constexpr bool kBf = sizeof(TW) == 2;
+  constexpr int KC = kBf ? 32 : 16, KL = KC / 4;  // columns per chunk, per lane
+  constexpr int U = 4;                             // chunks in flight per wave
+  using V = typename std::conditional<kBf, uint4, float4>::type;  // KL columns
+  const int nch = (p.d_H + KC - 1) / KC;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int c0 = w; c0 < nch; c0 += kWaves * U) {
+    V av[U], bv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = (c0 + u * kWaves) * KC + g * KL;  // (d_H % 8 == 0: a lane's KL are all in or out)
+      const bool ok = c0 + u * kWaves < nch && k < p.d_H;
+      av[u] = (ok && rok) ? *reinterpret_cast<const V *>(wr + k) : V{};
+      bv[u] = (ok && qok) ? *reinterpret_cast<const V *>(hr + k) : V{};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if constexpr (kBf) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av[u]),
+                                                     __builtin_bit_cast(bf16x8, bv[u]), acc, 0, 0, 0);
+      } else {
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].x, bv[u].x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].y, bv[u].y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].z, bv[u].z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].w, bv[u].w, acc, 0, 0, 0);
+      }
+    }
+  }
+  // lane l, register i: rank rt*16 + (l/16)*4 + i, row qt*16 + l%16
+#pragma unroll
+  for (int i = 0; i < 4; ++i) red[w * 256 + lane * 4 + i] = acc[i];
+  __syncthreads();
+  static_assert(kScanThreads == 256, "one thread per tile element");
+  const int e = threadIdx.x, el = e >> 2, ei = e & 3;
+  float sum = red[e];
+  for (int v = 1; v < kWaves; ++v) sum += red[v * 256 + e];
+  const int rr = rt * 16 + (el >> 4) * 4 + ei, qq = qt * 16 + (el & 15);
+  if (rr < p.rank && qq < rows) p.a[(size_t)qq * p.rank + rr] = sum;
+}
 
 constexpr int kRegion = kScanSortCap / kWaves;       // candidate keys per wave
 constexpr int kRegionCap = kRegion - kMaxM / kWaves;  // fill limit: the list fits beside them
@@ -238,11 +305,12 @@ __device__ inline float elem(const Raw<T> &r, int j, int e) {
 // largest value seen so far (never below them, so nothing overflows).
 // Also clears `zero_n` ints at `zero_ptr` (barrier counters of the expansion
 // kernel that follows on the stream).
-template <typename T, bool VEC>
+// TWP: the weights dtype of a head projection carried by the launch (void: none)
+template <typename T, bool VEC, typename TWP = void>
 __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     const T *__restrict__ logits, ScanGeom g, float c, uint64_t *__restrict__ ckeys,
     float2 *__restrict__ ctail, int32_t *__restrict__ cflag, int32_t *__restrict__ zero_ptr,
-    int zero_n) {
+    int zero_n, HeadProj hp) {
   constexpr int EPL = Elem<T>::EPL;
   constexpr int NL = Raw<T>::NL;
   constexpr int STEP = kScanThreads * EPL;
@@ -250,6 +318,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
   __shared__ ScanLDS sh;
   __shared__ uint64_t list[2][kMaxM];
   __shared__ float wthr[kWaves], wmax[kWaves];
+  if constexpr (!std::is_void<TWP>::value) {
+    if ((int)blockIdx.x >= g.nchunks) {
+      head_proj_tile<TWP>(hp, g.rows, blockIdx.y * hp.extra + blockIdx.x - g.nchunks,
+                          reinterpret_cast<float *>(sh.buf));
+      return;
+    }
+  }
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int row = blockIdx.y, seg = blockIdx.x;
   const int M = g.M;
@@ -677,28 +752,55 @@ static void launch_maybe_timed(F kernel, dim3 grid, dim3 block, uint32_t lds, hi
     hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
 }
 
+template <typename T, bool VEC>
+static void launch_scan_t(const T *p, const ScanGeom &g, float c, const Workspace &ws, int32_t *zero_ptr,
+                          int zero_n, const HeadProj *hp, hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
+  const dim3 block(kScanThreads);
+  if (!hp) {
+    launch_maybe_timed(scan_chunk_kernel<T, VEC>, dim3(g.nchunks, g.rows), block, 0, s, t0, t1, p, g, c,
+                       ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, HeadProj{});
+    return;
+  }
+  const dim3 grid(g.nchunks + hp->extra, g.rows);
+  if (hp->wdt == DT_BF16)
+    launch_maybe_timed(scan_chunk_kernel<T, VEC, uint16_t>, grid, block, 0, s, t0, t1, p, g, c, ws.chunk_keys,
+                       ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, *hp);
+  else
+    launch_maybe_timed(scan_chunk_kernel<T, VEC, float>, grid, block, 0, s, t0, t1, p, g, c, ws.chunk_keys,
+                       ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, *hp);
+}
+
+HeadProj head_proj_args(const dt_plan *p, int rows, const void *H, const dt_domino_head &hd, float *a_out) {
+  HeadProj h;
+  h.w1 = hd.w1;
+  h.H = H;
+  h.a = a_out;
+  h.d_H = hd.d_H;
+  h.ld1 = hd.d_H + p->d_h;
+  h.rank = hd.rank;
+  h.wdt = p->wdt;
+  const int tiles = ((hd.rank + 15) / 16) * ((rows + 15) / 16);
+  h.extra = (tiles + rows - 1) / rows;
+  return h;
+}
+
 hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, float inv_tau,
                               const Workspace &ws, int32_t *zero_ptr, int zero_n, hipStream_t s,
-                              hipEvent_t t0, hipEvent_t t1) {
+                              hipEvent_t t0, hipEvent_t t1, const HeadProj *hp) {
   const float c = 1.4426950408889634f * inv_tau;  // exp(x / tau) = exp2(x * c)
-  dim3 grid(g.nchunks, g.rows);
   const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16) == 0;
   if (ldt == DT_BF16) {
     const uint16_t *p = static_cast<const uint16_t *>(logits);
     if (aligned && g.V % 8 == 0)
-      launch_maybe_timed(scan_chunk_kernel<uint16_t, true>, grid, dim3(kScanThreads), 0, s, t0, t1, p, g,
-                         c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
+      launch_scan_t<uint16_t, true>(p, g, c, ws, zero_ptr, zero_n, hp, s, t0, t1);
     else
-      launch_maybe_timed(scan_chunk_kernel<uint16_t, false>, grid, dim3(kScanThreads), 0, s, t0, t1, p,
-                         g, c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
+      launch_scan_t<uint16_t, false>(p, g, c, ws, zero_ptr, zero_n, hp, s, t0, t1);
   } else {
     const float *p = static_cast<const float *>(logits);
     if (aligned && g.V % 4 == 0)
-      launch_maybe_timed(scan_chunk_kernel<float, true>, grid, dim3(kScanThreads), 0, s, t0, t1, p, g, c,
-                         ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
+      launch_scan_t<float, true>(p, g, c, ws, zero_ptr, zero_n, hp, s, t0, t1);
     else
-      launch_maybe_timed(scan_chunk_kernel<float, false>, grid, dim3(kScanThreads), 0, s, t0, t1, p, g,
-                         c, ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n);
+      launch_scan_t<float, false>(p, g, c, ws, zero_ptr, zero_n, hp, s, t0, t1);
   }
   return hipGetLastError();
 }
