@@ -672,6 +672,329 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wave-streaming variant (M <= 64, rows read with 16-byte loads): the same
+// segments, batches and per-element work, but each wave keeps its own list of
+// its 64 best keys in registers (lane p: position p, descending) and merges
+// its own candidates into it when they gather -- no block barrier while the
+// segment streams, so a wave that merges does not hold up the other waves'
+// loads.  A candidate must beat a lower bound on the segment's M-th key:
+//   * the first batch's bound tb (as above; the one block barrier), ties kept;
+//   * the wave's own list's M-th value, strictly: the wave's later elements
+//     have larger indices, so they lose ties with its own list;
+//   * any other wave's published M-th value (LDS; only ever rises), ties
+//     kept: that wave's keys may have larger indices;
+//   * once every wave has published, the least of the four lists' q-th values
+//     (q = ceil(M/4): at least M keys lie at or above it), ties kept.
+// A wave merges whenever a few dozen candidates have gathered, so that these
+// bounds rise early.  The region holds (index, value bits) pairs; the keys
+// are formed in the merge.
+// The four wave lists meet once, at the end of the segment.  A wave whose
+// candidates overflow its region re-reads the batch and merges as it goes;
+// a first batch without a finite bound (mostly -inf or padding) takes every
+// element in range as a candidate that way.
+// bf16 rows keep two batches per wave in flight: the batch being processed in
+// registers and the next two in LDS, filled by buffer-to-LDS loads (two slots
+// of 5 KB per wave; three workgroups per CU); fp32 rows use two register
+// buffers.
+// ---------------------------------------------------------------------------
+template <typename T>
+struct WaveScan {
+  static constexpr bool kDma = sizeof(T) == 2;
+  static constexpr int kRegion = kDma ? 256 : 512;  // candidate keys a wave gathers between merges
+  static constexpr int kSlot = 64 * Raw<T>::NL * 16;  // bytes of one wave's batch
+};
+
+// merge region[0..n) ((index << 32) | value bits each) into the wave's list
+// (descending keys, one per lane); keys that fall out of the best 64 join the
+// lane's tail
+__device__ inline void wave_merge(const uint64_t *region, int n, uint64_t &list, Tail &tail, float c) {
+  const int lane = threadIdx.x & 63;
+  for (int c0 = 0; c0 < n; c0 += 64) {
+    uint64_t k = 0ull;
+    if (c0 + lane < n) {
+      const uint64_t e = region[c0 + lane];
+      k = make_key(__uint_as_float((uint32_t)e), (uint32_t)(e >> 32));
+    }
+    list = sel::merge_halves(list, sel::wave_sort64(k, false), true, tail, c);
+  }
+}
+
+__device__ inline uint64_t readlane64(uint64_t v, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// a value slightly below v (v finite): comparing x > below(v) keeps x == v
+__device__ inline float below(float v) { return v - (fabsf(v) * 0x1p-20f + 0x1p-126f); }
+
+template <typename T, typename TWP = void>
+__global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
+    const T *__restrict__ logits, ScanGeom g, float c, uint64_t *__restrict__ ckeys,
+    float2 *__restrict__ ctail, int32_t *__restrict__ cflag, int32_t *__restrict__ zero_ptr,
+    int zero_n, HeadProj hp) {
+  constexpr int EPL = Elem<T>::EPL;
+  constexpr int NL = Raw<T>::NL;
+  constexpr int STEP = kScanThreads * EPL;
+  constexpr float NINF = -__builtin_huge_valf();
+  constexpr bool kDma = WaveScan<T>::kDma;
+  constexpr int kWaveRegion = WaveScan<T>::kRegion, kSlot = WaveScan<T>::kSlot;
+  __shared__ alignas(16) uint64_t regions[kWaves * kWaveRegion];
+  __shared__ alignas(16) char slots[kDma ? kWaves * 2 * kSlot : 16];
+  __shared__ uint64_t wl[kWaves][64];
+  __shared__ float wthr[kWaves], wmax[kWaves], pub[kWaves], pubq[kWaves];
+  __shared__ float2 red[kWaves];
+  __shared__ int flag;
+  static_assert(kWaves * kWaveRegion * 8 >= kWaves * 256 * 4, "projection partials fit the regions");
+  if constexpr (!std::is_void<TWP>::value) {
+    if ((int)blockIdx.x >= g.nchunks) {
+      head_proj_tile<TWP>(hp, g.rows, blockIdx.y * hp.extra + blockIdx.x - g.nchunks,
+                          reinterpret_cast<float *>(regions));
+      return;
+    }
+  }
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int row = blockIdx.y, seg = blockIdx.x;
+  const int M = g.M;
+  const int seg_start = seg * g.chunk;
+  const int seg_n = min(g.chunk, g.V - seg_start);
+  const int nbat = (seg_n + kScanChunk - 1) / kScanChunk;
+  const T *rowp = logits + (size_t)row * g.V + seg_start;
+  if (zero_ptr && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = tid; i < zero_n; i += kScanThreads) zero_ptr[i] = 0;
+  const __amdgpu_buffer_rsrc_t segr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T *>(rowp), 0, seg_n * (int)sizeof(T), 0x00020000);
+  // loads past the segment's end return zeros (no traffic); pad_batch makes them -inf
+  int lb = tid * EPL;
+  asm volatile("" : "+v"(lb));
+  // batch b of this wave into LDS slot sl (nothing waits for it here)
+  auto dma = [&](int b, int sl) {
+    char *dst = slots + (w * 2 + sl) * kSlot;
+    const int base = (b * kScanChunk + lb) * (int)sizeof(T);
+#pragma unroll
+    for (int j = 0; j < NL; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(segr, (__attribute__((address_space(3))) void *)(dst + j * 1024),
+                                               16, base + j * STEP * (int)sizeof(T), 0, 0, 0);
+  };
+  Raw<T> ra, rb;
+  load_batch_vec<T>(ra, segr, 0);
+  if constexpr (!kDma) load_batch_vec<T>(rb, segr, 1);
+  if (tid == 0) flag = 0;
+  if (lane == 0) {
+    pub[w] = NINF;
+    pubq[w] = NINF;
+  }
+
+  // ---- the first batch's lower bound tb (every wave: the ceil(M/4)-th largest
+  // of its lane maxima; the minimum over the waves) and its maximum
+  {
+    const int bn0 = min(kScanChunk, seg_n);
+    if (bn0 < kScanChunk) pad_batch<T>(ra, bn0);
+  }
+  float tmax = NINF;
+#pragma unroll
+  for (int j = 0; j < NL; ++j)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) tmax = fmaxf(tmax, elem<T>(ra, j, e));
+  {
+    const int q = (M + kWaves - 1) / kWaves;
+    const uint32_t code = ordered_bits(tmax);
+    uint32_t pre = 0;
+#pragma unroll
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t cand = pre | (1u << bit);
+      if (__popcll(__ballot(code >= cand)) >= q) pre = cand;
+    }
+    const float wm = sel::wave_reduce(tmax, [](float x, float y) { return fmaxf(x, y); });
+    if (lane == 0) {
+      wthr[w] = ordered_to_float(pre);
+      wmax[w] = wm;
+    }
+  }
+  __syncthreads();
+  // (issued after the barrier, which would wait for them)
+  if constexpr (kDma) {
+    dma(1, 1);
+    dma(2, 0);
+  }
+  float tb = wthr[0], mx = wmax[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) {
+    tb = fminf(tb, wthr[i]);
+    mx = fmaxf(mx, wmax[i]);
+  }
+  const bool all_in = !(tb > NINF);
+  const float tlow = all_in ? NINF : below(tb);
+  Tail tail = sel::tail_empty();
+  tail.m = fmaxf(mx, -3.402823466e38f);
+
+  uint64_t list = 0ull;   // this wave's best keys (0: empty)
+  float v_own = NINF;     // its M-th value once it holds M keys
+  int wpos = 0;           // candidates in the region (wave-uniform)
+  const int kMergeTrig = M < 16 ? 2 * M : 32;
+  uint64_t *region = regions + w * kWaveRegion;
+
+  const int q = (M + kWaves - 1) / kWaves;
+  auto after_merge = [&]() {
+    // (plain LDS accesses: atomic ones would wait for the slots' loads first)
+    const uint64_t kq = readlane64(list, q - 1);
+    if (kq && lane == 0) pubq[w] = key_value(kq);
+    const uint64_t km = readlane64(list, M - 1);
+    if (km) {
+      v_own = key_value(km);
+      if (lane == 0) pub[w] = v_own;
+    }
+  };
+  auto merge_now = [&]() {
+    wave_merge(region, wpos, list, tail, c);
+    wpos = 0;
+    after_merge();
+  };
+  // the candidates of batch b read again from memory, merged whenever the
+  // region might overflow (the tail already holds the batch's other elements)
+  auto slow = [&](int bstart, int bn, float te, bool in_all) {
+#pragma unroll 1
+    for (int k = 0; k < NL * EPL; ++k) {
+      const int off = lb + (k / EPL) * STEP + k % EPL;
+      const float x = off < bn ? to_f32<T>(rowp[bstart + off]) : NINF;
+      const bool pass = off < bn && (x > te || (in_all && x == NINF));
+      if (in_all && off < bn && x != x) tail.s = x;  // (a NaN: the row is flagged)
+      const uint64_t bal = __ballot(pass);
+      if (bal) {
+        if (wpos + 64 > kWaveRegion) merge_now();
+        const int at = wpos + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+        if (pass)
+          region[at] = ((uint64_t)(uint32_t)(seg_start + bstart + off) << 32) | __float_as_uint(x);
+        wpos += __popcll(bal);
+      }
+    }
+  };
+
+  auto process = [&](Raw<T> &raw, int b) {
+    const int bstart = b * kScanChunk;
+    const int bn = min(kScanChunk, seg_n - bstart);
+    if (b > 0 && bn < kScanChunk) pad_batch<T>(raw, bn);
+    // this batch's bound
+    float te = tlow;
+    if (b > 0) {
+      te = fmaxf(te, v_own);
+      float vo = NINF, vq = __builtin_huge_valf();
+      asm volatile("" ::: "memory");  // read the other waves' values afresh
+#pragma unroll
+      for (int i = 0; i < kWaves; ++i) {
+        if (i != w) vo = fmaxf(vo, pub[i]);
+        vq = fminf(vq, pubq[i]);
+      }
+      if (vo > NINF) te = fmaxf(te, below(vo));
+      if (vq > NINF) te = fmaxf(te, below(vq));
+    }
+    // every element that cannot enter is <= te: keep the tail's reference above it
+    if (te > tail.m) {
+      tail.s *= sel::fast_exp2((tail.m - te) * c);
+      tail.m = te;
+    }
+    if (b == 0 && all_in) {
+      slow(bstart, bn, NINF, true);
+    } else {
+      fence_regs<T>(raw);
+      const int wprev = wpos;
+      const int ibase = seg_start + bstart + lb;  // row index of this thread's element (0, 0)
+      // exp((x - m) / tau) = 2^((x - m) c) for every element; a candidate (x >
+      // te, rare) is appended to the region and adds nothing
+      auto tail_pass = [&](auto expo) {
+        float s = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NL; ++j)
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) {
+            float x = elem<T>(raw, j, e);
+            const bool pass = x > te;
+            const uint64_t bal = __ballot(pass);
+            if (__builtin_expect(bal != 0, 0)) {
+              // (past the region's end the last slot is overwritten: the
+              // overflow below discards this batch's entries)
+              const int at = min(wpos + (int)__builtin_amdgcn_mbcnt_hi(
+                                            (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0)),
+                                 kWaveRegion - 1);
+              if (pass)
+                region[at] = ((uint64_t)(uint32_t)(ibase + j * STEP + e) << 32) | __float_as_uint(x);
+              wpos += __popcll(bal);
+              x = pass ? NINF : x;
+            }
+            s += sel::fast_exp2(expo(x));
+          }
+        tail.s += s;
+      };
+      const float m = tail.m, mc = m * c;
+      if (fabsf(mc) <= 128.0f)
+        tail_pass([=](float x) { return __builtin_fmaf(x, c, -mc); });
+      else
+        tail_pass([=](float x) { return (x - m) * c; });
+      if (wpos > kWaveRegion) {
+        // overflow: merge what came before, then this batch's candidates again
+        wpos = wprev;
+        if (wpos) merge_now();
+        slow(bstart, bn, te, false);
+      }
+    }
+    if (wpos >= kMergeTrig || (wpos && b == nbat - 1)) merge_now();
+  };
+
+  if constexpr (kDma) {
+    // batch b + 1 sits in slot (b + 1) & 1, batch b + 2 in the other slot (its
+    // five loads the only ones issued after it): wait for it alone, move it
+    // to the registers, refill its slot with batch b + 3.  Loads past the end
+    // are issued too (zeros, no traffic) so that the count never changes.
+    for (int b = 0; b < nbat; ++b) {
+      process(ra, b);
+      if (b + 1 < nbat) {
+        __builtin_amdgcn_s_waitcnt(0xF70 | NL);  // vmcnt(NL): all but the last NL loads
+        const char *src = slots + (w * 2 + ((b + 1) & 1)) * kSlot;
+#pragma unroll
+        for (int j = 0; j < NL; ++j) ra.q[j] = *reinterpret_cast<const uint4 *>(src + j * 1024 + lane * 16);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the slot is read
+        dma(b + 3, (b + 1) & 1);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // no load may land in LDS after the workgroup
+  } else {
+    for (int b = 0; b < nbat; b += 2) {
+      process(ra, b);
+      if (b + 2 < nbat) load_batch_vec<T>(ra, segr, b + 2);
+      if (b + 1 < nbat) {
+        process(rb, b + 1);
+        if (b + 3 < nbat) load_batch_vec<T>(rb, segr, b + 3);
+      }
+    }
+  }
+
+  // ---- the four wave lists meet: the segment's M best, the rest to the tail
+  wl[w][lane] = list;
+  __syncthreads();
+  const size_t cidx = (size_t)row * g.nchunks + seg;
+  if (w == 0) {
+    const uint64_t a = sel::merge_halves(wl[0][lane], wl[1][63 - lane], true, tail, c);
+    const uint64_t b2 = sel::merge_halves(wl[2][lane], wl[3][63 - lane], false, tail, c);
+    uint64_t f = sel::merge_halves(a, b2, true, tail, c);
+    if (lane >= M) {
+      if (f) sel::tail_add1(tail, key_value(f), c);
+      f = 0ull;
+    }
+    if (lane < M) ckeys[cidx * M + lane] = f;
+    // +inf heads the list
+    if (lane == 0 && f && key_value(f) == __builtin_huge_valf()) atomicOr(&flag, 1);
+  }
+  // a NaN makes a tail sum NaN (it never passes a comparison)
+  if (!(tail.s == tail.s)) atomicOr(&flag, 1);
+  const Tail t = sel::block_tail<kScanThreads>(tail, c, red);
+  if (tid == 0) {
+    ctail[cidx] = make_float2(t.m, t.s);
+    cflag[cidx] = flag ? DT_TREE_NONFINITE : 0;
+  }
+}
+
 // K2 (dt_scan_topm only): merge the chunk lists of one row
 __global__ __launch_bounds__(kScanThreads) void scan_merge_kernel(
     ScanGeom g, float c, float inv_tau, const uint64_t *__restrict__ ckeys,
@@ -695,13 +1018,15 @@ ScanGeom scan_geom(int rows, int V, int M) {
   g.rows = rows;
   g.V = V;
   g.M = M;
-  // segments of sb batches: enough workgroups to fill the device about four
-  // deep, the rest of the work amortised inside each segment
+  // segments of sb batches: the fewest rounds of kScanSlots resident
+  // workgroups (each round pays a workgroup's start-up latency once; within a
+  // round the scan streams at the memory's rate whatever the split), then the
+  // shortest segments that keep it (the most workgroups in flight)
   const int nb = (V + kScanChunk - 1) / kScanChunk;
-  long long total = (long long)rows * nb;
-  int sb = (int)((total + kScanTargetGroups - 1) / kScanTargetGroups);
-  sb = sb < 1 ? 1 : (sb > kScanMaxBatches ? kScanMaxBatches : sb);
-  if (sb > nb) sb = nb;
+  auto rounds = [&](int t) { return ((long long)rows * ((nb + t - 1) / t) + kScanSlots - 1) / kScanSlots; };
+  const long long fewest = rounds(nb);
+  int sb = 1;
+  while (sb < nb && rounds(sb) > fewest) ++sb;
   g.chunk = sb * kScanChunk;
   g.nchunks = (V + g.chunk - 1) / g.chunk;
   return g;
@@ -756,6 +1081,22 @@ template <typename T, bool VEC>
 static void launch_scan_t(const T *p, const ScanGeom &g, float c, const Workspace &ws, int32_t *zero_ptr,
                           int zero_n, const HeadProj *hp, hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
   const dim3 block(kScanThreads);
+  if (VEC && g.M <= 64) {
+    // the wave-streaming kernel
+    if (!hp) {
+      launch_maybe_timed(scan_wave_kernel<T>, dim3(g.nchunks, g.rows), block, 0, s, t0, t1, p, g, c,
+                         ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, HeadProj{});
+      return;
+    }
+    const dim3 grid(g.nchunks + hp->extra, g.rows);
+    if (hp->wdt == DT_BF16)
+      launch_maybe_timed(scan_wave_kernel<T, uint16_t>, grid, block, 0, s, t0, t1, p, g, c, ws.chunk_keys,
+                         ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, *hp);
+    else
+      launch_maybe_timed(scan_wave_kernel<T, float>, grid, block, 0, s, t0, t1, p, g, c, ws.chunk_keys,
+                         ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, *hp);
+    return;
+  }
   if (!hp) {
     launch_maybe_timed(scan_chunk_kernel<T, VEC>, dim3(g.nchunks, g.rows), block, 0, s, t0, t1, p, g, c,
                        ws.chunk_keys, ws.chunk_tail, ws.chunk_flag, zero_ptr, zero_n, HeadProj{});

@@ -93,9 +93,13 @@ def test_scan_descending_rows_worst_case():
 
 def test_scan_nonfinite_flags():
     rng = np.random.default_rng(9)
-    x = rng.standard_normal((4, 3000)).astype(np.float32)
+    x = rng.standard_normal((5, 3000)).astype(np.float32)
     x[1, 17] = np.nan
     x[2, 2999] = np.inf
+    # a first batch without a finite lower bound, holding a NaN
+    x[3, :] = -np.inf
+    x[3, 5] = np.nan
+    x[3, 2500] = 1.0
     _check(x, synth.DT_F32, 8, 0.0, case="nonfinite")
 
 
@@ -117,11 +121,15 @@ def _mixed_rows(n_rows, V, seed):
     return x
 
 
+@pytest.mark.parametrize("V", [20480 + 37, 20480 + 40], ids=["unaligned", "aligned"])
 @pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16])
-def test_scan_streaming_segments(dtype):
+def test_scan_streaming_segments(dtype, V):
     # enough rows that every workgroup streams several batches of a segment
-    # against its running list (ramps overflow the candidate regions)
-    x = _mixed_rows(1100, 20480 + 37, 21)
+    # against its running lists (ramps and constant rows overflow the candidate
+    # regions; -inf blocks leave first batches without a finite bound).  Rows of
+    # 16-byte loads take the wave-streaming kernel at M <= 64, the others the
+    # block kernel.
+    x = _mixed_rows(1100, V, 21)
     if dtype == synth.DT_BF16:
         x = synth.f32_to_bf16_bits(x)
     rows = list(range(0, 14)) + list(range(500, 507)) + [1099]
