@@ -23,7 +23,7 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPerThread = 40;                         // elements held per thread
 constexpr int kScanChunk = kScanThreads * kScanPerThread;  // 10240
 constexpr int kScanSortCap = 4096;   // bitonic sort buffer (keys) per workgroup
-constexpr int kScanSlots = 768;     // scan workgroups resident at once (3 per CU of 256)
+constexpr int kScanSlots = 1024;    // scan workgroups resident at once (4 per CU of 256)
 constexpr int kScanFlushAt = 256;    // fallback: flush the candidate buffer beyond this
 constexpr int kMergeLdsMax = 96 * 1024;  // row merge buffer (sel::merge_buf_bytes) at most
 
