@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 2
+#define DT_ABI_VERSION 3
 
 typedef enum { DT_F32 = 0, DT_BF16 = 1 } dt_dtype;
 
@@ -157,21 +157,44 @@ const char *dt_status_string(int status);
 /* Thread-local detail of the last error returned on this host thread. */
 const char *dt_last_error(void);
 
-/* Create a plan for one model and one (L, M, B) shape.
- * The plan folds the embedding table through the GRU input projection and the
- * correction head for every token (W_ih E[v] + b_ih, W_c^T E[v], E[v] . b_c),
- * held in fp32: V * (4 d_h + 1) * 4 bytes of plan-owned device memory
- * (1.24 GB for Qwen3's vocabulary at d_h = 512).
+/* A drafter's model-level tables, shared by every plan made from it: the
+ * embedding table folded through the GRU input projection and the correction
+ * head for every token (W_ih E[v] + b_ih, W_c^T E[v], E[v] . b_c; section 2.3's
+ * encoder input and head, precomputed per token as the candidate gather of
+ * section 3.2 reads them), held in fp32, V * (4 d_h + 1) * 4 bytes of device
+ * memory (1.24 GB for Qwen3's vocabulary at d_h = 512), and the repacked GRU.
  *   emb:  [V, d_e] token-embedding table (caller-owned; only read while the
- *         plan is created);
+ *         model is created);
  *   gru, head: the Domino encoder and correction head (copied and repacked
- *         into plan-owned device memory; the caller may free them afterwards);
- *   weights_dtype: dtype of emb, GRU and head tensors;
+ *         into library-owned device memory; the caller may free them afterwards);
+ *   weights_dtype: dtype of emb, GRU and head tensors.
+ * The tables live on the device current at creation.  Runs packing kernels on
+ * the default stream and waits for them.  On success *model is set; on
+ * failure *model is NULL. */
+typedef struct dt_model dt_model;
+dt_status dt_model_create(dt_model **model, const void *emb, int V, int d_e, const dt_gru *gru,
+                          const dt_head *head, int weights_dtype);
+
+/* Release the caller's reference to the model (NULL is ignored).  Each plan
+ * made from it holds a reference of its own: the tables are freed when the
+ * model and all of its plans are destroyed, in any order. */
+void dt_model_destroy(dt_model *model);
+
+/* Create a plan for one (L, M, B) shape of a model: nothing is folded or
+ * copied (a few small buffers are allocated later, for profiling and the
+ * adaptive budget).  Plans of one model with different shapes, options or
+ * batch limits share its tables.  The model's device must be current
+ * (DT_ERR_SHAPE otherwise).
  *   logits_dtype: dtype of the marginal logits passed to dt_build_tree;
  *   max_batch: the largest batch dt_build_tree will be called with;
  *   opts: NULL for defaults.
- * Runs packing kernels on the default stream and waits for them.  On success
- * *plan is set; on failure *plan is NULL. */
+ * On success *plan is set; on failure *plan is NULL. */
+dt_status dt_plan_create_from_model(dt_plan **plan, dt_model *model, int L, int M, int B,
+                                    int logits_dtype, int max_batch, const dt_options *opts);
+
+/* Create a plan together with a model of its own (dt_model_create followed by
+ * dt_plan_create_from_model; the plan holds the model's only reference, so
+ * dt_plan_destroy frees its tables).  Arguments as for those two calls. */
 dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const dt_gru *gru,
                          const dt_head *head, int weights_dtype, int L, int M, int B,
                          int logits_dtype, int max_batch, const dt_options *opts);
@@ -212,7 +235,8 @@ dt_status dt_build_tree(dt_plan *plan, const void *marginal_logits, int batch, c
 dt_status dt_build_tree_noalloc(dt_plan *plan, const void *marginal_logits, int batch,
                                 const float *h0, float T, dt_tree *out, void *stream);
 
-/* Release the plan's device memory (NULL is ignored). */
+/* Release the plan's device memory and its reference to the model (NULL is
+ * ignored). */
 void dt_plan_destroy(dt_plan *plan);
 
 /* Stage timing (measurement aid).  With every = n > 0, every n-th dt_build_tree

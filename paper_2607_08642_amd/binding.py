@@ -25,7 +25,7 @@ DT_SCORER_STATIC = 2
 DT_TREE_NONFINITE = 0x1
 DT_TREE_TRUNCATED = 0x2
 DT_TREE_TIMEOUT = 0x4
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 STATUS = {0: "DT_OK", -1: "DT_ERR_NULL", -2: "DT_ERR_SHAPE", -3: "DT_ERR_DTYPE",
           -4: "DT_ERR_UNSUPPORTED", -5: "DT_ERR_WORKSPACE", -6: "DT_ERR_ALIGN", -7: "DT_ERR_HIP"}
@@ -35,7 +35,8 @@ EXPORTS = ("dt_abi_version", "dt_status_string", "dt_last_error", "dt_plan_creat
            "dt_workspace_size", "dt_build_tree", "dt_plan_destroy", "dt_plan_set_profiling",
            "dt_plan_stage_ms", "dt_scan_workspace_size", "dt_scan_topm", "dt_head_workspace_size",
            "dt_build_tree_head", "dt_build_tree_noalloc",
-           "dt_plan_expand_stats", "dt_plan_set_adaptive_budget")
+           "dt_plan_expand_stats", "dt_plan_set_adaptive_budget", "dt_model_create",
+           "dt_model_destroy", "dt_plan_create_from_model")
 STAGES = ("scan", "expand")
 
 
@@ -92,6 +93,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dt_plan_create.argtypes = [ctypes.POINTER(vp), vp, ci, ci, ctypes.POINTER(dt_gru),
                                    ctypes.POINTER(dt_head), ci, ci, ci, ci, ci, ci,
                                    ctypes.POINTER(dt_options)]
+    lib.dt_model_create.restype = ci
+    lib.dt_model_create.argtypes = [ctypes.POINTER(vp), vp, ci, ci, ctypes.POINTER(dt_gru),
+                                    ctypes.POINTER(dt_head), ci]
+    lib.dt_model_destroy.restype = None
+    lib.dt_model_destroy.argtypes = [vp]
+    lib.dt_plan_create_from_model.restype = ci
+    lib.dt_plan_create_from_model.argtypes = [ctypes.POINTER(vp), vp, ci, ci, ci, ci, ci,
+                                              ctypes.POINTER(dt_options)]
     lib.dt_workspace_size.restype = ci
     lib.dt_workspace_size.argtypes = [vp, ci, ctypes.POINTER(sz)]
     lib.dt_build_tree.restype = ci
@@ -180,11 +189,43 @@ class Tree:
         return c
 
 
+class Model:
+    """dt_model: a drafter's vocabulary tables (embedding table folded through
+    the GRU input projection and the correction head) and repacked GRU, shared
+    by every Plan made from it.  The weight tensors may be freed once it exists.
+    """
+
+    def __init__(self, emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c):
+        lib = load()
+        self._lib = lib
+        self.V, self.d_e = emb.shape
+        self.d_h = w_hh.shape[1]
+        self.device = emb.device
+        gru = dt_gru(_ptr(w_ih), _ptr(w_hh), _ptr(b_ih), _ptr(b_hh), self.d_e, self.d_h)
+        head = dt_head(_ptr(w_c), _ptr(b_c))
+        h = ctypes.c_void_p()
+        _check(lib.dt_model_create(ctypes.byref(h), _ptr(emb), self.V, self.d_e, ctypes.byref(gru),
+                                   ctypes.byref(head), _dtype_code(emb)))
+        self.handle = h
+
+    def close(self) -> None:
+        """Drop this reference (the tables live on while a plan uses them)."""
+        if getattr(self, "handle", None):
+            self._lib.dt_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 class Plan:
     """dt_plan: one model (embedding table, GRU, head) and one (L, M, B) shape.
 
-    The embedding tensor must outlive the plan; the GRU and head weights are
-    packed into plan-owned memory.
+    Plan(emb, w_ih, ...) builds a model of its own (dt_plan_create);
+    Plan.from_model(model, ...) shares an existing Model's tables.
     """
 
     def __init__(self, emb, w_ih, w_hh, b_ih, b_hh, w_c, b_c, *, L: int, M: int, B: int,
@@ -194,9 +235,9 @@ class Plan:
                  debug_spin_limit: int = 0):
         lib = load()
         self._lib = lib
-        self.emb = emb
         self.V, self.d_e = emb.shape
         self.d_h = w_hh.shape[1]
+        self.device = emb.device
         self.L, self.M, self.B, self.max_batch = L, M, B, max_batch
         self.logits_dtype = logits_dtype
         wdt = _dtype_code(emb)
@@ -211,6 +252,26 @@ class Plan:
         self.handle = h
         self._ws = {}
 
+    @classmethod
+    def from_model(cls, model: Model, *, L: int, M: int, B: int, logits_dtype: int,
+                   max_batch: int = 1, max_children: int = 0, norm_mode: int = DT_NORM_TAIL,
+                   pos_offset: int = 0, scorer: int = DT_SCORER_COND, frontier_width: int = 0,
+                   debug_spin_limit: int = 0) -> "Plan":
+        """dt_plan_create_from_model: a plan over `model`'s tables."""
+        self = cls.__new__(cls)
+        self._lib = model._lib
+        self.V, self.d_e, self.d_h, self.device = model.V, model.d_e, model.d_h, model.device
+        self.L, self.M, self.B, self.max_batch = L, M, B, max_batch
+        self.logits_dtype = logits_dtype
+        opts = dt_options(max_children, norm_mode, pos_offset, scorer, frontier_width,
+                          debug_spin_limit)
+        h = ctypes.c_void_p()
+        _check(self._lib.dt_plan_create_from_model(ctypes.byref(h), model.handle, L, M, B,
+                                                   logits_dtype, max_batch, ctypes.byref(opts)))
+        self.handle = h
+        self._ws = {}
+        return self
+
     def workspace_size(self, batch: int) -> int:
         n = ctypes.c_size_t()
         _check(self._lib.dt_workspace_size(self.handle, batch, ctypes.byref(n)))
@@ -220,7 +281,7 @@ class Plan:
         import torch
         if batch not in self._ws:
             self._ws[batch] = torch.empty(self.workspace_size(batch), dtype=torch.uint8,
-                                          device=self.emb.device)
+                                          device=self.device)
         return self._ws[batch]
 
     def build_tree(self, logits, T: float, h0=None, out: Optional[Tree] = None,

@@ -116,39 +116,113 @@ const char *dt_status_string(int s) {
 
 const char *dt_last_error(void) { return g_last_error.c_str(); }
 
-dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const dt_gru *gru,
-                         const dt_head *head, int weights_dtype, int L, int M, int B,
-                         int logits_dtype, int max_batch, const dt_options *opts) {
-  if (!plan) return fail(DT_ERR_NULL, "plan out-pointer is NULL");
-  *plan = nullptr;
+// the options (NULL: defaults) checked into *o
+static dt_status check_options(const dt_options *opts, dt_options *o) {
+  *o = dt_options{0, DT_NORM_TAIL, 0, 0, 0, 0};
+  if (opts) *o = *opts;
+  if (o->max_children < 0) return fail(DT_ERR_SHAPE, "max_children must be >= 0");
+  if (o->frontier_width < 0 || o->debug_spin_limit < 0)
+    return fail(DT_ERR_SHAPE, "frontier_width and debug_spin_limit must be >= 0");
+  if (o->norm_mode != DT_NORM_TAIL && o->norm_mode != DT_NORM_SLICE)
+    return fail(DT_ERR_UNSUPPORTED, "norm_mode must be DT_NORM_TAIL or DT_NORM_SLICE");
+  if (o->scorer != DT_SCORER_COND && o->scorer != DT_SCORER_MARG && o->scorer != DT_SCORER_STATIC)
+    return fail(DT_ERR_UNSUPPORTED, "scorer must be DT_SCORER_COND, DT_SCORER_MARG or DT_SCORER_STATIC");
+  return DT_OK;
+}
+
+// drop one reference; the last one frees the tables
+static void model_release(dt_model *m) {
+  if (!m || m->refs.fetch_sub(1) != 1) return;
+  if (m->wfold) (void)hipFree(m->wfold);
+  if (m->b_ih) (void)hipFree(m->b_ih);
+  if (m->b_hh) (void)hipFree(m->b_hh);
+  if (m->b_c) (void)hipFree(m->b_c);
+  if (m->whh_t) (void)hipFree(m->whh_t);
+  if (m->whh_rm) (void)hipFree(m->whh_rm);
+  if (m->P_all) (void)hipFree(m->P_all);
+  if (m->U_all) (void)hipFree(m->U_all);
+  if (m->c_all) (void)hipFree(m->c_all);
+  delete m;
+}
+
+dt_status dt_model_create(dt_model **model, const void *emb, int V, int d_e, const dt_gru *gru,
+                          const dt_head *head, int weights_dtype) {
+  if (!model) return fail(DT_ERR_NULL, "model out-pointer is NULL");
+  *model = nullptr;
   if (!emb || !gru || !head) return fail(DT_ERR_NULL, "emb, gru and head are required");
   if (!gru->w_ih || !gru->w_hh || !head->w) return fail(DT_ERR_NULL, "w_ih, w_hh and head.w are required");
-  if (!valid_dtype(weights_dtype) || !valid_dtype(logits_dtype))
-    return fail(DT_ERR_DTYPE, "dtype codes must be DT_F32 or DT_BF16");
-  if (V < 1 || d_e < 1 || L < 1 || M < 1 || B < 1 || max_batch < 1)
-    return fail(DT_ERR_SHAPE, "sizes must be positive (V=%d d_e=%d L=%d M=%d B=%d max_batch=%d)", V,
-                d_e, L, M, B, max_batch);
+  if (!valid_dtype(weights_dtype)) return fail(DT_ERR_DTYPE, "dtype codes must be DT_F32 or DT_BF16");
+  if (V < 1 || d_e < 1) return fail(DT_ERR_SHAPE, "sizes must be positive (V=%d d_e=%d)", V, d_e);
   if (gru->d_in != d_e) return fail(DT_ERR_SHAPE, "gru.d_in (%d) must equal d_e (%d)", gru->d_in, d_e);
   const int d_h = gru->d_h;
-  if (M > V) return fail(DT_ERR_SHAPE, "M (%d) exceeds V (%d)", M, V);
-  if (M > dt::kMaxM || B > dt::kMaxB || L > dt::kMaxL || d_e > dt::kMaxDe || d_h < 32 ||
-      d_h > dt::kMaxDh || d_h % 32 != 0)
-    return fail(DT_ERR_UNSUPPORTED,
-                "outside the envelope (M<=256, B<=256, L<=64, d_e<=8192, 32<=d_h<=1024, d_h%%32==0)");
-  dt_options o = {0, DT_NORM_TAIL, 0, 0, 0, 0};
-  if (opts) o = *opts;
-  if (o.max_children < 0) return fail(DT_ERR_SHAPE, "max_children must be >= 0");
-  if (o.frontier_width < 0 || o.debug_spin_limit < 0)
-    return fail(DT_ERR_SHAPE, "frontier_width and debug_spin_limit must be >= 0");
-  if (o.norm_mode != DT_NORM_TAIL && o.norm_mode != DT_NORM_SLICE)
-    return fail(DT_ERR_UNSUPPORTED, "norm_mode must be DT_NORM_TAIL or DT_NORM_SLICE");
-  if (o.scorer != DT_SCORER_COND && o.scorer != DT_SCORER_MARG && o.scorer != DT_SCORER_STATIC)
-    return fail(DT_ERR_UNSUPPORTED, "scorer must be DT_SCORER_COND, DT_SCORER_MARG or DT_SCORER_STATIC");
+  if (d_e > dt::kMaxDe || d_h < 32 || d_h > dt::kMaxDh || d_h % 32 != 0)
+    return fail(DT_ERR_UNSUPPORTED, "outside the envelope (d_e<=8192, 32<=d_h<=1024, d_h%%32==0)");
   const size_t ws = dsize(weights_dtype);
   if (!aligned(emb, 16) || !aligned(gru->w_ih, ws) || !aligned(gru->w_hh, ws) ||
       !aligned(head->w, ws) || (gru->b_ih && !aligned(gru->b_ih, ws)) ||
       (gru->b_hh && !aligned(gru->b_hh, ws)) || (head->b && !aligned(head->b, ws)))
     return fail(DT_ERR_ALIGN, "emb must be 16-byte aligned, weights naturally aligned");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  dt_model *m = new (std::nothrow) dt_model();
+  if (!m) return fail(DT_ERR_HIP, "host allocation failed");
+  m->refs.store(1);
+  m->V = V;
+  m->d_e = d_e;
+  m->d_h = d_h;
+  m->wdt = weights_dtype;
+  m->emb = emb;
+  m->nf = 4 * d_h;
+  m->nf_pad = (m->nf + dt::kFoldBN - 1) / dt::kFoldBN * dt::kFoldBN;
+  m->has_bc = head->b != nullptr;
+  m->device = dev;
+  e = hipMalloc(&m->wfold, (size_t)m->nf_pad * d_e * ws);
+  if (e == hipSuccess) e = hipMalloc(&m->b_ih, sizeof(float) * 3 * d_h);
+  if (e == hipSuccess) e = hipMalloc(&m->b_hh, sizeof(float) * 3 * d_h);
+  if (e == hipSuccess) e = hipMalloc(&m->b_c, sizeof(float) * d_e);
+  if (e == hipSuccess) e = hipMalloc(&m->whh_t, (size_t)3 * d_h * d_h * ws);
+  if (e == hipSuccess) e = hipMalloc(&m->whh_rm, (size_t)3 * d_h * d_h * ws);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(m->whh_rm, gru->w_hh, (size_t)3 * d_h * d_h * ws, hipMemcpyDeviceToDevice,
+                       nullptr);
+  if (e == hipSuccess) e = hipMalloc(&m->P_all, (size_t)V * 3 * d_h * sizeof(float));
+  if (e == hipSuccess) e = hipMalloc(&m->U_all, (size_t)V * d_h * sizeof(float));
+  if (e == hipSuccess) e = hipMalloc(&m->c_all, (size_t)V * sizeof(float));
+  if (e == hipSuccess) e = dt::pack_weights(m, gru, head, nullptr);
+  if (e == hipSuccess) e = dt::fold_vocab(m, nullptr);
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  if (e == hipSuccess) {
+    e = hipFree(m->wfold);
+    m->wfold = nullptr;
+  }
+  m->emb = nullptr;  // (only read while the tables are built)
+  if (e != hipSuccess) {
+    dt_status st = hip_fail(e, "model creation");
+    model_release(m);
+    return st;
+  }
+  *model = m;
+  return DT_OK;
+}
+
+void dt_model_destroy(dt_model *model) { model_release(model); }
+
+dt_status dt_plan_create_from_model(dt_plan **plan, dt_model *model, int L, int M, int B,
+                                    int logits_dtype, int max_batch, const dt_options *opts) {
+  if (!plan) return fail(DT_ERR_NULL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  if (!model) return fail(DT_ERR_NULL, "model is required");
+  if (!valid_dtype(logits_dtype)) return fail(DT_ERR_DTYPE, "dtype codes must be DT_F32 or DT_BF16");
+  const int V = model->V, d_h = model->d_h;
+  if (L < 1 || M < 1 || B < 1 || max_batch < 1)
+    return fail(DT_ERR_SHAPE, "sizes must be positive (L=%d M=%d B=%d max_batch=%d)", L, M, B, max_batch);
+  if (M > V) return fail(DT_ERR_SHAPE, "M (%d) exceeds V (%d)", M, V);
+  if (M > dt::kMaxM || B > dt::kMaxB || L > dt::kMaxL)
+    return fail(DT_ERR_UNSUPPORTED, "outside the envelope (M<=256, B<=256, L<=64)");
+  dt_options o;
+  const dt_status ost = check_options(opts, &o);
+  if (ost != DT_OK) return ost;
   int dev = 0, ncu = 0, maxlds = 0, nxcd = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
@@ -156,6 +230,8 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&maxlds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return hip_fail(e, "device query");
+  if (dev != model->device)
+    return fail(DT_ERR_SHAPE, "the model lives on device %d, the current device is %d", model->device, dev);
   if (nxcd < 1 || nxcd > dt::kMaxXcd)
     return fail(DT_ERR_UNSUPPORTED, "device reports %d XCDs; 1 to %d are supported", nxcd, dt::kMaxXcd);
   const int nchunks = dt::scan_geom(1, V, M).nchunks;
@@ -173,12 +249,25 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
     return fail(DT_ERR_UNSUPPORTED,
                 "expansion needs %zu bytes of LDS (d_h=%d, M=%d, max_batch=%d), device has %d",
                 lds_need, d_h, M, max_batch, maxlds);
+  void *scratch_ptr = nullptr;
+  e = scratch_address(dev, &scratch_ptr);  // once per device: dt_build_tree_noalloc's workspace
+  if (e != hipSuccess) return hip_fail(e, "scratch address");
 
   dt_plan *p = new (std::nothrow) dt_plan();
   if (!p) return fail(DT_ERR_HIP, "host allocation failed");
+  model->refs.fetch_add(1);
+  p->model = model;
   p->V = V;
-  p->d_e = d_e;
+  p->d_e = model->d_e;
   p->d_h = d_h;
+  p->wdt = model->wdt;
+  p->P_all = model->P_all;
+  p->U_all = model->U_all;
+  p->c_all = model->c_all;
+  p->b_ih = model->b_ih;
+  p->b_hh = model->b_hh;
+  p->whh_t = model->whh_t;
+  p->whh_rm = model->whh_rm;
   p->L = L;
   p->M = M;
   p->B = B;
@@ -189,50 +278,38 @@ dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const 
   p->norm_mode = o.norm_mode;
   p->scorer = o.scorer;
   p->pos_offset = o.pos_offset;
-  p->wdt = weights_dtype;
   p->ldt = logits_dtype;
   p->max_batch = max_batch;
-  p->emb = emb;
-  p->nf = 4 * d_h;
-  p->nf_pad = (p->nf + dt::kFoldBN - 1) / dt::kFoldBN * dt::kFoldBN;
-  p->has_bc = head->b != nullptr;
   p->num_cus = ncu;
   p->num_xcd = nxcd;
   p->frontier_w = o.frontier_width;
   p->spin_limit = o.debug_spin_limit;
   p->device = dev;
-  void *scratch_ptr = nullptr;
-  e = scratch_address(dev, &scratch_ptr);  // once per device: dt_build_tree_noalloc's workspace
-  if (e != hipSuccess) {
-    delete p;
-    return hip_fail(e, "scratch address");
-  }
-  e = hipMalloc(&p->wfold, (size_t)p->nf_pad * d_e * ws);
-  if (e == hipSuccess) e = hipMalloc(&p->b_ih, sizeof(float) * 3 * d_h);
-  if (e == hipSuccess) e = hipMalloc(&p->b_hh, sizeof(float) * 3 * d_h);
-  if (e == hipSuccess) e = hipMalloc(&p->b_c, sizeof(float) * d_e);
-  if (e == hipSuccess) e = hipMalloc(&p->whh_t, (size_t)3 * d_h * d_h * ws);
-  if (e == hipSuccess) e = hipMalloc(&p->whh_rm, (size_t)3 * d_h * d_h * ws);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(p->whh_rm, gru->w_hh, (size_t)3 * d_h * d_h * ws, hipMemcpyDeviceToDevice,
-                       nullptr);
-  if (e == hipSuccess) e = hipMalloc(&p->P_all, (size_t)V * 3 * d_h * sizeof(float));
-  if (e == hipSuccess) e = hipMalloc(&p->U_all, (size_t)V * d_h * sizeof(float));
-  if (e == hipSuccess) e = hipMalloc(&p->c_all, (size_t)V * sizeof(float));
-  if (e == hipSuccess) e = dt::pack_weights(p, gru, head, nullptr);
-  if (e == hipSuccess) e = dt::fold_vocab(p, nullptr);
-  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
-  if (e == hipSuccess) {
-    e = hipFree(p->wfold);
-    p->wfold = nullptr;
-  }
-  if (e != hipSuccess) {
-    dt_status st = hip_fail(e, "plan creation");
-    dt_plan_destroy(p);
-    return st;
-  }
   *plan = p;
   return DT_OK;
+}
+
+dt_status dt_plan_create(dt_plan **plan, const void *emb, int V, int d_e, const dt_gru *gru,
+                         const dt_head *head, int weights_dtype, int L, int M, int B,
+                         int logits_dtype, int max_batch, const dt_options *opts) {
+  if (!plan) return fail(DT_ERR_NULL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  // the plain shape checks come before the (large) tables are built
+  if (!valid_dtype(logits_dtype)) return fail(DT_ERR_DTYPE, "dtype codes must be DT_F32 or DT_BF16");
+  if (L < 1 || M < 1 || B < 1 || max_batch < 1)
+    return fail(DT_ERR_SHAPE, "sizes must be positive (L=%d M=%d B=%d max_batch=%d)", L, M, B, max_batch);
+  if (V >= 1 && M > V) return fail(DT_ERR_SHAPE, "M (%d) exceeds V (%d)", M, V);
+  if (M > dt::kMaxM || B > dt::kMaxB || L > dt::kMaxL)
+    return fail(DT_ERR_UNSUPPORTED, "outside the envelope (M<=256, B<=256, L<=64)");
+  dt_options o;
+  const dt_status ost = check_options(opts, &o);
+  if (ost != DT_OK) return ost;
+  dt_model *m = nullptr;
+  dt_status st = dt_model_create(&m, emb, V, d_e, gru, head, weights_dtype);
+  if (st != DT_OK) return st;
+  st = dt_plan_create_from_model(plan, m, L, M, B, logits_dtype, max_batch, opts);
+  model_release(m);  // the plan holds the only reference now (or none: freed)
+  return st;
 }
 
 dt_status dt_plan_set_profiling(dt_plan *p, int enable) {
@@ -333,15 +410,7 @@ void dt_plan_destroy(dt_plan *p) {
       if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
     delete[] p->ev;
   }
-  if (p->wfold) (void)hipFree(p->wfold);
-  if (p->b_ih) (void)hipFree(p->b_ih);
-  if (p->b_hh) (void)hipFree(p->b_hh);
-  if (p->b_c) (void)hipFree(p->b_c);
-  if (p->whh_t) (void)hipFree(p->whh_t);
-  if (p->whh_rm) (void)hipFree(p->whh_rm);
-  if (p->P_all) (void)hipFree(p->P_all);
-  if (p->U_all) (void)hipFree(p->U_all);
-  if (p->c_all) (void)hipFree(p->c_all);
+  model_release(p->model);
   delete p;
 }
 

@@ -267,7 +267,7 @@ inline int grid_for(size_t n) {
 
 }  // namespace
 
-hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s) {
+hipError_t pack_weights(dt_model *p, const dt_gru *gru, const dt_head *head, hipStream_t s) {
   const int d_e = p->d_e, d_h = p->d_h;
   const size_t wfold_n = (size_t)p->nf_pad * d_e;
   if (p->wdt == DT_BF16) {
@@ -299,7 +299,7 @@ hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipS
   return hipGetLastError();
 }
 
-hipError_t fold_vocab(const dt_plan *p, hipStream_t s) {
+hipError_t fold_vocab(const dt_model *p, hipStream_t s) {
   const int rows_total = p->V;
   const float *bc = p->b_c;  // zeros when the head has no bias
   if (p->wdt == DT_BF16 && p->d_e % 8 == 0) {

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "dominotree.h"
 
 namespace dt {
@@ -78,12 +80,14 @@ struct ScanGeom {
 
 }  // namespace dt
 
-struct dt_plan {
-  int V, d_e, d_h, L, M, B, k, norm_mode, pos_offset, scorer;
-  int wdt, ldt, max_batch;
+// The model-level tables: the vocabulary folded through the GRU input
+// projection and the correction head, and the repacked weights.  Shared by
+// every plan created from the model; freed with the last reference.
+struct dt_model {
+  int V, d_e, d_h, wdt;
   const void *emb;
   void *wfold;      // [nf_pad, d_e] (weights dtype): rows [0,3dh) = W_ih, [3dh,4dh) = W_c^T;
-                    // only alive while the plan is created
+                    // only alive while the model is created
   float *P_all;     // [V][3dh]  W_ih E[v] + b_ih + (b_hh on gates r, z)
   float *U_all;     // [V][dh]   W_c^T E[v]
   float *c_all;     // [V]       E[v] . b_c
@@ -94,6 +98,16 @@ struct dt_plan {
   int has_bc;
   void *whh_t;      // W_hh in MFMA A-fragment order (see pack_whh_*_kernel)
   void *whh_rm;     // [3dh][dh] W_hh as given (weights dtype), for the Domino-head path
+  int device;       // the device its memory lives on
+  std::atomic<int> refs;  // the creator's reference plus one per plan
+};
+
+struct dt_plan {
+  int V, d_e, d_h, L, M, B, k, norm_mode, pos_offset, scorer;
+  int wdt, ldt, max_batch;
+  dt_model *model;  // the tables below are the model's (one reference held)
+  const float *P_all, *U_all, *c_all, *b_ih, *b_hh;
+  const void *whh_t, *whh_rm;
   int num_cus;
   int num_xcd;              // XCDs of the device (workgroups are dealt to them round-robin)
   int frontier_w;           // dt_options.frontier_width (0: the heap builder)
@@ -156,7 +170,7 @@ hipError_t launch_scan_chunks(const void *logits, int ldt, const ScanGeom &g, fl
                               hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
                               const HeadProj *hp = nullptr);
 hipError_t launch_scan_merge(const ScanGeom &g, float inv_tau, const Workspace &ws, hipStream_t s);
-hipError_t fold_vocab(const dt_plan *p, hipStream_t s);
+hipError_t fold_vocab(const dt_model *m, hipStream_t s);
 // Domino-head path (dt_build_tree_head): heap entries per tree, workspace, launch
 constexpr int kHeadCap = 4096;
 struct HeadWorkspace {
@@ -201,6 +215,6 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
 int expand_group_size(int d_h, int num_cus, int num_xcd, int batch);
 size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L, int rj = 0, int wbytes = 0);
 size_t expand_part_bytes(const dt_plan *p, int batch);
-hipError_t pack_weights(dt_plan *p, const dt_gru *gru, const dt_head *head, hipStream_t s);
+hipError_t pack_weights(dt_model *m, const dt_gru *gru, const dt_head *head, hipStream_t s);
 
 }  // namespace dt

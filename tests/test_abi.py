@@ -49,6 +49,16 @@ def test_null_arguments_rejected_on_host():
     assert L.dt_workspace_size(None, 1, None) == -1
     assert L.dt_build_tree(None, None, 1, None, 0.0, None, 0, None, None) == -1
     L.dt_plan_destroy(None)
+    # the model and the plan made from one
+    m = ctypes.c_void_p(1)
+    assert L.dt_model_create(None, None, 1, 1, None, None, 0) == -1
+    assert L.dt_model_create(ctypes.byref(m), None, 1, 1, None, None, 0) == -1
+    assert m.value is None
+    h = ctypes.c_void_p(1)
+    assert L.dt_plan_create_from_model(ctypes.byref(h), None, 4, 8, 8, 0, 1, None) == -1
+    assert h.value is None and b"model" in L.dt_last_error()
+    assert L.dt_plan_create_from_model(None, None, 4, 8, 8, 0, 1, None) == -1
+    L.dt_model_destroy(None)
 
 
 def test_bad_shapes_and_dtypes_rejected_on_host():
@@ -80,6 +90,13 @@ def test_bad_shapes_and_dtypes_rejected_on_host():
     assert L.dt_plan_create(ctypes.byref(h), 18, 100, 64, ctypes.byref(gru), ctypes.byref(head),
                             0, 4, 8, 8, 0, 1, None) == -6
     assert h.value is None
+    # the same checks on the model alone
+    m = ctypes.c_void_p()
+    assert L.dt_model_create(ctypes.byref(m), 16, 100, 64, ctypes.byref(gru), ctypes.byref(head), 7) == -3
+    assert L.dt_model_create(ctypes.byref(m), 16, 100, 64, ctypes.byref(gru2), ctypes.byref(head), 0) == -2
+    assert L.dt_model_create(ctypes.byref(m), 16, 100, 64, ctypes.byref(gru3), ctypes.byref(head), 0) == -4
+    assert L.dt_model_create(ctypes.byref(m), 18, 100, 64, ctypes.byref(gru), ctypes.byref(head), 0) == -6
+    assert m.value is None
 
 
 def test_scan_workspace_query_and_checks():
