@@ -681,13 +681,15 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 // loads.  A candidate must beat a lower bound on the segment's M-th key:
 //   * the first batch's bound tb (as above; the one block barrier), ties kept;
 //   * the wave's own list's M-th value, strictly: the wave's later elements
-//     have larger indices, so they lose ties with its own list;
-//   * any other wave's published M-th value (LDS; only ever rises), ties
-//     kept: that wave's keys may have larger indices;
-//   * once every wave has published, the least of the four lists' q-th values
-//     (q = ceil(M/4): at least M keys lie at or above it), ties kept.
-// A wave merges whenever a few dozen candidates have gathered, so that these
-// bounds rise early.  The region holds (index, value bits) pairs; the keys
+//     have larger indices, so they lose ties with its own list.
+// Both depend on nothing but the data, so the candidates, the merges and the
+// order of every tail sum are the same from run to run.  (Reading the other
+// waves' list values as they stood was faster -- 40.2 against 43.3 us on 512
+// rows of 151936 bf16 logits -- but made the candidates, and with them the
+// tails' rounding, depend on timing; reading them two batches late, waiting
+// for them, gained nothing over the own bound.)
+// A wave merges whenever a few dozen candidates have gathered, so that its
+// bound rises early.  The region holds (index, value bits) pairs; the keys
 // are formed in the merge.
 // The four wave lists meet once, at the end of the segment.  A wave whose
 // candidates overflow its region re-reads the batch and merges as it goes;
@@ -695,7 +697,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 // element in range as a candidate that way.
 // Each wave keeps its next batch in flight in registers (two buffers; a third,
 // two batches ahead, measured slower: 43.2 against 40.0 us on 512 rows of
-// 151936 bf16 logits), four workgroups per CU.
+// 151936 bf16 logits, with the bounds shared), four workgroups per CU.
 // ---------------------------------------------------------------------------
 template <typename T>
 struct WaveScan {
@@ -740,7 +742,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   constexpr int kWaveRegion = WaveScan<T>::kRegion;
   __shared__ alignas(16) uint64_t regions[kWaves * kWaveRegion];
   __shared__ uint64_t wl[kWaves][64];
-  __shared__ float wthr[kWaves], wmax[kWaves], pub[kWaves], pubq[kWaves];
+  __shared__ float wthr[kWaves], wmax[kWaves];
   __shared__ float2 red[kWaves];
   __shared__ int flag;
   static_assert(kWaves * kWaveRegion * 8 >= kWaves * 256 * 4, "projection partials fit the regions");
@@ -768,10 +770,6 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   Raw<T> ra, rb, rc;
   load_batch_vec<T>(ra, segr, 0);
   if (tid == 0) flag = 0;
-  if (lane == 0) {
-    pub[w] = NINF;
-    pubq[w] = NINF;
-  }
 
   // ---- the first batch's lower bound tb (every wave: the ceil(M/4)-th largest
   // of its lane maxima; the minimum over the waves) and its maximum
@@ -820,16 +818,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   const int kMergeTrig = M < 16 ? 2 * M : 32;
   uint64_t *region = regions + w * kWaveRegion;
 
-  const int q = (M + kWaves - 1) / kWaves;
   auto after_merge = [&]() {
-    // (plain LDS accesses without a fence: a stale value is only a weaker bound)
-    const uint64_t kq = readlane64(list, q - 1);
-    if (kq && lane == 0) pubq[w] = key_value(kq);
     const uint64_t km = readlane64(list, M - 1);
-    if (km) {
-      v_own = key_value(km);
-      if (lane == 0) pub[w] = v_own;
-    }
+    if (km) v_own = key_value(km);
   };
   auto merge_now = [&]() {
     wave_merge(region, wpos, list, tail, c);
@@ -863,18 +854,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
     if (b > 0 && bn < kScanChunk) pad_batch<T>(raw, bn);
     // this batch's bound
     float te = tlow;
-    if (b > 0) {
-      te = fmaxf(te, v_own);
-      float vo = NINF, vq = __builtin_huge_valf();
-      asm volatile("" ::: "memory");  // read the other waves' values afresh
-#pragma unroll
-      for (int i = 0; i < kWaves; ++i) {
-        if (i != w) vo = fmaxf(vo, pub[i]);
-        vq = fminf(vq, pubq[i]);
-      }
-      if (vo > NINF) te = fmaxf(te, below(vo));
-      if (vq > NINF) te = fmaxf(te, below(vq));
-    }
+    if (b > 0) te = fmaxf(te, v_own);
     // every element that cannot enter is <= te: keep the tail's reference above it
     if (te > tail.m) {
       tail.s *= sel::fast_exp2((tail.m - te) * c);

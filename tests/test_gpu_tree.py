@@ -383,3 +383,37 @@ def test_graph_replay_matches_eager():
         del g
     finally:
         dw.close()
+
+
+def test_repeatable_under_concurrent_load():
+    # 32 trees per call (every scan wave streaming several batches): the same
+    # bits whether the calls run alone or beside heavy copies on another stream,
+    # which shifts the waves' relative timing -- the scan's bounds, candidates
+    # and tail sums must not depend on it
+    wl = qwen("concurrent")
+    dw = DeviceWorkload(wl)
+    src = torch.empty(2**28 // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    side = torch.cuda.Stream()
+    try:
+        first = dw.run()
+        for rep in range(3):
+            with torch.cuda.stream(side):
+                for _ in range(4):
+                    dst.copy_(src)
+            again = dw.run()
+            side.synchronize()
+            for k in first:
+                np.testing.assert_array_equal(first[k], again[k], err_msg=f"rep {rep}: {k}")
+        ids, vals, tail, flags = binding.scan_topm(dw.logits.view(-1, wl.weights.V), wl.M, wl.T)
+        torch.cuda.synchronize()
+        t0 = tail.cpu().numpy()
+        for rep in range(3):
+            with torch.cuda.stream(side):
+                for _ in range(4):
+                    dst.copy_(src)
+            _, _, tail2, _ = binding.scan_topm(dw.logits.view(-1, wl.weights.V), wl.M, wl.T)
+            side.synchronize()
+            np.testing.assert_array_equal(t0, tail2.cpu().numpy(), err_msg=f"scan rep {rep}")
+    finally:
+        dw.close()
