@@ -90,8 +90,13 @@ struct ExpArgs {
 };
 
 // LDS carve (byte offsets), identical on host and device
+// Scores kept beside the candidate lists (elist, elist2): the list's first
+// kCsCap entries.  After an expansion step the list holds the old candidates
+// and then the step's new children, whose scores are ranked in place.
+constexpr int kCsCap = 512;
+
 struct Lds {
-  int ng, ntok, nparent, nstate, nslot, ndepth, nrank, nexp, newidx, elist, elist2;
+  int ng, ntok, nparent, nstate, nslot, ndepth, nrank, nexp, newidx, elist, elist2, cs, cs2;
   int ins, popd, ppi, order, anc;
   int rcand, rcandv;  // the merged row of the depth being expanded
   int rowids, uslice;  // all rows' candidate ids; this member's U slice of one depth
@@ -144,6 +149,8 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
   l.newidx = take(NC * 2);
   l.elist = take(NC * 2);
   l.elist2 = take(NC * 2);
+  l.cs = take(kCsCap * 4);
+  l.cs2 = take(kCsCap * 4);
   l.ins = take(NC);
   l.popd = take(NC);
   l.ppi = take(NC * 2);
@@ -178,13 +185,18 @@ __host__ __device__ inline Lds lds_layout(int dh, int G, int M, int nchunks, int
 }
 
 // scalar slots in LDS
-enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NCAND, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR, S_CNT0 };
+enum { S_NN, S_VB, S_NEXP, S_STATUS, S_NCAND, S_NC, S_TOT, S_STOP, S_NPOP, S_R, S_MERGEFLAG, S_SLOT, S_CUR,
+       S_NNEXT0, S_NNEXT1 };
+// per-wave slots (16-byte aligned: read as two float4)
+constexpr int S_CNT0 = 16;
 // after the per-wave slots S_CNT0 ..: which candidate buffer holds the list,
-// the next list's count, and where the last append started
+// where the last append started, and the list's entries.  The next list's
+// count alternates between S_NNEXT0 and S_NNEXT1 from one ranking to the next.
+static_assert(kExpThreads / 64 == 8, "eight per-wave slots");
 constexpr int S_CLIST = S_CNT0 + kExpThreads / 64;
-constexpr int S_NNEXT = S_CLIST + 1;
-constexpr int S_ABASE = S_CLIST + 2;
-static_assert(S_ABASE + 1 <= 32, "scalar slots below the reduction area");
+constexpr int S_ABASE = S_CLIST + 1;
+constexpr int S_NVAL = S_CLIST + 2;  // entries of the current list: candidates, then new children
+static_assert(S_NVAL + 1 <= 32, "scalar slots below the reduction area");
 
 
 // GRU activations on the hardware exp2 and reciprocal (about 1 ulp each):
@@ -309,6 +321,16 @@ __device__ inline float wave_sum_f(float v) {
 }
 __device__ inline float wave_min_f(float v) {
   return sel::wave_reduce(v, [](float x, float y) { return fminf(x, y); });
+}
+
+// inclusive prefix sum over each row of 16 lanes (DPP row shifts; a lane
+// whose source lies outside the row adds 0)
+__device__ inline int row_prefix16(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  return x;
 }
 
 // ordered exclusive prefix of a predicate over the block (wcnt: NW ints in LDS)
@@ -500,6 +522,8 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int16_t *newidx = reinterpret_cast<int16_t *>(smem + ly.newidx);
   int16_t *elist = reinterpret_cast<int16_t *>(smem + ly.elist);
   int16_t *elist2 = reinterpret_cast<int16_t *>(smem + ly.elist2);
+  float *cs = reinterpret_cast<float *>(smem + ly.cs);
+  float *cs2 = reinterpret_cast<float *>(smem + ly.cs2);
   uint8_t *ins = reinterpret_cast<uint8_t *>(smem + ly.ins);
   uint8_t *popd = reinterpret_cast<uint8_t *>(smem + ly.popd);
   int16_t *ppi = reinterpret_cast<int16_t *>(smem + ly.ppi);
@@ -525,6 +549,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int *wcnt = scal + 48;
   uint64_t *sortbuf = reinterpret_cast<uint64_t *>(smem + ly.sortbuf);
   float2 *red = reinterpret_cast<float2 *>(scal + 32);
+  int *xoff = scal + 32;  // after the prologue: the chunk's nodes' first child offsets
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = a.L, M = a.M, B = a.B, dh = a.dh, G = a.G;
@@ -572,6 +597,13 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scal[S_NCAND] = 0;  // no candidates yet (vB is -inf)
     scal[S_CLIST] = 0;
     scal[S_ABASE] = 0;
+    scal[S_NVAL] = 0;
+    scal[S_NNEXT0] = 0;
+    scal[S_NNEXT1] = 0;
+  }
+  for (int i = tid; i < kCsCap; i += NT) {
+    cs[i] = NEG_INF;  // (entries past a list's end read -inf)
+    cs2[i] = NEG_INF;
   }
   __syncthreads();
 
@@ -699,7 +731,99 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   constexpr int kW1T = 2, kW1Q = 2;
   typename W4<TW>::T w1f[kW1T][kW1Q];
   const bool w1keep = HEAD && SDH > 0 && a.rank / 16 <= kW1T * NW && UW / 16 <= kW1Q;
+  // ---- the candidates: every known node scoring >= vB, the B-th best known
+  // score -- the only nodes that can still be popped or expanded.  They stay
+  // listed in one of two buffers (S_CLIST names it, S_NCAND their number); a
+  // step ranks the old candidates and its new children, which all scored >=
+  // the old vB when they were appended; no other node can be among the B
+  // best.  A value is a candidate when fewer than B values exceed it.  Both
+  // rankings write the next list (S_NNEXT0 + npar entries, with the scores of the
+  // first kCsCap) and each wave's least candidate score (S_CNT0 + wave); the
+  // select step then sets vB from them.
+  //
+  // rank_list: the current list holds nval entries, candidates then children,
+  // with their scores (entries past nval read -inf); a child's code becomes its
+  // table index, base + xoff[c] + rank (xoff: this wave's own copy of the
+  // offsets, written before the call).
+  int npar = 0;     // S_NNEXT0 + npar counts the next list (the same in every wave)
+  int clist_r = 0;  // the current list (S_CLIST; the same in every wave)
+  auto rank_list = [&](int clist, int nval, int base) {
+    const float *cv = clist ? cs2 : cs;
+    const int16_t *ci = clist ? elist2 : elist;
+    float *nv = clist ? cs : cs2;
+    int16_t *ni = clist ? elist : elist2;
+    const float4 *c4 = reinterpret_cast<const float4 *>(cv);
+    const int n4 = (nval + 3) >> 2;
+    float best = __builtin_huge_valf();
+    for (int q = tid; q < nval; q += NT) {
+      const float gi = cv[q];
+      int cnt = 0;
+#pragma unroll 4
+      for (int j = 0; j < n4; ++j) {  // (no early exit: the loads stay in flight together)
+        const float4 v = c4[j];
+        cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
+      }
+      if (cnt < B) {  // among the B best (ties included): a candidate
+        best = fminf(best, gi);
+        int id = ci[q];
+        if (id < 0) {
+          const int e = -1 - id;
+          id = base + xoff[e >> 8] + (e & 255);
+        }
+        const int j = atomicAdd(&scal[S_NNEXT0 + npar], 1);
+        ni[j] = (int16_t)id;
+        if (j < kCsCap) nv[j] = gi;
+      }
+    }
+    best = wave_min_f(best);
+    if (lane == 0) scalf[S_CNT0 + wave] = best;
+  };
+  // rank_table: the old candidates and the nodes appended since the last
+  // ranking (from S_ABASE) are gathered and ranked, or, if more than the
+  // gather buffer holds, every node of the table.
+  const int kGather = CH * MP;  // floats of `ell`, free between expansion steps
+  auto rank_table = [&]() {
+    const int nn = scal[S_NN];
+    const int ncand = scal[S_NCAND];
+    const int abase = scal[S_ABASE];
+    const int clist = clist_r;
+    const int16_t *cur = clist ? elist2 : elist;
+    int16_t *nxt = clist ? elist : elist2;
+    float *nv = clist ? cs : cs2;
+    const int ntot = ncand + (nn - abase);
+    const bool incr = ntot <= kGather;
+    const int nr = incr ? ntot : nn;  // nodes ranked
+    float *cg = ell;
+    if (incr)
+      for (int q = tid; q < ntot; q += NT) cg[q] = ng[q < ncand ? cur[q] : abase + q - ncand];
+    __syncthreads();
+    const float *src = incr ? cg : ng;
+    const float4 *g4 = reinterpret_cast<const float4 *>(src);
+    const int n4 = nr >> 2;
+    float best = __builtin_huge_valf();
+    for (int q = tid; q < nr; q += NT) {
+      const float gi = src[q];
+      int cnt = 0;
+#pragma unroll 4
+      for (int j = 0; j < n4; ++j) {
+        const float4 v = g4[j];
+        cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
+      }
+      for (int j = n4 * 4; j < nr; ++j) cnt += src[j] > gi;
+      if (cnt < B) {
+        best = fminf(best, gi);
+        const int j = atomicAdd(&scal[S_NNEXT0 + npar], 1);
+        nxt[j] = (int16_t)(incr ? (q < ncand ? cur[q] : abase + q - ncand) : q);
+        if (j < kCsCap) nv[j] = gi;
+      }
+    }
+    best = wave_min_f(best);
+    if (lane == 0) scalf[S_CNT0 + wave] = best;
+  };
+
   int pb = 0;  // partial-buffer parity
+  // L2 prefetches of the next staging's rows, consumed after its wait
+  float pf[3] = {0.0f, 0.0f, 0.0f};
   auto expand_chunk = [&](const int16_t *cn, int nc, int d) {
     // one batched round trip: the merged row of depth d (the children's
     // candidates and tail) and the parent path states of the chunk's nodes
@@ -799,6 +923,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       if (tid == NT - 1) scalf[S_R] = rt;
       __builtin_amdgcn_s_waitcnt(0);  // includes the LDS writes of the loads above
+      asm volatile("" ::"v"(pf[0]), "v"(pf[1]), "v"(pf[2]));  // (the prefetches: done)
       if (HEAD && tid < a.RJ) has[tid] = hav;
     }
     __syncthreads();
@@ -1049,6 +1174,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // 3. children of each node: normalise, rank, keep the top-k above vB
     const float vB = scalf[S_VB];
     const float R = scalf[S_R];
+    const int clist = clist_r;  // the candidate list the children join
     const __amdgpu_buffer_rsrc_t rp = dev_rsrc(a.part + ((size_t)t * 2 + pb) * G * CH * MP);
     pb ^= 1;
     // the G parts of a slot, one from each member's block: all loads are
@@ -1065,7 +1191,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       return p;
     };
-    auto node_children = [&](int c, const Parts &p0) {
+    auto node_children = [&](int c, const Parts &p0) -> int {
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
       float lv[4];
       if (a.menu_in) {
@@ -1124,7 +1250,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       if (ne == 0) {
         if (lane == 0) wcnt[c] = 0;
-        return;
+        return 0;
       }
       int kc = 0;
       if (ne <= 24) {
@@ -1185,30 +1311,66 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         }
       }
       if (lane == 0) wcnt[c] = kc;
+      return kc;
     };
     // two nodes per wave: the second node's loads are in flight during the first
     const int c0 = wave, c1 = wave + NW;
     Parts p0, p1;
     if (c0 < nc && !nocorr) p0 = load_parts(c0, 0);
     if (c1 < nc && !nocorr) p1 = load_parts(c1, 0);
+    int k0 = 0, k1 = 0;
     if (c0 < nc)
-      node_children(c0, p0);
+      k0 = node_children(c0, p0);
     else if (lane == 0)
       wcnt[c0] = 0;
     if (c1 < nc)
-      node_children(c1, p1);
+      k1 = node_children(c1, p1);
     else if (lane == 0)
       wcnt[c1] = 0;
+    // The kept children also join this step's candidate list after the old
+    // candidates (positions from one counter per wave; their order does not
+    // matter): score, and the code -1 - (256 c + rank), which becomes a table
+    // index once the nodes' offsets are known.  Entries past kCsCap are
+    // dropped (the step then ranks the table instead).  Ranks and log-probs
+    // are read back from this wave's own rnk and ell rows.
+    if (k0 + k1 > 0) {
+      int o = 0;
+      if (lane == 0) o = atomicAdd(&scal[S_NVAL], k0 + k1);
+      o = __builtin_amdgcn_readlane(o, 0);
+      float *lcs = clist ? cs2 : cs;
+      int16_t *lci = clist ? elist2 : elist;
+      for (int h = 0; h < 2; ++h) {
+        const int c = h ? c1 : c0, oc = h ? o + k0 : o;
+        if ((h ? k1 : k0) == 0) continue;
+        const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          if (s >= MP / 64) break;
+          const int m = lane + 64 * s;
+          const int r = rnk[c * MP + m];
+          if (r >= 0 && oc + r < kCsCap) {
+            lcs[oc + r] = gpar + ell[c * MP + m];
+            lci[oc + r] = (int16_t)(-1 - (c * 256 + r));
+          }
+        }
+      }
+    }
     // (read before the barrier: thread 0 rewrites it after the barrier)
     const int base = scal[S_NN];
     __syncthreads();
-    // 4. append children (node order, then rank order) to the node table
-    int tot = 0;
-    for (int c = 0; c < nc; ++c) tot += wcnt[c];
+    // 4. append children (node order, then rank order) to the node table: node
+    // c's children start at base + the children of nodes 0..c-1 (a prefix sum
+    // over the lanes of row 0; nc <= 16)
+    const int wc = lane < nc ? wcnt[lane] : 0;
+    const int nval = scal[S_NVAL];
+    const int incl = row_prefix16(wc);
+    const int tot = __builtin_amdgcn_readlane(incl, 15);
+    const int excl = incl - wc;
+    // (every wave writes the same offsets; each reads back its own)
+    if (lane < CH) xoff[lane] = excl;
     for (int c = wave; c < nc; c += NW) {
-      if (wcnt[c] == 0) continue;
-      int off = base;
-      for (int c2 = 0; c2 < c; ++c2) off += wcnt[c2];
+      if (__builtin_amdgcn_readlane(wc, c) == 0) continue;
+      const int off = base + __builtin_amdgcn_readlane(excl, c);
       const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
       #pragma unroll
       for (int s = 0; s < 4; ++s) {
@@ -1230,6 +1392,38 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         }
       }
     }
+    // Prefetch into L2 what the next steps stage: the P rows (this member's
+    // three gate slices, 128-byte lines) of the children this wave appended --
+    // tokens read back from its own table writes -- and this member's U slice
+    // of the next depth's candidates.  The values are consumed only after the
+    // next staging's wait, so nothing waits for them earlier: their HBM latency
+    // passes during the ranking and the select step.
+    if (!a.nocorr) {
+      const int LPS = (UW * 4 + 127) / 128;  // lines per gate slice
+      const int per = 3 * LPS;               // lines per child
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c = wave + h * NW;
+        pf[h] = 0.0f;
+        if (c < nc) {
+          const int r = lane / per;
+          const int pos = base + __builtin_amdgcn_readlane(excl, c) + r;
+          if (r < __builtin_amdgcn_readlane(wc, c) && pos < NC) {
+            const int gl = lane - r * per, g = gl / LPS;
+            pf[h] = a.P_all[(size_t)ntok[pos] * (3 * dh) + g * dh + member * UW + (gl - g * LPS) * 32];
+          }
+        }
+      }
+      pf[2] = 0.0f;
+      if (a.use_us && wave == NW - 1 && d + 1 < L) {
+        const int m = lane / LPS;
+        if (m < M)
+          pf[2] = a.U_all[(size_t)rowids[(d + 1) * MP + m] * dh + member * UW + (lane - m * LPS) * 32];
+      }
+    }
+    // 5. the candidates: rank the list of old candidates and new children in
+    // place, or, when the table or the list overflowed, the table
+    const bool inlist = base + tot <= NC && nval <= kCsCap;
     // (these writes touch no entry the appends above write)
     if (tid == 0) {
       int nn = base + tot;
@@ -1238,68 +1432,17 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         scal[S_STATUS] |= DT_TREE_TRUNCATED;  // table overflow (massive exact ties)
       }
       scal[S_NN] = nn;
-      scal[S_ABASE] = base;
+      scal[S_ABASE] = inlist ? nn : base;
       if (d > 0) scal[S_NEXP] += nc;
     }
     if (d > 0 && tid < nc) nexp[cn[tid]] = 1;
-    __syncthreads();
-  };
-
-  // ---- vB = B-th best known score ---------------------------------------------
-  // The nodes scoring >= vB -- the candidates, the only nodes that can still be
-  // popped or expanded -- stay listed in one of two buffers (S_CLIST names it,
-  // S_NCAND their number).  A new vB ranks the old candidates and the children
-  // appended since, which all scored >= the old vB when they were appended; no
-  // other node can be among the B best.  (If more than the gather buffer holds,
-  // every node of the table is ranked instead.)  Returns vB to every thread;
-  // S_VB and the list are written for readers past the next barrier.
-  const int kGather = CH * MP;  // floats of `ell`, free between expansion steps
-  auto update_vb = [&]() -> float {
-    const int nn = scal[S_NN];
-    const int ncand = scal[S_NCAND];
-    const int abase = scal[S_ABASE];
-    const int16_t *cur = scal[S_CLIST] ? elist2 : elist;
-    int16_t *nxt = scal[S_CLIST] ? elist : elist2;
-    const int ntot = ncand + (nn - abase);
-    const bool incr = ntot <= kGather;
-    const int nr = incr ? ntot : nn;  // nodes ranked
-    float *cg = ell;
-    if (incr)
-      for (int q = tid; q < ntot; q += NT) cg[q] = ng[q < ncand ? cur[q] : abase + q - ncand];
-    if (tid == 0) scal[S_NNEXT] = 0;
-    __syncthreads();
-    const float *src = incr ? cg : ng;
-    const float4 *g4 = reinterpret_cast<const float4 *>(src);
-    const int n4 = nr >> 2;
-    float best = __builtin_huge_valf();
-    for (int q = tid; q < nr; q += NT) {
-      const float gi = src[q];
-      int cnt = 0;
-#pragma unroll 4
-      for (int j = 0; j < n4; ++j) {  // (no early exit: the loads stay in flight together)
-        const float4 v = g4[j];
-        cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
-      }
-      for (int j = n4 * 4; j < nr; ++j) cnt += src[j] > gi;
-      if (cnt < B) {  // among the B best (ties included): a candidate
-        best = fminf(best, gi);
-        nxt[atomicAdd(&scal[S_NNEXT], 1)] = (int16_t)(incr ? (q < ncand ? cur[q] : abase + q - ncand) : q);
-      }
+    if (inlist) {
+      rank_list(clist, nval, base);
+    } else {
+      __syncthreads();
+      rank_table();
     }
-    best = wave_min_f(best);
-    if (lane == 0) scalf[S_CNT0 + wave] = best;
     __syncthreads();
-    float vB = scalf[S_CNT0];
-#pragma unroll
-    for (int w = 1; w < NW; ++w) vB = fminf(vB, scalf[S_CNT0 + w]);
-    if (nn < B) vB = -__builtin_huge_valf();  // fewer than B known: every node qualifies
-    if (tid == 0) {
-      scalf[S_VB] = vB;
-      scal[S_NCAND] = scal[S_NNEXT];
-      scal[S_CLIST] ^= 1;
-      scal[S_ABASE] = nn;  // (a repeated call ranks no node twice)
-    }
-    return vB;
   };
 
   // ---- drop the nodes below vB to make room (parents always score at least
@@ -1384,9 +1527,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   }
   expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
   int nsteps = 1;
+  bool ranked = true;  // a ranking since the last select step
+  int cur_r = 0;       // the cursor (the same in every wave)
   for (;;) {
     if (scal[S_STATUS] & DT_TREE_TIMEOUT) break;
-    const float vB = update_vb();
     if (a.W > 0) {
       // Frontier builder (Appendix B): only the top W nodes of their depth, by
       // (score desc, table order), become lanes.  The table is depth-ordered,
@@ -1405,76 +1549,112 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       __syncthreads();
     }
-    if (wave == 0) {
-      const int nn = scal[S_NN];
-      int p = scal[S_CUR], c = 0, dsel = -1;
-      bool done = false;
-      while (!done && p < nn) {
-        const int i = p + lane;
-        const bool ok = i < nn && !nexp[i] && ndepth[i] < L && ng[i] >= vB && (a.W == 0 || ins[i]);
-        const int di = ok ? (int)ndepth[i] : -1;
-        const uint64_t bal = __ballot(ok);
-        if (bal == 0) {
-          p += 64;
-          continue;
-        }
-        if (dsel < 0) dsel = __shfl(di, __builtin_ctzll(bal));
-        const uint64_t deeper = __ballot(ok && di != dsel);
-        uint64_t use = __ballot(ok && di == dsel);
-        if (deeper) use &= (1ull << __builtin_ctzll(deeper)) - 1;  // stop at the next depth
-        const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(use >> 32),
-                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)use, 0));
-        const bool mine = (use >> lane) & 1ull;
-        const int have = __popcll(use), need = chunk_cap - c;
-        if (mine && before < need) cl[c + before] = (int16_t)i;
-        if (have >= need) {
-          // the cursor moves right past the need-th node taken
-          const uint64_t last = __ballot(mine && before == need - 1);
-          p += __builtin_ctzll(last) + 1;
-          c = chunk_cap;
+    // Every wave takes the select step itself, with identical results: vB,
+    // the next list and the next chunk (the chunk and the shared words are
+    // written with the same contents by every wave, and each reads back its
+    // own), so no barrier follows it.  (The next step's staging barrier keeps
+    // every wave's reads here ahead of the step's writes.)
+    const int4 s0 = *reinterpret_cast<const int4 *>(scal);  // S_NN, S_VB, S_NEXP, S_STATUS
+    const int nn = s0.x;
+    float vB;
+    if (ranked) {
+      // vB from the ranking: the least candidate score, or -inf while fewer
+      // than B nodes are known (every node is then a candidate); the next list
+      // becomes the current one
+      const float4 m0 = *reinterpret_cast<const float4 *>(scalf + S_CNT0);
+      const float4 m1 = *reinterpret_cast<const float4 *>(scalf + S_CNT0 + 4);
+      const int nnext = scal[S_NNEXT0 + npar];
+      vB = fminf(fminf(fminf(m0.x, m0.y), fminf(m0.z, m0.w)), fminf(fminf(m1.x, m1.y), fminf(m1.z, m1.w)));
+      if (nn < B) vB = -__builtin_huge_valf();
+      clist_r ^= 1;
+      if (lane == 0) {
+        scalf[S_VB] = vB;
+        scal[S_NCAND] = nnext;
+        scal[S_CLIST] = clist_r;
+        scal[S_ABASE] = nn;  // (a repeated ranking ranks no node twice)
+        scal[S_NVAL] = nnext;
+        scal[S_NNEXT0 + (npar ^ 1)] = 0;  // (read by every wave a ranking ago)
+      }
+      npar ^= 1;
+      if (wave == 0) {
+        float *ncs = clist_r ? cs2 : cs;
+        for (int i = lane; i < kCsCap; i += 64)
+          if (i >= nnext) ncs[i] = NEG_INF;
+      }
+    } else {
+      vB = __builtin_bit_cast(float, s0.y);
+    }
+    int p = cur_r, c = 0, dsel = -1;
+    bool done = false;
+    while (!done && p < nn) {
+      const int i = p + lane;
+      const int ic = i < nn ? i : 0;  // (every load issued: one wait)
+      const int ex = nexp[ic], dp = ndepth[ic], in_ = ins[ic];
+      const float gg = ng[ic];
+      const bool ok = (i < nn) & (ex == 0) & (dp < L) & (gg >= vB) & ((a.W == 0) | (in_ != 0));
+      const int di = ok ? dp : -1;
+      const uint64_t bal = __ballot(ok);
+      if (bal == 0) {
+        p += 64;
+        continue;
+      }
+      if (dsel < 0) dsel = __builtin_amdgcn_readlane(di, __builtin_ctzll(bal));
+      const uint64_t deeper = __ballot(ok && di != dsel);
+      uint64_t use = __ballot(ok && di == dsel);
+      if (deeper) use &= (1ull << __builtin_ctzll(deeper)) - 1;  // stop at the next depth
+      const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(use >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)use, 0));
+      const bool mine = (use >> lane) & 1ull;
+      const int have = __popcll(use), need = chunk_cap - c;
+      if (mine && before < need) cl[c + before] = (int16_t)i;
+      if (have >= need) {
+        // the cursor moves right past the need-th node taken
+        const uint64_t last = __ballot(mine && before == need - 1);
+        p += __builtin_ctzll(last) + 1;
+        c = chunk_cap;
+        done = true;
+      } else {
+        c += have;
+        if (deeper) {
+          p += __builtin_ctzll(deeper);
           done = true;
         } else {
-          c += have;
-          if (deeper) {
-            p += __builtin_ctzll(deeper);
-            done = true;
-          } else {
-            p += 64;
-          }
-        }
-      }
-      if (lane == 0) {
-        scal[S_NC] = c;
-        scal[S_CUR] = p < nn ? p : nn;
-        if (c && scal[S_NEXP] + c > a.ecap - 1) {
-          scal[S_STATUS] |= DT_TREE_TRUNCATED;
-          scal[S_STOP] = 1;
+          p += 64;
         }
       }
     }
-    __syncthreads();
-    const int nc = scal[S_NC];
-    if (scal[S_STOP] || nc == 0) break;
-    if (scal[S_NN] + nc * a.k > NC - CH) {
+    cur_r = p < nn ? p : nn;
+    if (c && s0.z + c > a.ecap - 1) {
+      if (tid == 0) atomicOr(&scal[S_STATUS], DT_TREE_TRUNCATED);
+      break;
+    }
+    if (c == 0) break;
+    int nc = c;
+    if (nn + nc * a.k > NC - CH) {
       // make room for this chunk's children; the cursor restarts (nodes it
       // passed are expanded or below vB, and are passed again)
+      __syncthreads();  // (every wave's select reads ahead of the moves)
       compact_table();
       if (tid == 0) {
         int c2 = 0;
-        for (int c = 0; c < nc; ++c) {
-          const int i = newidx[cl[c]];
+        for (int c3 = 0; c3 < nc; ++c3) {
+          const int i = newidx[cl[c3]];
           if (i >= 0) cl[c2++] = (int16_t)i;
         }
         scal[S_NC] = c2;
-        scal[S_CUR] = 0;
       }
       __syncthreads();
+      nc = scal[S_NC];
+      cur_r = 0;
     }
-    const int nc2 = scal[S_NC];
-    if (nc2 == 0) continue;
-    expand_chunk(cl, nc2, ndepth[cl[0]]);
+    ranked = false;
+    if (nc == 0) continue;
+    expand_chunk(cl, nc, dsel);
+    ranked = true;
     ++nsteps;
   }
+  __builtin_amdgcn_s_waitcnt(0);  // (the last prefetches)
+  asm volatile("" ::"v"(pf[0]), "v"(pf[1]), "v"(pf[2]));
   if (scal[S_STATUS] & DT_TREE_TIMEOUT) {
     // a wait gave up: the tree may hold parts of members that had not written
     // them; it is emitted empty
