@@ -86,7 +86,7 @@ Workspace carve(const dt_plan *p, int batch, char *base) {
   ws.part = at(expand_part_bytes(p, batch));
   // per tree: barrier counters; then the member-slot counters of the launch
   // (two sets: a call makes up to two expansion launches)
-  ws.bar = reinterpret_cast<int32_t *>(at((size_t)2 * (batch + 2) * kBarStride * sizeof(int32_t)));
+  ws.bar = reinterpret_cast<int32_t *>(at((size_t)2 * (batch + kSlotRows) * kBarStride * sizeof(int32_t)));
   ws.menus = p->scorer == DT_SCORER_STATIC
                  ? at((size_t)batch * p->L * ((p->M + 63) / 64 * 64) * sizeof(float))
                  : nullptr;
@@ -457,7 +457,7 @@ static dt_status build_tree_on(dt_plan *plan, const void *logits, int batch, con
   // profiled calls time each kernel from its start to its end
   hipEvent_t *ev = prof ? plan->ev + 4 * (plan->profiled_calls % dt::kProfSlots) : nullptr;
   // the scan kernel also clears the expansion launches' barrier counters
-  const int nbar = (batch + 2) * dt::kBarStride;
+  const int nbar = (batch + dt::kSlotRows) * dt::kBarStride;
   hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, ws, ws.bar, 2 * nbar, s,
                                         prof ? ev[0] : nullptr, prof ? ev[1] : nullptr);
   if (e != hipSuccess) return hip_fail(e, "scan launch");
@@ -687,7 +687,7 @@ dt_status dt_build_tree_head(dt_plan *plan, const void *logits, int batch, const
     // workgroups compute a_d = W_1^H H_d), then the default path's expansion
     // kernel with Domino's head
     const HeadFastWs hf = carve_head_fast(plan, batch, head->rank, G, static_cast<char *>(workspace));
-    const int nbar = (batch + 2) * dt::kBarStride;
+    const int nbar = (batch + dt::kSlotRows) * dt::kBarStride;
     const dt::HeadProj hp = dt::head_proj_args(plan, batch * plan->L, H, *head, hf.a);
     hipError_t e = dt::launch_scan_chunks(logits, plan->ldt, g, inv_tau, hf.ws, hf.ws.bar, 2 * nbar, s,
                                           prof ? ev[0] : nullptr, prof ? ev[1] : nullptr, &hp);

@@ -85,7 +85,7 @@ struct ExpArgs {
   const float *h0;
   float *states;   // [batch][ecap][dh] path states of expanded nodes; slot ecap-1: the root
   float *part;     // [batch][2][G][CH][MP] partial corrections
-  int32_t *bar;    // [batch + 2][kBarStride] barrier and slot counters (zeroed by the scan kernel)
+  int32_t *bar;    // [batch + kSlotRows][kBarStride] barrier and slot counters (zeroed by the scan kernel)
   dt_tree out;
 };
 
@@ -306,12 +306,13 @@ __device__ inline void st_dev16(__amdgpu_buffer_rsrc_t r, int byte_off, float4 v
 }
 
 __device__ inline uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint64_t p = __shfl_xor(v, o);
-    v = p > v ? p : v;
-  }
-  return v;
+  auto mx = [](uint64_t x, uint64_t y) { return x > y ? x : y; };
+  v = mx(v, sel::lane_xor64<32>(v));
+  v = mx(v, sel::lane_xor64<16>(v));
+  v = mx(v, sel::lane_xor64<8>(v));
+  v = mx(v, sel::lane_xor64<4>(v));
+  v = mx(v, sel::lane_xor64<2>(v));
+  return mx(v, sel::lane_xor64<1>(v));
 }
 __device__ inline float wave_max_f(float v) {
   return sel::wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
@@ -568,8 +569,11 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   int t, member;
   if (G > 1) {
     const int xcd = blockIdx.x % a.nxcd;
+    // (an XCD class without a tree -- tree t lives in class t % nxcd -- leaves
+    // at once: its slot could only name a tree >= batch)
+    if (xcd >= a.batch) return;
     if (tid == 0)
-      scal[S_SLOT] = __hip_atomic_fetch_add(a.bar + a.batch * kBarStride + xcd * 16, 1,
+      scal[S_SLOT] = __hip_atomic_fetch_add(a.bar + a.batch * kBarStride + xcd * kSlotStride, 1,
                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     const int kk = scal[S_SLOT];

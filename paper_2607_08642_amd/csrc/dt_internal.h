@@ -39,7 +39,9 @@ constexpr int kExpThreads = 512;
 constexpr int kNodeCap = 1536;       // live nodes per tree kept in LDS
 constexpr int kChunkNodes = 16;      // nodes expanded together (shared weight pass)
 constexpr int kBarStride = 64;       // ints per tree of barrier counters (own cache lines)
-constexpr int kMaxXcd = 8;           // member-slot counters: 16 ints per XCD in 2 x kBarStride
+constexpr int kMaxXcd = 8;           // XCDs with a member-slot counter each
+constexpr int kSlotStride = 32;      // ints per XCD's slot counter (its own 128-byte line)
+constexpr int kSlotRows = kMaxXcd * kSlotStride / kBarStride;  // kBarStride rows of slot counters
 constexpr int kProfSlots = 1024;     // profiled calls kept for stage averages
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -139,7 +141,7 @@ struct Workspace {
   // expansion
   float *states;          // [batch][ecap][dh]
   float *part;            // [batch][2][G][16][MP] partial corrections
-  int32_t *bar;           // [2][batch + 2][kBarStride] barrier and slot counters (one set
+  int32_t *bar;           // [2][batch + kSlotRows][kBarStride] barrier and slot counters (one set
                           // per expansion launch of a call)
   float *menus;           // [batch][L][MP] corrected menus of the greedy chain (scorer
                           // DT_SCORER_STATIC)

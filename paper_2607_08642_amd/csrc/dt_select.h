@@ -86,22 +86,6 @@ __device__ inline Tail block_tail(Tail t, float c, float2 *red) {
   return Tail{m, sum};
 }
 
-// descending bitonic sort of a wave's 64 values (one per lane)
-__device__ inline uint64_t wave_sort_desc(uint64_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const uint64_t p = __shfl_xor(v, j);
-      const bool desc = (lane & k) == 0;
-      const bool lower = (lane & j) == 0;
-      v = (desc == lower) ? (v > p ? v : p) : (v < p ? v : p);
-    }
-  }
-  return v;
-}
-
 __host__ __device__ inline int pow2_at_least(int n, int lo) {
   int p = lo;
   while (p < n) p <<= 1;
