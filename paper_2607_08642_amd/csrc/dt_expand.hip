@@ -841,6 +841,20 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // (Domino's head is not zero at a zero state: SiLU(a_d))
     const bool nocorr = a.nocorr || (!HEAD && d == 0 && a.h0 == nullptr);
     if (d > 0 && tid < nc) nstate[cn[tid]] = (int16_t)(scal[S_NEXP] + tid);
+    // the chunk's nodes in registers (lane c < nc of every wave): node, token,
+    // score and the parent's state slot, read once; the new state of node c
+    // goes to slot q_base + c
+    const int root_slot = a.ecap - 1;
+    const int q_base = scal[S_NEXP];
+    int q_node = 0, q_tok = 0, q_pslot = root_slot;
+    float q_g = 0.0f;
+    if (d > 0 && lane < nc) {
+      q_node = cn[lane];
+      q_tok = ntok[q_node];
+      q_g = ng[q_node];
+      const int par = nparent[q_node];
+      if (par >= 0) q_pslot = nstate[par];
+    }
     {
       // all loads are issued before the first LDS write (one wait)
       const size_t row = (size_t)t * L + (d < L ? d : 0);
@@ -856,17 +870,14 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       }
       if (d < L && tid == NT - 1) rt = ld_dev(a.tailR + row);
       // parent states straight into LDS (16 bytes per lane, 256 floats per
-      // wave instruction); unused columns read the root slot
+      // wave instruction), the chunk's nc columns only: the MFMA outputs of the
+      // other columns are never read (an instruction that reaches past column
+      // nc - 1 reads the root slot there)
       if (d > 0 && !a.nocorr) {
-        const int root_slot = a.ecap - 1;
-        for (int i = wave; i < CH * dh / 256; i += NW) {
+        for (int i = wave; i < (nc * dh + 255) / 256; i += NW) {
           const int e = i * 256 + 4 * lane;
           const int c = e / dh, k = e - c * dh;
-          int slot = root_slot;
-          if (c < nc) {
-            const int par = nparent[cn[c]];
-            if (par >= 0) slot = nstate[par];
-          }
+          const int slot = __builtin_amdgcn_ds_bpermute(c * 4, q_pslot);  // (root slot for c >= nc)
           // (one row, or whole rows when unpadded: the 256 floats are contiguous)
           const int c0 = (i * 256) / dh;
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -913,7 +924,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         const int g = lane / QW, k = (lane - g * QW) * 4;
         const int voff = lane < 3 * QW ? (g * dh + k) * 4 : 0;
         for (int c = wave; c < nc; c += NW) {
-          const int tok = __builtin_amdgcn_readfirstlane(ntok[cn[c]]);
+          const int tok = __builtin_amdgcn_readlane(q_tok, c);
           const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
               const_cast<float *>(a.P_all + (size_t)tok * (3 * dh) + member * UW), 0, 0x7FFFFFF0,
               0x00020000);
@@ -942,7 +953,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     } else {
       const int c = lane & 15;
       const int node = c < nc ? cn[c] : -1;
-      const float *prow = a.P_all + (size_t)(node >= 0 ? ntok[node] : 0) * (3 * dh);
+      const float *prow = use_pin ? a.P_all : a.P_all + (size_t)(node >= 0 ? ntok[node] : 0) * (3 * dh);
       // r = sig(P_r + W_hr h), z = sig(P_z + W_hz h), n = tanh(P_n + r (W_hn h + b_hn)),
       // S = (1 - z) n + z h  (P_r, P_z carry b_hr, b_hz)
       auto apply = [&](int gi, const f32x4 (&gh)[3]) {
@@ -972,7 +983,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           Sn[c * UW + u4 + i] = sv[i];
         }
         const __amdgpu_buffer_rsrc_t rsw = dev_rsrc(a.states + (size_t)t * a.ecap * dh);
-        st_dev16(rsw, (nstate[node] * dh + j0) * 4, make_float4(sv[0], sv[1], sv[2], sv[3]));
+        st_dev16(rsw, ((q_base + c) * dh + j0) * 4, make_float4(sv[0], sv[1], sv[2], sv[3]));
       };
       if (NG >= NW) {
         for (int gi = wave; gi < NG; gi += NW) {
@@ -1009,7 +1020,6 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           const int gi = e >> 8, l = (e >> 2) & 63, i = e & 3;
           const int cc = l & 15;
           const bool live = e < NG * 256 && cc < nc;  // uniform over a quad
-          const int nd = live ? cn[cc] : 0;
           const int u = gi * 16 + (l >> 4) * 4 + i;
           const int j = member * UW + u;
           float sv = 0.0f;
@@ -1032,7 +1042,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
               // buffer loads: a pointer shared with the LDS branch would make
               // both flat accesses
               const __amdgpu_buffer_rsrc_t rpr = __builtin_amdgcn_make_buffer_rsrc(
-                  const_cast<float *>(a.P_all + (size_t)ntok[nd] * (3 * dh)), 0, 0x7FFFFFF0, 0x00020000);
+                  const_cast<float *>(a.P_all + (size_t)ntok[cn[cc]] * (3 * dh)), 0, 0x7FFFFFF0, 0x00020000);
               const __amdgpu_buffer_rsrc_t rbh =
                   __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.b_hh), 0, 0x7FFFFFF0, 0x00020000);
               xr = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rpr, j * 4, 0, 0));
@@ -1047,7 +1057,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
             Sn[cc * UW + u] = sv;
           }
           const float s1 = sel::dpp_f<0x55>(sv), s2 = sel::dpp_f<0xAA>(sv), s3 = sel::dpp_f<0xFF>(sv);
-          if (live && i == 0) st_dev16(rsw, (nstate[nd] * dh + j) * 4, make_float4(sv, s1, s2, s3));
+          if (live && i == 0) st_dev16(rsw, ((q_base + cc) * dh + j) * 4, make_float4(sv, s1, s2, s3));
         }
       }
     }
@@ -1196,7 +1206,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       return p;
     };
     auto node_children = [&](int c, const Parts &p0) -> int {
-      const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
+      const float gpar = (d == 0) ? 0.0f : __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, q_g), c));
       float lv[4];
       if (a.menu_in) {
         // a shared menu: depth d's slot log-probs, already normalised
@@ -1346,7 +1356,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       for (int h = 0; h < 2; ++h) {
         const int c = h ? c1 : c0, oc = h ? o + k0 : o;
         if ((h ? k1 : k0) == 0) continue;
-        const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
+        const float gpar = (d == 0) ? 0.0f : __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, q_g), c));
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
           if (s >= MP / 64) break;
@@ -1375,7 +1385,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     for (int c = wave; c < nc; c += NW) {
       if (__builtin_amdgcn_readlane(wc, c) == 0) continue;
       const int off = base + __builtin_amdgcn_readlane(excl, c);
-      const float gpar = (d == 0) ? 0.0f : ng[cn[c]];
+      const float gpar = (d == 0) ? 0.0f : __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, q_g), c));
       #pragma unroll
       for (int s = 0; s < 4; ++s) {
         if (s >= MP / 64) break;
@@ -1388,7 +1398,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
             ntok[pos] = ccand[m];
             nslot[pos] = (int16_t)m;
             ndepth[pos] = (uint8_t)(d + 1);
-            nparent[pos] = (d == 0) ? (int16_t)-1 : cn[c];
+            nparent[pos] = (d == 0) ? (int16_t)-1 : (int16_t)__builtin_amdgcn_readlane(q_node, c);
             nrank[pos] = (uint8_t)rk;
             nstate[pos] = -1;
             nexp[pos] = 0;
