@@ -1527,7 +1527,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   // >= vB, all at the depth of the first of them.  A node the cursor passes
   // without taking scores below vB, and vB only grows, so it can never be
   // popped.
-  if (wkeep) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);  // in flight during the root step
+  if (wkeep) Gates<TW>::preload(a, u0 + gu, gk0, gk1, wpre);  // in flight while the loop starts
   if (w1keep) {
     const TW *w1m = static_cast<const TW *>(a.w1) + a.d_H + member * UW + (lane >> 4) * 4;
 #pragma unroll
@@ -1539,11 +1539,20 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
           w1f[j][q] = W4<TW>::load(w1m + (size_t)(rt * 16 + (lane & 15)) * a.ld1 + q * 16);
       }
   }
-  expand_chunk(cl, 1, 0);  // root: children at depth 1 scored from h0
-  int nsteps = 1;
-  bool ranked = true;  // a ranking since the last select step
-  int cur_r = 0;       // the cursor (the same in every wave)
+  // One call site of expand_chunk (a second copy of the inlined step would
+  // double the loop's code and its register shuffling): the first pass
+  // expands the root (children at depth 1 scored from h0).
+  int nsteps = 0;
+  bool ranked = false;  // a ranking since the last select step
+  int cur_r = 0;        // the cursor (the same in every wave)
+  bool expand = true;   // a chunk to expand at the top of the loop
+  int x_nc = 1, x_d = 0;
   for (;;) {
+    if (expand) {
+      expand_chunk(cl, x_nc, x_d);
+      ranked = true;
+      ++nsteps;
+    }
     if (scal[S_STATUS] & DT_TREE_TIMEOUT) break;
     if (a.W > 0) {
       // Frontier builder (Appendix B): only the top W nodes of their depth, by
@@ -1662,10 +1671,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
       cur_r = 0;
     }
     ranked = false;
-    if (nc == 0) continue;
-    expand_chunk(cl, nc, dsel);
-    ranked = true;
-    ++nsteps;
+    expand = nc > 0;  // (none: select again)
+    x_nc = nc;
+    x_d = dsel;
   }
   __builtin_amdgcn_s_waitcnt(0);  // (the last prefetches)
   asm volatile("" ::"v"(pf[0]), "v"(pf[1]), "v"(pf[2]));
