@@ -605,10 +605,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     scal[S_NNEXT0] = 0;
     scal[S_NNEXT1] = 0;
   }
-  for (int i = tid; i < kCsCap; i += NT) {
-    cs[i] = NEG_INF;  // (entries past a list's end read -inf)
-    cs2[i] = NEG_INF;
-  }
+
   __syncthreads();
 
   // ---- prologue: merge this member's rows of the scan ------------------------
@@ -746,9 +743,9 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   // select step then sets vB from them.
   //
   // rank_list: the current list holds nval entries, candidates then children,
-  // with their scores (entries past nval read -inf); a child's code becomes its
-  // table index, base + xoff[c] + rank (xoff: this wave's own copy of the
-  // offsets, written before the call).
+  // with their scores; a child's code becomes its table index, base + xoff[c]
+  // + rank (xoff: this wave's own copy of the offsets, written before the
+  // call).
   int npar = 0;     // S_NNEXT0 + npar counts the next list (the same in every wave)
   int clist_r = 0;  // the current list (S_CLIST; the same in every wave)
   auto rank_list = [&](int clist, int nval, int base) {
@@ -757,7 +754,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     float *nv = clist ? cs : cs2;
     int16_t *ni = clist ? elist : elist2;
     const float4 *c4 = reinterpret_cast<const float4 *>(cv);
-    const int n4 = (nval + 3) >> 2;
+    const int n4 = nval >> 2, t0 = n4 * 4;
     float best = __builtin_huge_valf();
     for (int q = tid; q < nval; q += NT) {
       const float gi = cv[q];
@@ -767,6 +764,10 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         const float4 v = c4[j];
         cnt += (v.x > gi) + (v.y > gi) + (v.z > gi) + (v.w > gi);
       }
+      // the last nval % 4 entries (read together; entries past nval are not counted)
+      const float e0 = cv[min(t0, kCsCap - 1)], e1 = cv[min(t0 + 1, kCsCap - 1)],
+                  e2 = cv[min(t0 + 2, kCsCap - 1)];
+      cnt += (t0 < nval && e0 > gi) + (t0 + 1 < nval && e1 > gi) + (t0 + 2 < nval && e2 > gi);
       if (cnt < B) {  // among the B best (ties included): a candidate
         best = fminf(best, gi);
         int id = ci[q];
@@ -1599,11 +1600,6 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
         scal[S_NNEXT0 + (npar ^ 1)] = 0;  // (read by every wave a ranking ago)
       }
       npar ^= 1;
-      if (wave == 0) {
-        float *ncs = clist_r ? cs2 : cs;
-        for (int i = lane; i < kCsCap; i += 64)
-          if (i >= nnext) ncs[i] = NEG_INF;
-      }
     } else {
       vB = __builtin_bit_cast(float, s0.y);
     }
