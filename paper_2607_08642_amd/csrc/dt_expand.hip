@@ -1671,19 +1671,27 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     x_nc = nc;
     x_d = dsel;
   }
-  __builtin_amdgcn_s_waitcnt(0);  // (the last prefetches)
-  asm volatile("" ::"v"(pf[0]), "v"(pf[1]), "v"(pf[2]));
+  // the last step's prefetches are waited for on the way out (after the
+  // emission for the member that emits), not before the replay
+  auto drain = [&]() {
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::"v"(pf[0]), "v"(pf[1]), "v"(pf[2]));
+  };
   if (scal[S_STATUS] & DT_TREE_TIMEOUT) {
     // a wait gave up: the tree may hold parts of members that had not written
     // them; it is emitted empty
     if (member == 0 && a.emit) emit_empty();
+    drain();
     return;
   }
   if (a.stats && member == 0 && tid == 0) {
     a.stats[2 * t] = nsteps;
     a.stats[2 * t + 1] = scal[S_NEXP] + 1;  // the root and every expanded node
   }
-  if (member != 0 || !a.emit) return;
+  if (member != 0 || !a.emit) {
+    drain();
+    return;
+  }
 
   // ---- phase B: exact replay of the heap --------------------------------------
   // Only nodes scoring >= vB (the B-th best score in the table) can be among
@@ -1874,6 +1882,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     o.n_nodes[t] = npop;
     o.status[t] = scal[S_STATUS];
   }
+  drain();
 }
 
 }  // namespace
