@@ -269,6 +269,32 @@ def test_tie_rules_on_gpu():
     assert_identical(got, run_oracle(wl), what="twin tokens")
 
 
+def test_table_overflow_with_exact_ties():
+    # Constant rows and zero correction: every child ties with its siblings and
+    # cousins, B = 256 and k = M = 64, so one chunk of 16 depth-1 nodes appends
+    # 1,024 tied children; every node stays a candidate (all score >= vB), the
+    # candidate list outgrows its score buffer and the next chunk overflows the
+    # node table (the table's ranking path).  The tree is flagged truncated; its
+    # first 256 pops (64 depth-1 nodes, then the children of the first three by
+    # insertion order) were appended before the overflow and match the oracle's.
+    V, L, M, B = 128, 4, 64, 256
+    X = np.zeros((L, V), np.float32)
+    wl = synth.Workload("overflow", X[None], synth.DT_F32, None, _tie_weights(V, 8, 32), L, M, B, 0.0, 1)
+    ref = run_oracle(wl)
+    dw = DeviceWorkload(wl)
+    try:
+        got = dw.run()
+    finally:
+        dw.close()
+    assert int(got["status"][0]) & binding.DT_TREE_TRUNCATED, got["status"][0]
+    n = int(got["n_nodes"][0])
+    assert n == ref["n_nodes"] == B, (n, ref["n_nodes"])
+    for key in ("tokens", "parents", "depth", "position_ids"):
+        np.testing.assert_array_equal(got[key][0][:n], ref[key][:n], err_msg=key)
+    np.testing.assert_allclose(got["scores"][0][:n], ref["scores"][:n], rtol=0, atol=1e-5)
+    print(f"[tree] table overflow: truncated, {n} pops identical", flush=True)
+
+
 def test_marg_integer_logit_ties_on_gpu():
     # Marg over rows with repeated logit values: siblings tie exactly (slot order
     # decides) and so do their children across parents (insertion order decides);
