@@ -33,6 +33,8 @@
 #include "dt_select.h"
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 namespace dt {
 
 namespace {
@@ -1162,28 +1164,38 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
                    make_float4(acc[0], acc[1], acc[2], acc[3]));
       }
     }
-    for (int rt = (nocorr || HEAD) ? RT : wave; rt < RT; rt += NW) {
-      const int m = rt * 16 + (lane & 15);
-      const int c = lane & 15, kq = (lane >> 4) * 4;
-      const float *urow = a.U_all + (size_t)(m < M ? ccand[m] : 0) * dh + member * UW;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int q = 0; q < nq; ++q) {
-        float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (a.use_us)
-          av = *reinterpret_cast<const float4 *>(Us + m * UW + q * 16 + kq);  // slots >= M: row 0, unused
-        else if (m < M)
-          av = *reinterpret_cast<const float4 *>(urow + q * 16 + kq);
-        const float4 bv = *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+    // (two instances of the loop, the U rows from the LDS slice or from
+    // memory: one load instruction serving both would be a flat load, whose
+    // wait also waits for the state stores just issued)
+    auto corr_tiles = [&](auto from_lds) {
+      constexpr bool LDSU = decltype(from_lds)::value;
+      for (int rt = (nocorr || HEAD) ? RT : wave; rt < RT; rt += NW) {
+        const int m = rt * 16 + (lane & 15);
+        const int c = lane & 15, kq = (lane >> 4) * 4;
+        const float *urow = a.U_all + (size_t)(m < M ? ccand[m] : 0) * dh + member * UW;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < nq; ++q) {
+          float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
+          if constexpr (LDSU)
+            av = *reinterpret_cast<const float4 *>(Us + m * UW + q * 16 + kq);  // slots >= M: row 0, unused
+          else if (m < M)
+            av = *reinterpret_cast<const float4 *>(urow + q * 16 + kq);
+          const float4 bv = *reinterpret_cast<const float4 *>(Sn + c * UW + q * 16 + kq);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+        }
+        // lane l, register i: slot rt*16 + (l/16)*4 + i, node l%16
+        if (c < nc)
+          st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
+                   make_float4(acc[0], acc[1], acc[2], acc[3]));
       }
-      // lane l, register i: slot rt*16 + (l/16)*4 + i, node l%16
-      if (c < nc)
-        st_dev16(rmy, (c * MP + rt * 16 + (lane >> 4) * 4) * 4,
-                 make_float4(acc[0], acc[1], acc[2], acc[3]));
-    }
+    };
+    if (a.use_us)
+      corr_tiles(std::true_type{});
+    else
+      corr_tiles(std::false_type{});
     if (!nocorr) group_barrier(ctr, G, nbar, &scal[S_STATUS], a.spin_limit);
     if (scal[S_STATUS] & DT_TREE_TIMEOUT) return;  // (uniform: read after the barrier)
     // 3. children of each node: normalise, rank, keep the top-k above vB
