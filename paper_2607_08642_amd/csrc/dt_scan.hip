@@ -679,7 +679,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 // its own candidates into it when they gather -- no block barrier while the
 // segment streams, so a wave that merges does not hold up the other waves'
 // loads.  A candidate must beat a lower bound on the segment's M-th key:
-//   * the first batch's bound tb (as above; the one block barrier), ties kept;
+//   * the bound tb of the first two batches (as above, over the lane maxima of
+//     both; the one block barrier), ties kept.  Drawn from twice the elements,
+//     it admits about 40% fewer candidates over an eight-batch segment of
+//     Gaussian-like logits than the first batch's alone;
 //   * the wave's own list's M-th value, strictly: the wave's later elements
 //     have larger indices, so they lose ties with its own list.
 // Both depend on nothing but the data, so the candidates, the merges and the
@@ -688,8 +691,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 // rows of 151936 bf16 logits -- but made the candidates, and with them the
 // tails' rounding, depend on timing; reading them two batches late, waiting
 // for them, gained nothing over the own bound.)
-// A wave merges whenever a few dozen candidates have gathered, so that its
-// bound rises early.  The region holds (index, value bits) pairs; the keys
+// A wave merges once 48 candidates have gathered (fewer merges than at 32,
+// with the bound from two batches rising early enough).  The region holds (index, value bits) pairs; the keys
 // are formed in the merge.
 // The four wave lists meet once, at the end of the segment.  A wave whose
 // candidates overflow its region re-reads the batch and merges as it goes;
@@ -768,20 +771,31 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   int lb = tid * EPL;
   asm volatile("" : "+v"(lb));
   Raw<T> ra, rb, rc;
+  const bool two = nbat > 1;
   load_batch_vec<T>(ra, segr, 0);
+  if (two) load_batch_vec<T>(rb, segr, 1);
   if (tid == 0) flag = 0;
 
-  // ---- the first batch's lower bound tb (every wave: the ceil(M/4)-th largest
-  // of its lane maxima; the minimum over the waves) and its maximum
-  {
-    const int bn0 = min(kScanChunk, seg_n);
-    if (bn0 < kScanChunk) pad_batch<T>(ra, bn0);
-  }
+  // ---- the first two batches' lower bound tb (every wave: the ceil(M/4)-th
+  // largest of its lane maxima; the minimum over the waves) and their maximum.
+  // (Two batches rather than one: the bound then admits about half as many
+  // candidates over a segment of eight batches, and every candidate costs an
+  // append and a share of a merge.)
+  const int bn0 = min(kScanChunk, seg_n);
+  if (bn0 < kScanChunk) pad_batch<T>(ra, bn0);
   float tmax = NINF;
 #pragma unroll
   for (int j = 0; j < NL; ++j)
 #pragma unroll
     for (int e = 0; e < EPL; ++e) tmax = fmaxf(tmax, elem<T>(ra, j, e));
+  if (two) {
+    const int bn1 = min(kScanChunk, seg_n - kScanChunk);
+    if (bn1 < kScanChunk) pad_batch<T>(rb, bn1);
+#pragma unroll
+    for (int j = 0; j < NL; ++j)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) tmax = fmaxf(tmax, elem<T>(rb, j, e));
+  }
   {
     const int q = (M + kWaves - 1) / kWaves;
     const uint32_t code = ordered_bits(tmax);
@@ -798,8 +812,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
     }
   }
   __syncthreads();
-  // the next batches (issued after the barrier, which would wait for them)
-  load_batch_vec<T>(rb, segr, 1);
+  // the batch after them (issued after the barrier, which would wait for it)
   if constexpr (kBufs == 3) load_batch_vec<T>(rc, segr, 2);
   float tb = wthr[0], mx = wmax[0];
 #pragma unroll
@@ -815,7 +828,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   uint64_t list = 0ull;   // this wave's best keys (0: empty)
   float v_own = NINF;     // its M-th value once it holds M keys
   int wpos = 0;           // candidates in the region (wave-uniform)
-  const int kMergeTrig = M < 16 ? 2 * M : 32;
+  const int kMergeTrig = M < 16 ? 2 * M : 48;
   uint64_t *region = regions + w * kWaveRegion;
 
   auto after_merge = [&]() {
