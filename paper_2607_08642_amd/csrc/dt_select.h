@@ -411,11 +411,13 @@ __device__ inline uint64_t bitonic_clean64(uint64_t v, bool desc) {
 }
 
 // the better half of a descending list a and an ascending list b, sorted in
-// direction desc; the worse half joins the lane's tail (empty slots add nothing)
+// direction desc; the worse half joins the lane's tail (empty slots add
+// nothing: -inf, whose term is 0 against any reference the tail can hold --
+// the least being -FLT_MAX, against which -FLT_MAX itself would add 1)
 __device__ inline uint64_t merge_halves(uint64_t a, uint64_t b, bool desc, Tail &t, float c) {
   const bool ga = a > b;
   const uint64_t hi = ga ? a : b, lo = ga ? b : a;
-  tail_add1(t, lo ? key_value(lo) : -3.402823466e38f, c);
+  tail_add1(t, lo ? key_value(lo) : -__builtin_huge_valf(), c);
   return bitonic_clean64(hi, desc);
 }
 

@@ -135,3 +135,24 @@ def test_scan_streaming_segments(dtype, V):
     rows = list(range(0, 14)) + list(range(500, 507)) + [1099]
     _check(x, dtype, 64, 0.8, rows=rows, case=f"streaming {dtype}")
     _check(x, dtype, 200, 0.0, rows=rows[:7], case=f"streaming M=200 {dtype}")
+
+
+@pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16])
+def test_scan_neg_inf_prefixes(dtype):
+    # Segments of four batches (1100 rows of 30760) whose first batch, or first
+    # two batches, hold no finite value: the first bound then comes from the
+    # second batch alone, or from neither (every element of the first batch is
+    # taken as a candidate and the finite ones arrive through overflowing
+    # regions later); and rows with fewer finite values than M.
+    V = 30720 + 40
+    x = (np.random.default_rng(5).standard_normal((1100, V)) * 2).astype(np.float32)
+    kinds = np.arange(1100) % 5
+    x[kinds == 1, :10240] = -np.inf
+    x[kinds == 2, : 20480 + 100] = -np.inf
+    x[kinds == 3, : V - 20] = -np.inf
+    x[kinds == 4, 10240:20480] = -np.inf
+    if dtype == synth.DT_BF16:
+        x = synth.f32_to_bf16_bits(x)
+    rows = list(range(0, 10)) + [1095, 1096, 1097, 1098, 1099]
+    _check(x, dtype, 64, 0.8, rows=rows, case=f"-inf prefixes {dtype}")
+    _check(x, dtype, 32, 0.0, rows=rows[:5], case=f"-inf prefixes M=32 {dtype}")
