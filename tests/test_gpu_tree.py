@@ -136,6 +136,30 @@ def test_nonfinite_tree_isolated():
     assert got["status"][0] == 0 and got["status"][2] == 0
 
 
+def _masked(seed, dtype):
+    # vocabulary masks: rows whose finite logits number fewer than M (dead
+    # candidate slots with id -1), a row with one finite logit, and rows with
+    # fewer finite logits than B
+    wl = synth.random_small(seed, batch=3, L=5, V=700, M=16, B=12, T=0.8, d_e=48, d_h=32,
+                            dtype=dtype)
+    x = synth.bf16_bits_to_f32(wl.logits) if dtype == synth.DT_BF16 else wl.logits.copy()
+    rng = np.random.default_rng(seed)
+    for t, r, n in ((0, 1, 5), (1, 0, 1), (1, 3, 6), (2, 2, 9), (2, 4, 3)):
+        row = np.full(700, -np.inf, np.float32)
+        idx = rng.choice(700, size=n, replace=False)
+        row[idx] = x[t, r, idx]
+        x[t, r] = row
+    wl.logits = synth.f32_to_bf16_bits(x) if dtype == synth.DT_BF16 else x
+    return wl
+
+
+@pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16], ids=["f32", "bf16"])
+def test_masked_rows(dtype):
+    wl = _masked(31 + dtype, dtype)
+    kinds, got = run_case(wl, name=f"masked {dtype}")
+    assert all(int(s) == 0 for s in got["status"][: wl.batch])
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
