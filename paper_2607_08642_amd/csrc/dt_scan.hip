@@ -317,7 +317,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
   constexpr float NINF = -__builtin_huge_valf();
   __shared__ ScanLDS sh;
   __shared__ uint64_t list[2][kMaxM];
-  __shared__ float wthr[kWaves], wmax[kWaves];
+  __shared__ float wthr[kWaves];
   if constexpr (!std::is_void<TWP>::value) {
     if ((int)blockIdx.x >= g.nchunks) {
       head_proj_tile<TWP>(hp, g.rows, blockIdx.y * hp.extra + blockIdx.x - g.nchunks,
@@ -468,13 +468,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
     nl = nc + nl < M ? nc + nl : M;
   };
 
-  // after a merge: the threshold and the tail reference follow the list
+  // after a merge: the threshold and the tail reference follow the list's M-th
+  // value (later tail elements lie at or below it)
   auto after_merge = [&]() {
     if (nl == M) thr = fmaxf(thr, key_value(list[cur][M - 1]));
-    const float top = nl ? key_value(list[cur][0]) : NINF;
-    if (top > tail.m) {
-      tail.s *= sel::fast_exp2((tail.m - top) * c);
-      tail.m = top;
+    if (thr > tail.m) {
+      tail.s *= sel::fast_exp2((tail.m - thr) * c);
+      tail.m = thr;
     }
     wbase = 0;
   };
@@ -510,20 +510,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
         const uint32_t cand = pre | (1u << bit);
         if (__popcll(__ballot(code >= cand)) >= q) pre = cand;
       }
-      const float wm = sel::wave_reduce(tmax, [](float x, float y) { return fmaxf(x, y); });
-      if (lane == 0) {
-        wthr[w] = ordered_to_float(pre);
-        wmax[w] = wm;
-      }
+      if (lane == 0) wthr[w] = ordered_to_float(pre);
       __syncthreads();
       thr = wthr[0];
-      float mx = wmax[0];
 #pragma unroll
-      for (int i = 1; i < kWaves; ++i) {
-        thr = fminf(thr, wthr[i]);
-        mx = fmaxf(mx, wmax[i]);
-      }
-      tail.m = fmaxf(mx, -3.402823466e38f);
+      for (int i = 1; i < kWaves; ++i) thr = fminf(thr, wthr[i]);
+      // (the tail's reference follows the threshold, at or above every element
+      // the tail takes, not the maximum: see the wave kernel)
+      tail.m = fmaxf(thr, -3.402823466e38f);
     }
     // Candidate test: the first batch keeps ties with its lower bound; later
     // elements must beat the list's M-th value (they lose ties on the index).
@@ -745,7 +739,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   constexpr int kWaveRegion = WaveScan<T>::kRegion;
   __shared__ alignas(16) uint64_t regions[kWaves * kWaveRegion];
   __shared__ uint64_t wl[kWaves][64];
-  __shared__ float wthr[kWaves], wmax[kWaves];
+  __shared__ float wthr[kWaves];
   __shared__ float2 red[kWaves];
   __shared__ int flag;
   static_assert(kWaves * kWaveRegion * 8 >= kWaves * 256 * 4, "projection partials fit the regions");
@@ -777,7 +771,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   if (tid == 0) flag = 0;
 
   // ---- the first two batches' lower bound tb (every wave: the ceil(M/4)-th
-  // largest of its lane maxima; the minimum over the waves) and their maximum.
+  // largest of its lane maxima; the minimum over the waves).
   // (Two batches rather than one: the bound then admits about half as many
   // candidates over a segment of eight batches, and every candidate costs an
   // append and a share of a merge.)
@@ -805,25 +799,22 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
       const uint32_t cand = pre | (1u << bit);
       if (__popcll(__ballot(code >= cand)) >= q) pre = cand;
     }
-    const float wm = sel::wave_reduce(tmax, [](float x, float y) { return fmaxf(x, y); });
-    if (lane == 0) {
-      wthr[w] = ordered_to_float(pre);
-      wmax[w] = wm;
-    }
+    if (lane == 0) wthr[w] = ordered_to_float(pre);
   }
   __syncthreads();
   // the batch after them (issued after the barrier, which would wait for it)
   if constexpr (kBufs == 3) load_batch_vec<T>(rc, segr, 2);
-  float tb = wthr[0], mx = wmax[0];
+  float tb = wthr[0];
 #pragma unroll
-  for (int i = 1; i < kWaves; ++i) {
-    tb = fminf(tb, wthr[i]);
-    mx = fmaxf(mx, wmax[i]);
-  }
+  for (int i = 1; i < kWaves; ++i) tb = fminf(tb, wthr[i]);
   const bool all_in = !(tb > NINF);
   const float tlow = all_in ? NINF : below(tb);
+  // The tail's reference follows the bound, which every element the tail
+  // takes lies at or below, not the segment's maximum: at a small
+  // temperature (c large) the tail's terms against the maximum of the
+  // candidates would all underflow.
   Tail tail = sel::tail_empty();
-  tail.m = fmaxf(mx, -3.402823466e38f);
+  tail.m = fmaxf(tlow, -3.402823466e38f);
 
   uint64_t list = 0ull;   // this wave's best keys (0: empty)
   float v_own = NINF;     // its M-th value once it holds M keys

@@ -43,10 +43,20 @@ def test_scan_tiny_fp32():
     _check(wl.logits[0], synth.DT_F32, 8, 0.0, case="tiny")
 
 
-@pytest.mark.parametrize("T", [0.0, 1.0, 0.7])
+@pytest.mark.parametrize("T", [0.0, 1.0, 0.7, 0.05, 4.0])
 def test_scan_qwen_rows_bf16(T):
     x = synth.peaked_logits(2, 0, 16, synth.QWEN3_VOCAB, synth.DT_BF16, 1, 4, 6.0, 12.0)
     _check(x, synth.DT_BF16, 64, T, case="qwen16")
+
+
+@pytest.mark.parametrize("T", [0.05, 4.0])
+def test_scan_block_kernel_temperatures(T):
+    # rows of an odd length (4-byte loads: the block kernel), M above and below
+    # 64, at a small temperature (exponents far below the row maximum) and a
+    # large one
+    x = synth.peaked_logits(3, 0, 8, 20001, synth.DT_F32, 1, 4, 6.0, 12.0)
+    _check(x, synth.DT_F32, 100, T, case=f"block M=100 T={T}")
+    _check(x, synth.DT_F32, 32, T, case=f"block M=32 T={T}")
 
 
 def test_scan_concurrent_rows_sampled():

@@ -160,6 +160,15 @@ def test_masked_rows(dtype):
     assert all(int(s) == 0 for s in got["status"][: wl.batch])
 
 
+@pytest.mark.parametrize("T", [0.1, 3.0])
+def test_extreme_temperatures(T):
+    # sharp and flat menus: exponent arguments far from the row maxima (the
+    # scan's two exponent forms, the children's normalisation)
+    wl = synth.random_small(41, batch=2, L=5, V=900, M=24, B=16, T=T, d_e=48, d_h=32,
+                            dtype=synth.DT_BF16, h0=True)
+    run_case(wl, name=f"T={T}")
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
