@@ -624,7 +624,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // all waves on each of this member's rows
     for (int d = member; d < L; d += G) {
       const int row = t * L + d;
-      sel::merge_row_tree<true, NT>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+      sel::merge_row_tree<true, NT, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
                                     a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
                                     a.c2, a.inv_tau, sortbuf, red, a.cand + (size_t)row * M,
                                     a.candv + (size_t)row * M, a.tailR + row, a.rflag + row, a.c_all);
@@ -633,7 +633,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
     // one wave per row (a single merge): rows member + G * (wave + NW * i)
     for (int d = member + G * wave; d < L; d += G * NW) {
       const int row = t * L + d;
-      sel::merge_row_wave<true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+      sel::merge_row_wave<true, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
                                 a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
                                 a.c2, a.inv_tau, a.cand + (size_t)row * M, a.candv + (size_t)row * M,
                                 a.tailR + row, a.rflag + row, a.c_all);
@@ -641,7 +641,7 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
   } else {
     for (int d = member; d < L; d += G) {
       const int row = t * L + d;
-      sel::merge_row<NT, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
+      sel::merge_row<NT, true, true>(a.ckeys + (size_t)row * a.nchunks * M, a.nchunks, M,
                                a.ctail + (size_t)row * a.nchunks, a.cflag + (size_t)row * a.nchunks,
                                a.c2, a.inv_tau, sortbuf, red, &scal[S_MERGEFLAG],
                                a.cand + (size_t)row * M, a.candv + (size_t)row * M, a.tailR + row,

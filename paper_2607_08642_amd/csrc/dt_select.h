@@ -20,6 +20,14 @@ __device__ inline Tail tail_empty() { return Tail{-3.402823466e38f, 0.0f}; }
 // which a sum of exponentials relative to its running max can ignore
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// SHIFT: the row's candidate values and R are written less the row's largest
+// value s0 (R less s0 / tau), which changes no log-probability (a constant
+// per row) but keeps the consumer's sums of a value and a correction at the
+// magnitude of their difference: logits offset by thousands would otherwise
+// leave fp32 ulps of 1e-4 in every score.  (s0 = 0 for a row whose largest
+// value is not finite.)
+__device__ inline float row_shift(float top) { return __builtin_isfinite(top) ? top : 0.0f; }
+
 template <int N>
 __device__ inline void tail_add_group(Tail &t, const float (&x)[N], float c) {
   float mx = t.m;
@@ -162,7 +170,7 @@ __host__ __device__ inline int merge_buf_bytes(int nlists, int M) { return merge
 // buf: merge_buf_bytes(nlists, M) bytes of LDS; red: NT/64 float2.
 // DEV_SCOPE selects device-scope stores (results read by other workgroups).
 // vadd (nullable): candv[m] = logit + vadd[cand[m]] instead of the logit.
-template <int NT, bool DEV_SCOPE>
+template <int NT, bool DEV_SCOPE, bool SHIFT = false>
 __device__ __attribute__((always_inline)) void merge_row(const uint64_t *lists, int nlists, int M, const float2 *tails,
                           const int32_t *flags, float c, float inv_tau, uint64_t *buf,
                           float2 *red, int *flag_lds, int32_t *cand, float *candv, float *tailR,
@@ -339,13 +347,16 @@ __device__ __attribute__((always_inline)) void merge_row(const uint64_t *lists, 
     if (k >= thr) tail_add1(t, key_value(k), c);  // thr >= 1: empty slots stay out
   }
   t = block_tail<NT>(t, c, red);
+  const float s0 = SHIFT && top[0] ? row_shift(key_value(top[0])) : 0.0f;
   for (int i = tid; i < M; i += NT) {
     const uint64_t k = top[i];
     put<DEV_SCOPE>(cand + i, k ? (int32_t)key_index(k) : (int32_t)-1);
-    put<DEV_SCOPE>(candv + i, k ? topv[i] : -__builtin_huge_valf());
+    float v = k ? topv[i] : -__builtin_huge_valf();
+    if (SHIFT && k) v = (key_value(k) - s0) + (vadd ? vadd[key_index(k)] : 0.0f);
+    put<DEV_SCOPE>(candv + i, v);
   }
   if (tid == 0) {
-    put<DEV_SCOPE>(tailR, t.s > 0.0f ? t.m * inv_tau + logf(t.s) : -__builtin_huge_valf());
+    put<DEV_SCOPE>(tailR, t.s > 0.0f ? (t.m - s0) * inv_tau + logf(t.s) : -__builtin_huge_valf());
     put<DEV_SCOPE>(rflag, (int32_t)(*flag_lds ? DT_TREE_NONFINITE : 0));
   }
   __syncthreads();
@@ -452,7 +463,7 @@ __host__ __device__ inline bool wave_merge_fits(int nlists, int M) {
 
 // The same results as merge_row (the row's M best keys, R over the rest, the
 // row flag), computed by the calling wave alone; wave_merge_fits must hold.
-template <bool DEV_SCOPE>
+template <bool DEV_SCOPE, bool SHIFT = false>
 __device__ __attribute__((always_inline)) void merge_row_wave(
     const uint64_t *lists, int nlists, int M, const float2 *tails, const int32_t *flags, float c,
     float inv_tau, int32_t *cand, float *candv, float *tailR, int32_t *rflag, const float *vadd) {
@@ -496,12 +507,13 @@ __device__ __attribute__((always_inline)) void merge_row_wave(
   const float sum = wave_reduce(t.s > 0.0f ? t.s * fast_exp2((t.m - m) * c) : 0.0f,
                                 [](float x, float y) { return x + y; });
   const bool any_bad = __ballot(bad != 0) != 0ull;
+  const float s0 = SHIFT ? row_shift(readlane_f(top ? key_value(top) : 0.0f, 0)) : 0.0f;
   if (lane < M) {
     put<DEV_SCOPE>(cand + lane, keep ? (int32_t)key_index(top) : (int32_t)-1);
-    put<DEV_SCOPE>(candv + lane, keep ? key_value(top) + va : -__builtin_huge_valf());
+    put<DEV_SCOPE>(candv + lane, keep ? (key_value(top) - s0) + va : -__builtin_huge_valf());
   }
   if (lane == 0) {
-    put<DEV_SCOPE>(tailR, sum > 0.0f ? m * inv_tau + logf(sum) : -__builtin_huge_valf());
+    put<DEV_SCOPE>(tailR, sum > 0.0f ? (m - s0) * inv_tau + logf(sum) : -__builtin_huge_valf());
     put<DEV_SCOPE>(rflag, (int32_t)(any_bad ? DT_TREE_NONFINITE : 0));
   }
 }
@@ -509,7 +521,7 @@ __device__ __attribute__((always_inline)) void merge_row_wave(
 // The same merge spread over the NT / 64 waves of a workgroup (every thread
 // calls it): wave w merges lists 2w and 2w + 1, then the tree's levels meet in
 // LDS (xbuf: NT keys), one barrier each; the tails combine as in block_tail.
-template <bool DEV_SCOPE, int NT>
+template <bool DEV_SCOPE, int NT, bool SHIFT = false>
 __device__ __attribute__((always_inline)) void merge_row_tree(
     const uint64_t *lists, int nlists, int M, const float2 *tails, const int32_t *flags, float c,
     float inv_tau, uint64_t *xbuf, float2 *red, int32_t *cand, float *candv, float *tailR,
@@ -555,12 +567,13 @@ __device__ __attribute__((always_inline)) void merge_row_tree(
   const bool any_bad = __ballot(bad != 0) != 0ull;  // (wave 0 holds the flags)
   t = block_tail<NT>(t, c, red);
   if (wave == 0) {
+    const float s0 = SHIFT ? row_shift(readlane_f(v ? key_value(v) : 0.0f, 0)) : 0.0f;
     if (lane < M) {
       put<DEV_SCOPE>(cand + lane, keep ? (int32_t)key_index(v) : (int32_t)-1);
-      put<DEV_SCOPE>(candv + lane, keep ? key_value(v) + va : -__builtin_huge_valf());
+      put<DEV_SCOPE>(candv + lane, keep ? (key_value(v) - s0) + va : -__builtin_huge_valf());
     }
     if (lane == 0) {
-      put<DEV_SCOPE>(tailR, t.s > 0.0f ? t.m * inv_tau + logf(t.s) : -__builtin_huge_valf());
+      put<DEV_SCOPE>(tailR, t.s > 0.0f ? (t.m - s0) * inv_tau + logf(t.s) : -__builtin_huge_valf());
       put<DEV_SCOPE>(rflag, (int32_t)(any_bad ? DT_TREE_NONFINITE : 0));
     }
   }

@@ -166,3 +166,16 @@ def test_scan_neg_inf_prefixes(dtype):
     rows = list(range(0, 10)) + [1095, 1096, 1097, 1098, 1099]
     _check(x, dtype, 64, 0.8, rows=rows, case=f"-inf prefixes {dtype}")
     _check(x, dtype, 32, 0.0, rows=rows[:5], case=f"-inf prefixes M=32 {dtype}")
+
+
+@pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16])
+def test_scan_large_magnitudes(dtype):
+    # logits far from zero (an offset of 5000, a spread of hundreds): the
+    # exponent's fma form does not apply (|m c| > 128), and the bf16 rows (a
+    # spacing of 32 at 5000) are full of exact ties
+    x = synth.peaked_logits(4, 0, 8, 30720 + 40, synth.DT_F32, 1, 4, 6.0, 12.0) * 150.0 + 5000.0
+    x = x.astype(np.float32)
+    if dtype == synth.DT_BF16:
+        x = synth.f32_to_bf16_bits(x)
+    _check(x, dtype, 64, 1.0, case=f"large {dtype}")
+    _check(x, dtype, 64, 40.0, case=f"large T=40 {dtype}")

@@ -169,6 +169,14 @@ def test_extreme_temperatures(T):
     run_case(wl, name=f"T={T}")
 
 
+def test_shifted_logits():
+    # a constant added to every logit changes no log-probability: the tree of
+    # logits offset by 3000 (fp32) is the oracle's tree of those logits
+    wl = synth.random_small(43, batch=2, L=5, V=900, M=24, B=16, T=0.8, d_e=48, d_h=32, h0=True)
+    wl.logits = (wl.logits + np.float32(3000.0)).astype(np.float32)
+    run_case(wl, name="shifted")
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
