@@ -177,6 +177,16 @@ def test_shifted_logits():
     run_case(wl, name="shifted")
 
 
+@pytest.mark.parametrize("L,M,B", [(2, 4, 30), (1, 5, 12), (3, 3, 64)])
+def test_budget_beyond_reachable_nodes(L, M, B):
+    # every node the depth limit and the menus allow (M + M^2 + ... < B) is in
+    # the tree, which ends short of B
+    wl = synth.random_small(51, batch=2, L=L, V=200, M=M, B=B, T=0.9, d_e=32, d_h=32)
+    kinds, got = run_case(wl, name=f"short L={L} M={M} B={B}")
+    reach = sum(M ** d for d in range(1, L + 1))
+    assert all(int(n) == reach for n in got["n_nodes"][: wl.batch])
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
