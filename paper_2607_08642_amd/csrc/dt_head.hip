@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kHT) void head_tree_kernel(HeadArgs a) {
   // ---- Alg. 1 step 1: this tree's rows, one wave per row ---------------------
   for (int d = wave; d < L; d += kHT / 64) {
     const size_t row = (size_t)t * L + d;
-    sel::merge_row_wave<false>(a.ckeys + row * a.nchunks * M, a.nchunks, M,
+    sel::merge_row_wave<false, true>(a.ckeys + row * a.nchunks * M, a.nchunks, M,
                                a.ctail + row * a.nchunks, a.cflag + row * a.nchunks, a.c2,
                                a.inv_tau, rc + 64 * d, rv + 64 * d, rt + d, rf + d, nullptr);
   }

@@ -147,6 +147,23 @@ def test_head_deep_concurrent_sampled():
     assert sum(k == "exact" for k, _ in kinds) >= 4, kinds
 
 
+@pytest.mark.parametrize("rank,d_h", [(32, 32), (256, 64)], ids=["expansion-kernel", "head-kernel"])
+def test_head_shifted_and_masked_logits(rank, d_h):
+    # logits offset by 3000 (fp32) with vocabulary-masked rows (fewer finite
+    # logits than M), on both kernels that build head trees
+    wl = synth.random_small(61, batch=2, L=4, V=400, M=16, B=12, T=0.8, d_e=48, d_h=d_h)
+    x = wl.logits.copy()
+    rng = np.random.default_rng(61)
+    for t, r, n in ((0, 1, 5), (1, 2, 3)):
+        row = np.full(400, -np.inf, np.float32)
+        idx = rng.choice(400, size=n, replace=False)
+        row[idx] = x[t, r, idx]
+        x[t, r] = row
+    wl.logits = (x + np.float32(3000.0)).astype(np.float32)
+    with_head(wl, 61, 64, rank)
+    run_head(wl, f"shifted head rank {rank}")
+
+
 def test_head_argument_errors():
     wl = synth.random_small(44, batch=1, L=3, V=300, M=8, B=8, T=0.0, d_e=32, d_h=32)
     with_head(wl, 44, 32, 16)
