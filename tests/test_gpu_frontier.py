@@ -57,6 +57,26 @@ def test_frontier_small(case, W):
                     np.testing.assert_array_equal(got[key][t], ref[key], err_msg=f"{t} {key}")
 
 
+@pytest.mark.parametrize("W", [1, 3])
+def test_frontier_masked_rows_and_short_budget(W):
+    # vocabulary-masked rows (fewer finite logits than M, one row with a
+    # single finite logit), and a budget the frontier cannot fill (L = 2, M = 4)
+    wl = synth.random_small(71, batch=2, L=5, V=600, M=16, B=12, T=0.8, d_e=48, d_h=32)
+    x = wl.logits.copy()
+    rng = np.random.default_rng(71)
+    for t, r, n in ((0, 1, 5), (1, 0, 1), (1, 2, 4)):
+        row = np.full(600, -np.inf, np.float32)
+        idx = rng.choice(600, size=n, replace=False)
+        row[idx] = x[t, r, idx]
+        x[t, r] = row
+    wl.logits = x
+    run_frontier(wl, W, "masked")
+    wl = synth.random_small(72, batch=2, L=2, V=200, M=4, B=30, T=0.9, d_e=32, d_h=32)
+    kinds, got = run_frontier(wl, W, "short")
+    for t in range(wl.batch):
+        assert int(got["n_nodes"][t]) == run_oracle(wl, t, frontier_width=W)["n_nodes"] < 30
+
+
 @pytest.mark.parametrize("scorer", [1, 2], ids=["marg", "static"])
 def test_frontier_ablation_arms(scorer):
     wl = synth.random_small(2, batch=3, L=6, V=500, M=16, B=24, T=0.7, d_e=64, d_h=64, h0=True)
