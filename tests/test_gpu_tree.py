@@ -187,6 +187,16 @@ def test_budget_beyond_reachable_nodes(L, M, B):
     assert all(int(n) == reach for n in got["n_nodes"][: wl.batch])
 
 
+@pytest.mark.parametrize("batch,d_h", [(100, 64), (300, 32)])
+def test_many_trees_per_call(batch, d_h):
+    # more trees than XCD classes hold at once: 100 trees of two members each
+    # (13 per class, start-order member slots) and 300 one-member trees (more
+    # workgroups than CUs)
+    wl = synth.random_small(81, batch=batch, L=4, V=300, M=8, B=10, T=0.8, d_e=32, d_h=d_h,
+                            h0=True)
+    run_case(wl, name=f"batch {batch}")
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
