@@ -269,6 +269,14 @@ def test_deep_concurrent_all_trees():
     assert int(got["depth"].max()) >= 12
 
 
+def test_deep_qwen_shape_100_trees_sampled():
+    # 100 deep Qwen3-8B-shaped trees in one call: two members per tree on the
+    # generic instance (d_h 512 split in halves), 13 trees per XCD class
+    wl = synth.deep_concurrent(batch=100)
+    kinds, got = run_case(wl, trees=[0, 1, 49, 98, 99], name="deep x100", tol=QWEN_TOL)
+    assert all(int(s) == 0 for s in got["status"][:100])
+
+
 def test_twin_ties_at_qwen_shape():
     # every near-tie of this tree is an exact structural tie (twin tokens): the
     # GPU must order them by the heap's insertion order, node for node
