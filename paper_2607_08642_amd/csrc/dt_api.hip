@@ -234,16 +234,18 @@ dt_status dt_plan_create_from_model(dt_plan **plan, dt_model *model, int L, int 
     return fail(DT_ERR_SHAPE, "the model lives on device %d, the current device is %d", model->device, dev);
   if (nxcd < 1 || nxcd > dt::kMaxXcd)
     return fail(DT_ERR_UNSUPPORTED, "device reports %d XCDs; 1 to %d are supported", nxcd, dt::kMaxXcd);
-  const int nchunks = dt::scan_geom(1, V, M).nchunks;
   if (dt::merge_lds_bytes(dt::scan_geom(1, V, M)) > (size_t)dt::kMergeLdsMax)
     return fail(DT_ERR_UNSUPPORTED, "the row merge of V and M needs %zu bytes of LDS, more than %d",
                 dt::merge_lds_bytes(dt::scan_geom(1, V, M)), dt::kMergeLdsMax);
-  // the expansion's LDS for every group size a batch in [1, max_batch] can use
+  // the expansion's LDS at the group size of every batch in [1, max_batch]
+  // (the group shrinks until its layout fits; only one member per tree can
+  // still be too large)
   size_t lds_need = 0;
-  for (int G = dt::expand_group_size(d_h, ncu, nxcd, max_batch);; G *= 2) {
-    const size_t b = dt::expand_lds_bytes(d_h, G, M, nchunks, L);
-    lds_need = b > lds_need ? b : lds_need;
-    if (G == dt::expand_group_size(d_h, ncu, nxcd, 1)) break;
+  for (int b = 1; b <= max_batch; ++b) {
+    const int nb = dt::scan_geom(b * L, V, M).nchunks;
+    const int G = dt::expand_group_size(d_h, ncu, nxcd, b, M, L, nb, (size_t)maxlds);
+    const size_t need = dt::expand_lds_bytes(d_h, G, M, nb, L);
+    lds_need = need > lds_need ? need : lds_need;
   }
   if (lds_need > (size_t)maxlds)
     return fail(DT_ERR_UNSUPPORTED,
@@ -282,6 +284,7 @@ dt_status dt_plan_create_from_model(dt_plan **plan, dt_model *model, int L, int 
   p->max_batch = max_batch;
   p->num_cus = ncu;
   p->num_xcd = nxcd;
+  p->max_lds = (size_t)maxlds;
   p->frontier_w = o.frontier_width;
   p->spin_limit = o.debug_spin_limit;
   p->device = dev;
@@ -571,7 +574,7 @@ dt_status dt_scan_topm(const void *logits, int rows, int V, int logits_dtype, in
 // [j rank / G, (j + 1) rank / G).  Returns G, or 0 when the shape is outside
 // that kernel's envelope and the one-workgroup head kernel builds the tree.
 static int head_fast_group(const dt_plan *p, int batch, const dt_domino_head *hd, int maxlds) {
-  const int G = dt::expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch);
+  const int G = dt::expand_group_size(p, batch);
   if (hd->rank % (16 * G) != 0) return 0;
   const int rj = hd->rank / G;
   if (rj != 16 && rj != 32 && rj != 64) return 0;  // whole MFMA tiles; 64 % (lanes per W_2 row) == 0

@@ -1899,14 +1899,22 @@ __global__ __launch_bounds__(NT) void expand_kernel(ExpArgs a) {
 
 }  // namespace
 
-int expand_group_size(int d_h, int num_cus, int num_xcd, int batch) {
-  // largest power-of-two group (<= 16, >= 32 units per member) whose grid
-  // (every XCD holding the same number of tree slots) fits one workgroup per CU
+int expand_group_size(int d_h, int num_cus, int num_xcd, int batch, int M, int L, int nchunks,
+                      size_t max_lds) {
+  // (a smaller group can need less LDS: fewer units per member than 128 take
+  // a 24 KB block for the gates' k-split partial sums; d_h 768 and 1024 fit
+  // at 8 members, not at 16)
   int G = 16;
   while (G > 1 && (d_h / G < 32 || (d_h / G) % 16 != 0 ||
-                   num_xcd * G * ((batch + num_xcd - 1) / num_xcd) > num_cus))
+                   num_xcd * G * ((batch + num_xcd - 1) / num_xcd) > num_cus ||
+                   expand_lds_bytes(d_h, G, M, nchunks, L) > max_lds))
     G >>= 1;
   return G;
+}
+
+int expand_group_size(const dt_plan *p, int batch) {
+  return expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch, p->M, p->L,
+                           scan_geom(batch * p->L, p->V, p->M).nchunks, p->max_lds);
 }
 
 size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L, int rj, int wbytes) {
@@ -1914,7 +1922,7 @@ size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L, int rj, int wb
 }
 
 size_t expand_part_bytes(const dt_plan *p, int batch) {
-  const int G = expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch);
+  const int G = expand_group_size(p, batch);
   return (size_t)batch * 2 * G * CH * mp_of(p->M) * sizeof(float);
 }
 
@@ -1935,7 +1943,7 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
   a.stats = mode.stats;
   a.cost = (mode.emit && p->frontier_w == 0) ? p->cost : nullptr;
   a.dh = p->d_h;
-  a.G = expand_group_size(p->d_h, p->num_cus, p->num_xcd, batch);
+  a.G = expand_group_size(p, batch);
   a.norm_mode = p->norm_mode;
   a.pos_offset = p->pos_offset;
   a.ecap = ws.ecap;

@@ -112,6 +112,7 @@ struct dt_plan {
   const void *whh_t, *whh_rm;
   int num_cus;
   int num_xcd;              // XCDs of the device (workgroups are dealt to them round-robin)
+  size_t max_lds;           // LDS bytes a workgroup may allocate on the device
   int frontier_w;           // dt_options.frontier_width (0: the heap builder)
   int spin_limit;           // dt_options.debug_spin_limit (0: the default)
   int device;               // the device the plan was created on (its memory lives there)
@@ -214,7 +215,13 @@ hipError_t launch_expand(const dt_plan *p, int batch, const float *h0, float inv
                          const Workspace &ws, const dt_tree *out, hipStream_t s,
                          hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
                          const ExpMode &mode = ExpMode());
-int expand_group_size(int d_h, int num_cus, int num_xcd, int batch);
+// members per tree: the largest power of two (<= 16) that leaves each member a
+// multiple of 16 and at least 32 hidden units, fits the grid (every XCD holding
+// the same number of tree slots) one workgroup per CU, and whose LDS layout fits
+// max_lds
+int expand_group_size(int d_h, int num_cus, int num_xcd, int batch, int M, int L, int nchunks,
+                      size_t max_lds);
+int expand_group_size(const dt_plan *p, int batch);
 size_t expand_lds_bytes(int dh, int G, int M, int nchunks, int L, int rj = 0, int wbytes = 0);
 size_t expand_part_bytes(const dt_plan *p, int batch);
 hipError_t pack_weights(dt_model *m, const dt_gru *gru, const dt_head *head, hipStream_t s);

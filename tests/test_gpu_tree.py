@@ -197,6 +197,25 @@ def test_many_trees_per_call(batch, d_h):
     run_case(wl, name=f"batch {batch}")
 
 
+@pytest.mark.parametrize("d_h,batch", [(160, 2), (768, 1), (1024, 1), (1024, 9)])
+def test_state_widths(d_h, batch):
+    # path-state widths off the tested grid: 160 (two members of 80 units), 768
+    # and 1024 (the largest), whose sixteen-member layouts exceed the LDS: eight
+    # members of 96 and 128 units
+    wl = synth.random_small(91, batch=batch, L=5, V=600, M=16, B=14, T=0.8, d_e=64, d_h=d_h,
+                            h0=True, w_scale=0.2)
+    run_case(wl, name=f"d_h {d_h} batch {batch}")
+
+
+def test_single_candidate_rows():
+    # M = 1: every menu holds one token, so the tree is the chain of the rows' top
+    # tokens (min(B, L) nodes)
+    wl = synth.random_small(92, batch=2, L=7, V=500, M=1, B=5, T=0.8, d_e=32, d_h=32)
+    kinds, got = run_case(wl, name="M=1")
+    for t in range(2):
+        np.testing.assert_array_equal(got["parents"][t][:5], np.arange(-1, 4))
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
