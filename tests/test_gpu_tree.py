@@ -216,6 +216,21 @@ def test_single_candidate_rows():
         np.testing.assert_array_equal(got["parents"][t][:5], np.arange(-1, 4))
 
 
+def test_menus_of_the_whole_vocabulary():
+    # M = V: every token is a candidate, the tail is empty (R = -inf)
+    for norm_mode in (0, 1):
+        wl = synth.random_small(93, batch=2, L=4, V=64, M=64, B=20, T=0.9, d_e=32, d_h=32)
+        run_case(wl, name=f"M=V norm {norm_mode}", norm_mode=norm_mode)
+
+
+def test_odd_vocabulary_at_qwen_width():
+    # a vocabulary of 151937 bf16 logits (rows not 16-byte aligned: the block
+    # scan kernel, fifteen segment lists per row) at d_h = 512, M = 64
+    wl = synth.random_small(94, batch=1, L=4, V=151937, M=64, B=16, T=1.0, d_e=64, d_h=512,
+                            dtype=synth.DT_BF16, w_scale=0.1)
+    run_case(wl, name="odd V")
+
+
 def test_determinism_and_stream():
     wl = synth.random_small(24, batch=4, L=6, V=900, M=32, B=16, T=0.7, d_e=64, d_h=64,
                             dtype=synth.DT_BF16, h0=True)
