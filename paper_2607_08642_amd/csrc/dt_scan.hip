@@ -686,8 +686,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 // tails' rounding, depend on timing; reading them two batches late, waiting
 // for them, gained nothing over the own bound.)
 // A wave merges once 48 candidates have gathered (fewer merges than at 32,
-// with the bound from two batches rising early enough).  The region holds (index, value bits) pairs; the keys
-// are formed in the merge.
+// with the bound from two batches rising early enough).  The region holds
+// (index, value bits) pairs; the keys are formed in the merge.
 // The four wave lists meet once, at the end of the segment.  A wave whose
 // candidates overflow its region re-reads the batch and merges as it goes;
 // a first batch without a finite bound (mostly -inf or padding) takes every
@@ -772,7 +772,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
 
   // ---- the first two batches' lower bound tb (every wave: the ceil(M/4)-th
   // largest of its lane maxima; the minimum over the waves).
-  // (Two batches rather than one: the bound then admits about half as many
+  // (Two batches rather than one: the bound then admits about 40% fewer
   // candidates over a segment of eight batches, and every candidate costs an
   // append and a share of a merge.)
   const int bn0 = min(kScanChunk, seg_n);
