@@ -194,6 +194,21 @@ struct Elem<float> {
   static constexpr int EPL = 4;
 };
 
+// The bitwise search for a bound runs down to this bit: a bf16 value's
+// order-preserving code is set by its high 16 bits (its low 16 are 0 for a
+// value >= 0 and all ones below 0), so 16 steps of one ballot each (a serial
+// chain) find the high half of the q-th largest code, and full_code restores
+// the low half.
+template <typename T>
+constexpr int kLowBit = 0;
+template <>
+constexpr int kLowBit<uint16_t> = 16;
+template <typename T>
+__device__ inline uint32_t full_code(uint32_t pre) {
+  if constexpr (kLowBit<T> == 16) return (pre & 0x80000000u) ? pre : (pre | 0xFFFFu);
+  return pre;
+}
+
 template <typename T>
 __device__ inline float to_f32(T x);
 template <>
@@ -506,10 +521,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
       const uint32_t code = ordered_bits(tmax);
       uint32_t pre = 0;
 #pragma unroll
-      for (int bit = 31; bit >= 0; --bit) {
+      for (int bit = 31; bit >= kLowBit<T>; --bit) {
         const uint32_t cand = pre | (1u << bit);
         if (__popcll(__ballot(code >= cand)) >= q) pre = cand;
       }
+      pre = full_code<T>(pre);
       if (lane == 0) wthr[w] = ordered_to_float(pre);
       __syncthreads();
       thr = wthr[0];
@@ -795,10 +811,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
     const uint32_t code = ordered_bits(tmax);
     uint32_t pre = 0;
 #pragma unroll
-    for (int bit = 31; bit >= 0; --bit) {
+    for (int bit = 31; bit >= kLowBit<T>; --bit) {
       const uint32_t cand = pre | (1u << bit);
       if (__popcll(__ballot(code >= cand)) >= q) pre = cand;
     }
+    pre = full_code<T>(pre);
     if (lane == 0) wthr[w] = ordered_to_float(pre);
   }
   __syncthreads();

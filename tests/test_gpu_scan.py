@@ -179,3 +179,18 @@ def test_scan_large_magnitudes(dtype):
         x = synth.f32_to_bf16_bits(x)
     _check(x, dtype, 64, 1.0, case=f"large {dtype}")
     _check(x, dtype, 64, 40.0, case=f"large T=40 {dtype}")
+
+
+@pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16])
+def test_scan_waves_without_enough_finite_lanes(dtype):
+    # finite values only in the elements one wave of the first batch reads
+    # (the first 300 of each 2048), so the other waves' bound inputs are -inf:
+    # the segment's bound must then be -inf (every element a candidate), not
+    # that wave's; one- and two-batch segments, the wave and block kernels
+    rng = np.random.default_rng(9)
+    for V in (10240, 20480, 10243):
+        x = np.full((6, V), -np.inf, np.float32)
+        for j in range(0, V, 2048):
+            x[:, j : j + 300] = (rng.standard_normal((6, min(300, V - j))) * 2).astype(np.float32)
+        xd = synth.f32_to_bf16_bits(x) if dtype == synth.DT_BF16 else x
+        _check(xd, dtype, 64, 0.9, case=f"sparse waves V={V} {dtype}")
