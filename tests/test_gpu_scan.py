@@ -194,3 +194,16 @@ def test_scan_waves_without_enough_finite_lanes(dtype):
             x[:, j : j + 300] = (rng.standard_normal((6, min(300, V - j))) * 2).astype(np.float32)
         xd = synth.f32_to_bf16_bits(x) if dtype == synth.DT_BF16 else x
         _check(xd, dtype, 64, 0.9, case=f"sparse waves V={V} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", [synth.DT_F32, synth.DT_BF16])
+def test_scan_signed_zeros(dtype):
+    # -0 and +0 are one value: ties between them go to the lower id
+    x = np.zeros((3, 20480 + 64), np.float32)
+    x[:, ::2] = -0.0
+    x[0, 7] = 1.0
+    x[1, 100:140] = -1.0
+    x[2, ::3] = -np.inf
+    xd = synth.f32_to_bf16_bits(x) if dtype == synth.DT_BF16 else x
+    _check(xd, dtype, 64, 1.0, case=f"signed zeros {dtype}")
+    _check(xd, dtype, 200, 0.5, case=f"signed zeros M=200 {dtype}")
