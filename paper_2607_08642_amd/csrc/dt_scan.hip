@@ -720,8 +720,10 @@ struct WaveScan {
 
 // merge region[0..n) ((index << 32) | value bits each) into the wave's list
 // (descending keys, one per lane); keys that fall out of the best 64 join the
-// lane's tail
-__device__ inline void wave_merge(const uint64_t *region, int n, uint64_t &list, Tail &tail, float c) {
+// lane's tail.  fresh: the list is still empty, and the first 64 keys become
+// it sorted, with nothing to merge (wave-uniform; cleared here).
+__device__ inline void wave_merge(const uint64_t *region, int n, uint64_t &list, bool &fresh, Tail &tail,
+                                  float c) {
   const int lane = threadIdx.x & 63;
   for (int c0 = 0; c0 < n; c0 += 64) {
     uint64_t k = 0ull;
@@ -729,7 +731,9 @@ __device__ inline void wave_merge(const uint64_t *region, int n, uint64_t &list,
       const uint64_t e = region[c0 + lane];
       k = make_key(__uint_as_float((uint32_t)e), (uint32_t)(e >> 32));
     }
-    list = sel::merge_halves(list, sel::wave_sort64(k, false), true, tail, c);
+    const uint64_t srt = sel::wave_sort64(k, fresh);
+    list = fresh ? srt : sel::merge_halves(list, srt, true, tail, c);
+    fresh = false;
   }
 }
 
@@ -834,6 +838,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   tail.m = fmaxf(tlow, -3.402823466e38f);
 
   uint64_t list = 0ull;   // this wave's best keys (0: empty)
+  bool fresh = true;      // no merge yet (the list is empty)
   float v_own = NINF;     // its M-th value once it holds M keys
   int wpos = 0;           // candidates in the region (wave-uniform)
   const int kMergeTrig = M < 16 ? 2 * M : 48;
@@ -844,7 +849,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
     if (km) v_own = key_value(km);
   };
   auto merge_now = [&]() {
-    wave_merge(region, wpos, list, tail, c);
+    wave_merge(region, wpos, list, fresh, tail, c);
     wpos = 0;
     after_merge();
   };
@@ -949,13 +954,15 @@ __global__ __launch_bounds__(kScanThreads) void scan_wave_kernel(
   }
 
   // ---- the four wave lists meet: the segment's M best, the rest to the tail
+  // (waves 0 and 2 merge the pairs side by side, wave 2's result ascending;
+  // wave 0 merges the two)
   wl[w][lane] = list;
   __syncthreads();
   const size_t cidx = (size_t)row * g.nchunks + seg;
+  if ((w & 1) == 0) wl[w][lane] = sel::merge_halves(wl[w][lane], wl[w + 1][63 - lane], w == 0, tail, c);
+  __syncthreads();
   if (w == 0) {
-    const uint64_t a = sel::merge_halves(wl[0][lane], wl[1][63 - lane], true, tail, c);
-    const uint64_t b2 = sel::merge_halves(wl[2][lane], wl[3][63 - lane], false, tail, c);
-    uint64_t f = sel::merge_halves(a, b2, true, tail, c);
+    uint64_t f = sel::merge_halves(wl[0][lane], wl[2][lane], true, tail, c);
     if (lane >= M) {
       if (f) sel::tail_add1(tail, key_value(f), c);
       f = 0ull;
