@@ -704,7 +704,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_chunk_kernel(
 // A wave merges once 48 candidates have gathered (fewer merges than at 32,
 // with the bound from two batches rising early enough).  The region holds
 // (index, value bits) pairs; the keys are formed in the merge.
-// The four wave lists meet once, at the end of the segment.  A wave whose
+// The four wave lists meet once, at the end of the segment (two pairs side by
+// side, then the two results).  A wave whose
 // candidates overflow its region re-reads the batch and merges as it goes;
 // a first batch without a finite bound (mostly -inf or padding) takes every
 // element in range as a candidate that way.
