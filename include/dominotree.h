@@ -45,7 +45,10 @@
  * 32 <= d_h <= 1024 with d_h % 32 == 0; 1 <= d_e <= 8192; 1 <= V < 2^31;
  * the per-row merge buffer, about 22 * ceil(V / 10240) * M + 20 * M bytes,
  * must fit 96 KiB (DT_ERR_UNSUPPORTED otherwise); the expansion kernel's LDS
- * must fit the device (both checked by dt_plan_create and dt_scan_topm).
+ * layout must fit the device at some number of workgroups per tree (the plan
+ * takes the largest that fits; on a 160 KiB device only d_h 864, 928 and 992
+ * with M >= 128 fit at none).  Both are checked by dt_plan_create, the first
+ * also by dt_scan_topm.
  */
 #ifndef DOMINOTREE_H
 #define DOMINOTREE_H
